@@ -1,0 +1,219 @@
+"""CPU oracle for the fused BitLinear forward (arXiv 2406.02528).
+
+TEST INFRASTRUCTURE ONLY: the test-suite, ``__graft_entry__.smoke()`` and the
+CPU-baseline leg of ``bench.py`` may import this package; the product package
+``paper_2406_02528_amd`` never does, and this package never imports it.
+
+The arithmetic lives in ``oracle.c`` (plain C, built with gcc into
+``liboracle.so``); this module only marshals numpy arrays into it.  Each
+wrapper names the passage of the paper it follows:
+
+* :func:`weight_quant`   -- Algorithm 1, ``weight_quant`` (absmean ternarisation)
+* :func:`pack`, :func:`unpack` -- the library's 2-bit storage format
+* :func:`rms_norm`       -- the RMSNorm equation of the Loihi-methods section
+  (mean of squares, eps = 1e-6, learned scale)
+* :func:`act_quant`      -- Algorithm 1, ``activation_quant`` (per-token absmax)
+* :func:`ternary_accumulate` -- Sec. "MatMul-free Dense Layers with Ternary
+  Weights" (add where t = +1, subtract where t = -1, skip where t = 0)
+* :func:`dequant`        -- Algorithm 1 (fake-quant form: integer sum times
+  1/s_a times 1/s_w)
+* :func:`bitlinear_fwd`  -- the composition, Algorithm 1 ``forward_pass`` with
+  bias 0
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+EPS = 1e-6  # RMSNorm epsilon stated next to the RMSNorm equation
+
+_lib = None
+
+
+def build(force: bool = True) -> str:
+    """Compile ``oracle.c`` into ``liboracle.so`` with gcc (plain -O2, OpenMP,
+    no fast-math, no FMA contraction)."""
+    if force or not os.path.exists(_LIB):
+        tmp = _LIB + ".tmp"
+        cmd = ["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-fopenmp",
+               "-fno-fast-math", "-ffp-contract=off", "-Wall", "-Wextra",
+               _SRC, "-o", tmp, "-lm"]
+        subprocess.run(cmd, check=True)
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        build(force=True)
+    lib = ctypes.CDLL(_LIB)
+    P = ctypes.c_void_p
+    I64 = ctypes.c_int64
+    lib.oracle_num_threads.restype = ctypes.c_int
+    lib.oracle_set_num_threads.argtypes = [ctypes.c_int]
+    lib.oracle_weight_quant.argtypes = [P, I64, I64, P, P]
+    lib.oracle_weight_quant.restype = ctypes.c_int
+    lib.oracle_pack.argtypes = [P, I64, I64, P]
+    lib.oracle_pack.restype = ctypes.c_int
+    lib.oracle_unpack.argtypes = [P, I64, I64, P]
+    lib.oracle_unpack.restype = I64
+    lib.oracle_rms_norm.argtypes = [P, P, I64, I64, ctypes.c_double, P, P]
+    lib.oracle_act_quant.argtypes = [P, I64, I64, P, P]
+    lib.oracle_ternary_accumulate.argtypes = [P, P, I64, I64, I64, P]
+    lib.oracle_ternary_accumulate.restype = ctypes.c_int
+    lib.oracle_ternary_accumulate_pairs.argtypes = [P, P, I64, P, P, I64, P]
+    lib.oracle_ternary_accumulate_pairs.restype = ctypes.c_int
+    lib.oracle_dequant.argtypes = [P, P, ctypes.c_float, I64, I64, P]
+    lib.oracle_bitlinear_fwd.argtypes = [P, P, P, ctypes.c_float, I64, I64, I64,
+                                         ctypes.c_double, P, P, P, P, P]
+    lib.oracle_bitlinear_fwd.restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def _c(a: np.ndarray, dtype) -> np.ndarray:
+    return np.ascontiguousarray(a, dtype=dtype)
+
+
+def _p(a: np.ndarray):
+    return ctypes.c_void_p(a.ctypes.data)
+
+
+def num_threads() -> int:
+    return int(_load().oracle_num_threads())
+
+
+def set_num_threads(n: int) -> None:
+    _load().oracle_set_num_threads(int(n))
+
+
+def weight_quant(W: np.ndarray):
+    """Absmean ternarisation (Algorithm 1 ``weight_quant``).
+
+    W: float32 [N][K] latent weights.  Returns (t int8 [N][K] in {-1,0,1},
+    w_scale float = max(mean|W|, 1e-5), the dequantisation multiplier).
+    """
+    W = _c(W, np.float32)
+    N, K = W.shape
+    t = np.empty((N, K), np.int8)
+    ws = np.zeros(1, np.float32)
+    _load().oracle_weight_quant(_p(W), N, K, _p(t), _p(ws))
+    return t, float(ws[0])
+
+
+def pack(t: np.ndarray) -> np.ndarray:
+    """Pack ternary codes t [N][K] into uint32 [K/16][N] (the library format)."""
+    t = _c(t, np.int8)
+    N, K = t.shape
+    if K % 16:
+        raise ValueError("K must be a multiple of 16")
+    out = np.empty((K // 16, N), np.uint32)
+    if _load().oracle_pack(_p(t), N, K, _p(out)) != 0:
+        raise ValueError("codes outside {-1,0,1}")
+    return out
+
+
+def unpack(Wp: np.ndarray, N: int, K: int):
+    """Decode uint32 [K/16][N] into t int8 [N][K].  Returns (t, n_invalid)."""
+    Wp = _c(Wp, np.uint32)
+    if Wp.shape != (K // 16, N) or K % 16:
+        raise ValueError("bad packed shape")
+    t = np.empty((N, K), np.int8)
+    bad = _load().oracle_unpack(_p(Wp), N, K, _p(t))
+    return t, int(bad)
+
+
+def rms_norm(x: np.ndarray, gamma: np.ndarray | None, eps: float = EPS):
+    """RMSNorm with the mean of squares; returns (y float32 [M][K], r float32 [M])."""
+    x = _c(x, np.float32)
+    M, K = x.shape
+    g = None if gamma is None else _c(gamma, np.float32)
+    y = np.empty((M, K), np.float32)
+    r = np.empty(M, np.float32)
+    _load().oracle_rms_norm(_p(x), None if g is None else _p(g), M, K,
+                            float(eps), _p(y), _p(r))
+    return y, r
+
+
+def act_quant(y: np.ndarray):
+    """Per-token absmax int8 quantisation; returns (q int8 [M][K], a_scale f32 [M])."""
+    y = _c(y, np.float32)
+    M, K = y.shape
+    q = np.empty((M, K), np.int8)
+    a = np.empty(M, np.float32)
+    _load().oracle_act_quant(_p(y), M, K, _p(q), _p(a))
+    return q, a
+
+
+def rmsnorm_act_quant(x: np.ndarray, gamma: np.ndarray | None, eps: float = EPS):
+    """RMSNorm followed by activation quantisation (the fused prologue)."""
+    y, _ = rms_norm(x, gamma, eps)
+    return act_quant(y)
+
+
+def ternary_accumulate(q: np.ndarray, t: np.ndarray) -> np.ndarray:
+    """acc int32 [M][N] = add q where t = +1, subtract where t = -1."""
+    q = _c(q, np.int8)
+    t = _c(t, np.int8)
+    M, K = q.shape
+    N, K2 = t.shape
+    if K != K2:
+        raise ValueError("K mismatch")
+    acc = np.empty((M, N), np.int32)
+    if _load().oracle_ternary_accumulate(_p(q), _p(t), M, K, N, _p(acc)) != 0:
+        raise OverflowError("ternary sum outside int32 or code outside {-1,0,1}")
+    return acc
+
+
+def ternary_accumulate_pairs(q: np.ndarray, t: np.ndarray, ms, ns) -> np.ndarray:
+    """acc for the listed (m, n) pairs only."""
+    q = _c(q, np.int8)
+    t = _c(t, np.int8)
+    ms = _c(ms, np.int64)
+    ns = _c(ns, np.int64)
+    K = q.shape[1]
+    out = np.empty(len(ms), np.int32)
+    if _load().oracle_ternary_accumulate_pairs(_p(q), _p(t), K, _p(ms), _p(ns),
+                                               len(ms), _p(out)) != 0:
+        raise OverflowError("ternary sum outside int32 or code outside {-1,0,1}")
+    return out
+
+
+def dequant(acc: np.ndarray, a_scale: np.ndarray, w_scale: float) -> np.ndarray:
+    acc = _c(acc, np.int32)
+    a_scale = _c(a_scale, np.float32)
+    M, N = acc.shape
+    y = np.empty((M, N), np.float32)
+    _load().oracle_dequant(_p(acc), _p(a_scale), ctypes.c_float(w_scale), M, N, _p(y))
+    return y
+
+
+def bitlinear_fwd(x: np.ndarray, gamma: np.ndarray | None, t: np.ndarray,
+                  w_scale: float, eps: float = EPS):
+    """Whole forward; returns dict with y, q, a_scale, acc."""
+    x = _c(x, np.float32)
+    t = _c(t, np.int8)
+    M, K = x.shape
+    N = t.shape[0]
+    g = None if gamma is None else _c(gamma, np.float32)
+    ybuf = np.empty((M, K), np.float32)
+    q = np.empty((M, K), np.int8)
+    a = np.empty(M, np.float32)
+    acc = np.empty((M, N), np.int32)
+    y = np.empty((M, N), np.float32)
+    st = _load().oracle_bitlinear_fwd(_p(x), None if g is None else _p(g), _p(t),
+                                      ctypes.c_float(w_scale), M, K, N, float(eps),
+                                      _p(ybuf), _p(q), _p(a), _p(acc), _p(y))
+    if st != 0:
+        raise OverflowError("ternary sum outside int32")
+    return {"y": y, "q": q, "a_scale": a, "acc": acc}

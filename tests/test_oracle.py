@@ -1,0 +1,305 @@
+"""Pins for the CPU oracle: hand-worked examples, closed forms, invariants and a
+second formulation of the ternary sum.  None of these re-runs the oracle's own
+formula; each would fail on a dropped term, a wrong sign or index, a
+transposed operand or the wrong rounding mode.  CPU only."""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "hand_examples.json")
+
+
+@pytest.fixture(scope="module")
+def golden():
+    with open(GOLDEN) as f:
+        return json.load(f)
+
+
+# --------------------------------------------------------------------------
+# hand-worked examples
+# --------------------------------------------------------------------------
+
+def test_hand_act_quant(golden):
+    ex = golden["act_quant_1"]
+    x = np.array([ex["x"]], np.float32)
+    q, a = oracle.rmsnorm_act_quant(x, None)
+    assert q[0].tolist() == ex["q"]
+    _, r = oracle.rms_norm(x, None)
+    assert math.isclose(float(r[0]), 1 / math.sqrt(ex["mean_square"] + 1e-6), rel_tol=1e-6)
+    assert math.isclose(float(a[0]), 7 / (127 * math.sqrt(13.15625 + 1e-6)), rel_tol=1e-6)
+
+
+def test_hand_act_quant_gamma(golden):
+    ex = golden["act_quant_gamma"]
+    x = np.array([ex["x"]], np.float32)
+    g = np.array(ex["gamma"], np.float32)
+    q, a = oracle.rmsnorm_act_quant(x, g)
+    assert q[0].tolist() == ex["q"]
+    assert math.isclose(float(a[0]), 1.6 / (127 * math.sqrt(1 + 1e-6)), rel_tol=1e-6)
+
+
+def test_hand_round_half_even(golden):
+    ex = golden["act_quant_ties"]
+    q, a = oracle.act_quant(np.array([ex["y"]], np.float32))
+    assert q[0].tolist() == ex["q"]
+    assert float(a[0]) == ex["a_scale"]
+    ex = golden["weight_quant_ties"]
+    t, ws = oracle.weight_quant(np.array(ex["W"], np.float32))
+    assert t.tolist() == ex["t"]
+    assert ws == ex["w_scale"]
+
+
+def test_hand_weight_quant(golden):
+    ex = golden["weight_quant_1"]
+    t, ws = oracle.weight_quant(np.array(ex["W"], np.float32))
+    assert t.tolist() == ex["t"]
+    assert math.isclose(ws, ex["w_scale"], rel_tol=1e-6)
+
+
+def test_hand_accumulate(golden):
+    q = np.array([golden["act_quant_1"]["q"]], np.int8)
+    t = np.array(golden["weight_quant_1"]["t"], np.int8)
+    acc = oracle.ternary_accumulate(q, t)
+    assert acc[0].tolist() == golden["accumulate_1"]["acc"]
+
+
+def test_hand_pack(golden):
+    t = np.array(golden["weight_quant_1"]["t"], np.int8)
+    words = oracle.pack(t)
+    assert words.shape == (1, 2)
+    assert [f"0x{int(w):08X}" for w in words[0]] == golden["pack_1"]["words"]
+    for case in golden["pack_fixed_words"]["cases"]:
+        w = oracle.pack(np.array([case["t"]], np.int8))
+        assert f"0x{int(w[0, 0]):08X}" == case["word"]
+
+
+# --------------------------------------------------------------------------
+# weight quantisation
+# --------------------------------------------------------------------------
+
+def test_ternary_values_and_gaussian_zero_fraction():
+    # For W ~ N(0, s^2), mean|W| = s sqrt(2/pi) and t = 0 iff |W| < mean/2, so
+    # P(t = 0) = 2 Phi(sqrt(2/pi)/2) - 1 = erf(1 / (2 sqrt(pi))).
+    w = workloads.WORKLOADS["tiny"]
+    W = workloads.make_w(w)
+    t, ws = oracle.weight_quant(W)
+    assert set(np.unique(t).tolist()) <= {-1, 0, 1}
+    p0 = math.erf(1 / (2 * math.sqrt(math.pi)))
+    assert abs(p0 - 0.3101) < 1e-4
+    sd = math.sqrt(p0 * (1 - p0) / t.size)
+    assert abs((t == 0).mean() - p0) < 5 * sd
+    # mean|N(0, 0.02^2)| = 0.02 sqrt(2/pi)
+    assert abs(ws - 0.02 * math.sqrt(2 / math.pi)) < 5 * 0.02 * 0.6 / math.sqrt(t.size)
+    # symmetric: +1 and -1 equally likely
+    sd1 = math.sqrt(0.345 * 0.655 / t.size)
+    assert abs((t == 1).mean() - (t == -1).mean()) < 7 * sd1
+
+
+def test_weight_quant_power_of_two_invariance():
+    rs = np.random.default_rng(1)
+    W = (rs.standard_normal((33, 48)) * 0.02).astype(np.float32)
+    t, ws = oracle.weight_quant(W)
+    for e in (-3, 1, 4):
+        t2, ws2 = oracle.weight_quant(W * np.float32(2.0 ** e))
+        assert np.array_equal(t, t2)
+        assert ws2 == np.float32(ws * 2.0 ** e)
+
+
+def test_weight_quant_zero_tensor():
+    t, ws = oracle.weight_quant(np.zeros((4, 16), np.float32))
+    assert not t.any()
+    assert ws == np.float32(1e-5)
+
+
+def test_weight_quant_is_per_tensor():
+    # scaling one row changes the codes of the other rows through the shared mean
+    W = np.full((2, 16), 0.3, np.float32)
+    W[0] = 1.0
+    t, ws = oracle.weight_quant(W)
+    assert math.isclose(ws, 0.65, rel_tol=1e-6)
+    assert t[0].tolist() == [1] * 16 and t[1].tolist() == [0] * 16
+
+
+# --------------------------------------------------------------------------
+# packing
+# --------------------------------------------------------------------------
+
+def test_pack_roundtrip_and_invalid_code():
+    rs = np.random.default_rng(2)
+    t = rs.integers(-1, 2, size=(37, 64)).astype(np.int8)
+    p = oracle.pack(t)
+    assert p.shape == (4, 37)
+    t2, bad = oracle.unpack(p, 37, 64)
+    assert bad == 0 and np.array_equal(t, t2)
+    p[1, 5] |= np.uint32(3 << 6)  # bits 6-7 of word j=1 hold k = 16*1 + 4*3 + 0
+    t3, bad = oracle.unpack(p, 37, 64)
+    assert bad == 1 and t3[5, 16 + 12] == 0
+
+
+# --------------------------------------------------------------------------
+# RMSNorm + activation quantisation
+# --------------------------------------------------------------------------
+
+def test_act_quant_range_and_row_max():
+    rs = np.random.default_rng(3)
+    x = rs.standard_normal((64, 320)).astype(np.float32)
+    x[5] *= 1e-3
+    x[7, 11] = 300.0
+    g = rs.uniform(0.5, 1.5, 320).astype(np.float32)
+    q, a = oracle.rmsnorm_act_quant(x, g)
+    assert np.abs(q.astype(int)).max() <= 127
+    assert (np.abs(q.astype(int)).max(axis=1) == 127).all()
+    assert (q.min() >= -127)
+
+
+def test_zero_row():
+    x = np.zeros((2, 64), np.float32)
+    x[1, 3] = 1.0
+    q, a = oracle.rmsnorm_act_quant(x, None)
+    assert not q[0].any()
+    assert a[0] == np.float32(np.float32(1e-5) / np.float32(127.0))
+
+
+@pytest.mark.parametrize("c", [3.0, -0.25, 1e-3])
+def test_constant_row_closed_form(c):
+    # x = c * ones, gamma = 1: mean square = c^2, so max|y| = |c| / sqrt(c^2 + eps)
+    # and every q_k = 127 sign(c).  With c = 1e-3, eps = 1e-6 is as large as
+    # c^2, so this also pins where eps sits and that the mean (not the sum) of
+    # squares is used (K = 256).
+    K = 256
+    x = np.full((1, K), c, np.float32)
+    q, a = oracle.rmsnorm_act_quant(x, None)
+    assert (q == 127 * int(np.sign(c))).all()
+    expect = abs(c) / (127 * math.sqrt(c * c + 1e-6))
+    assert math.isclose(float(a[0]), expect, rel_tol=2e-6)
+
+
+def test_one_hot_row():
+    x = np.zeros((1, 128), np.float32)
+    x[0, 17] = -4.5
+    q, a = oracle.rmsnorm_act_quant(x, None)
+    e = np.zeros(128, int)
+    e[17] = -127
+    assert np.array_equal(q[0].astype(int), e)
+    # mean square = 4.5^2 / 128
+    assert math.isclose(float(a[0]), 4.5 / (127 * math.sqrt(4.5 ** 2 / 128 + 1e-6)), rel_tol=2e-6)
+
+
+def test_rmsnorm_scale_invariance_of_q():
+    # in exact arithmetic q does not depend on r; fp32 rounding may move at
+    # most a tie by one step
+    rs = np.random.default_rng(4)
+    x = rs.standard_normal((16, 256)).astype(np.float32)
+    q1, _ = oracle.rmsnorm_act_quant(x, None)
+    q2, _ = oracle.rmsnorm_act_quant(x * np.float32(3.0), None)
+    d = np.abs(q1.astype(int) - q2.astype(int))
+    assert d.max() <= 1 and (d > 0).mean() < 1e-2
+
+
+def test_permutation_changes_q_by_at_most_one_lsb():
+    rs = np.random.default_rng(5)
+    x = rs.standard_normal((8, 512)).astype(np.float32)
+    g = rs.uniform(0.5, 1.5, 512).astype(np.float32)
+    perm = rs.permutation(512)
+    q1, _ = oracle.rmsnorm_act_quant(x, g)
+    q2, _ = oracle.rmsnorm_act_quant(x[:, perm], g[perm])
+    d = np.abs(q1[:, perm].astype(int) - q2.astype(int))
+    assert d.max() <= 1
+
+
+# --------------------------------------------------------------------------
+# ternary accumulation: a second formulation (integer matrix product)
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("M,K,N", [(1, 16, 1), (1, 64, 17), (17, 48, 1), (5, 32, 9), (17, 64, 17)])
+def test_accumulate_vs_integer_matmul(M, K, N):
+    rs = np.random.default_rng(M * 1000 + K * 10 + N)
+    q = rs.integers(-128, 128, size=(M, K)).astype(np.int8)
+    t = rs.integers(-1, 2, size=(N, K)).astype(np.int8)
+    acc = oracle.ternary_accumulate(q, t)
+    ref = q.astype(np.int64) @ t.astype(np.int64).T  # multiply-add form
+    assert np.array_equal(acc, ref)
+
+
+def test_accumulate_special_weights():
+    rs = np.random.default_rng(6)
+    K = 64
+    q = rs.integers(-127, 128, size=(3, K)).astype(np.int8)
+    eye = np.eye(K, dtype=np.int8)
+    assert np.array_equal(oracle.ternary_accumulate(q, eye), q.astype(np.int32))
+    ones = np.ones((2, K), np.int8)
+    s = q.astype(np.int64).sum(axis=1)
+    assert np.array_equal(oracle.ternary_accumulate(q, ones), np.stack([s, s], 1))
+    assert np.array_equal(oracle.ternary_accumulate(q, -ones), -np.stack([s, s], 1))
+    assert not oracle.ternary_accumulate(q, np.zeros((2, K), np.int8)).any()
+
+
+def test_accumulate_negation_linearity_bound():
+    rs = np.random.default_rng(7)
+    K = 96
+    q1 = rs.integers(-60, 61, size=(4, K)).astype(np.int8)
+    q2 = rs.integers(-60, 61, size=(4, K)).astype(np.int8)
+    t = rs.integers(-1, 2, size=(11, K)).astype(np.int8)
+    a1 = oracle.ternary_accumulate(q1, t)
+    assert np.array_equal(oracle.ternary_accumulate(q1, -t), -a1)
+    assert np.array_equal(oracle.ternary_accumulate((q1 + q2).astype(np.int8), t),
+                          a1 + oracle.ternary_accumulate(q2, t))
+    qmax = np.full((1, K), 127, np.int8)
+    assert oracle.ternary_accumulate(qmax, np.ones((1, K), np.int8))[0, 0] == 127 * K
+
+
+def test_accumulate_pairs_matches_full():
+    rs = np.random.default_rng(8)
+    q = rs.integers(-127, 128, size=(9, 80)).astype(np.int8)
+    t = rs.integers(-1, 2, size=(13, 80)).astype(np.int8)
+    full = oracle.ternary_accumulate(q, t)
+    ms = rs.integers(0, 9, 50)
+    ns = rs.integers(0, 13, 50)
+    assert np.array_equal(oracle.ternary_accumulate_pairs(q, t, ms, ns), full[ms, ns])
+
+
+# --------------------------------------------------------------------------
+# dequantisation and the whole forward
+# --------------------------------------------------------------------------
+
+def test_fake_quant_equivalence():
+    # Algorithm 1 returns fake-quantised operands round(sX)/s and round(sW)/s;
+    # their fp64 product summed over k must equal the integer sum times the
+    # two scales.  The fake-quant side recomputes s_a = 127/max|y| in fp64
+    # from the normalised activations, so it differs from the stored fp32
+    # a_scale by at most one fp32 rounding.
+    rs = np.random.default_rng(9)
+    x = rs.standard_normal((6, 128)).astype(np.float32)
+    g = rs.uniform(0.5, 1.5, 128).astype(np.float32)
+    W = (rs.standard_normal((10, 128)) * 0.02).astype(np.float32)
+    t, ws = oracle.weight_quant(W)
+    out = oracle.bitlinear_fwd(x, g, t, ws)
+    y_norm, _ = oracle.rms_norm(x, g)
+    inv_sa = np.abs(y_norm.astype(np.float64)).max(axis=1) / 127.0
+    x_fq = out["q"].astype(np.float64) * inv_sa[:, None]
+    w_fq = t.astype(np.float64) * ws
+    o = x_fq @ w_fq.T
+    rel = np.abs(out["y"] - o) / np.maximum(np.abs(o), 1e-30)
+    assert rel[o != 0].max() < 3e-7
+    assert (out["y"][o == 0] == 0).all()
+
+
+def test_forward_negated_weights_and_zero_row():
+    rs = np.random.default_rng(10)
+    x = rs.standard_normal((5, 64)).astype(np.float32)
+    x[2] = 0.0
+    t = rs.integers(-1, 2, size=(7, 64)).astype(np.int8)
+    a = oracle.bitlinear_fwd(x, None, t, 0.02)
+    b = oracle.bitlinear_fwd(x, None, -t, 0.02)
+    assert np.array_equal(a["y"], -b["y"])
+    assert not a["y"][2].any()
+
+
+def test_oracle_threads_reported():
+    assert oracle.num_threads() >= 1
