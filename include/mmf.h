@@ -1,0 +1,188 @@
+/*
+ * mmf.h -- C ABI of the MI355X (gfx950) fused BitLinear library.
+ *
+ * The library computes the forward pass of the BitLinear layer of "Scalable
+ * MatMul-free Language Modeling" (arXiv 2406.02528): RMSNorm of each token,
+ * per-token absmax int8 quantisation, ternary accumulation against weights in
+ * {-1, 0, +1} with int32 sums, and dequantisation by the activation and weight
+ * scales (Algorithm 1, "Fused RMSNorm and BitLinear Algorithm with
+ * Quantization", forward_pass with bias 0; Sec. "MatMul-free Dense Layers with
+ * Ternary Weights" for the ternary sum).
+ *
+ * Conventions for every entry point
+ *  - Array arguments are DEVICE pointers on the current HIP device, owned by
+ *    the caller; the library keeps no pointer after a call returns.
+ *  - Work is enqueued on `stream` (NULL = the null stream) and is
+ *    asynchronous: results are valid once the stream has been synchronised.
+ *    No entry point synchronises the device.
+ *  - Arguments are checked on the host before anything is enqueued; on any
+ *    error nothing is enqueued and no output is touched.
+ *  - Every pointer to an array must be 16-byte aligned (MMF_ERR_ALIGN).
+ *  - K (in-features) must be a positive multiple of 16 and at most 2^20
+ *    (MMF_ERR_SHAPE); M (tokens) and N (out-features) may be any value in
+ *    [0, 2^31 - 1]; M == 0 or N == 0 is a successful no-op.
+ *  - Outputs must not alias inputs.
+ *  - Calls on different streams may run concurrently.
+ *  - Return value: an mmf_status code.
+ *
+ * Shapes and layouts (row-major, sizes in elements)
+ *  - x        [M][K]  activations, bfloat16 (uint16 bit patterns) or float32
+ *                     for the _f32 variants.
+ *  - gamma    [K]     float32 RMSNorm scale; NULL means all ones.
+ *  - W        [N][K]  float32 latent weights (out x in).
+ *  - Wpacked  [K/16][N] uint32 ternary weights, 2 bits each (see below).
+ *  - w_scale  [1]     float32 weight dequantisation multiplier, mean|W|.
+ *  - q        [M][K]  int8 quantised activations.
+ *  - a_scale  [M]     float32 per-token dequantisation multiplier, absmax/127.
+ *  - q_rowsum [M]     int32 sum over k of q[m][k].
+ *  - y        [M][N]  float32 output.
+ *
+ * Packed weight format.  Word (j, n) = Wpacked[j * N + n] holds the ternary
+ * weights t[n][16j .. 16j + 15].  For k = 16j + 4i + b (i, b in 0..3) the code
+ * c = t + 1 in {0, 1, 2} sits in bits 8b + 2i and 8b + 2i + 1, so that
+ * (word >> 2i) & 0x03030303 holds the codes of k = 16j + 4i .. 16j + 4i + 3 in
+ * byte order.  A word of zero weights is 0x55555555.  Code 3 never appears in
+ * what mmf_ternarize_weights writes; a word containing it gives an
+ * unspecified (memory-safe) result.
+ */
+#ifndef MMF_H
+#define MMF_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes. */
+#define MMF_OK 0
+#define MMF_ERR_NULL 1      /* a required pointer is NULL                      */
+#define MMF_ERR_SHAPE 2     /* a size is out of range (K % 16, K == 0, ...)    */
+#define MMF_ERR_ALIGN 3     /* an array pointer is not 16-byte aligned         */
+#define MMF_ERR_WORKSPACE 4 /* the caller's workspace is too small             */
+#define MMF_ERR_HIP 5       /* a HIP runtime call or a kernel launch failed    */
+#define MMF_ERR_ARG 6       /* another argument is invalid (e.g. path value)   */
+
+/* Human-readable name of a status code (static storage; never NULL). */
+const char *mmf_status_string(int status);
+
+/* Library ABI version, incremented on any incompatible change. */
+int mmf_version(void);
+
+/* Bytes of the packed weight array for N out-features and K in-features,
+ * (K / 16) * N * 4.  Returns 0 for invalid shapes. */
+size_t mmf_packed_weight_bytes(int64_t N, int64_t K);
+
+/*
+ * Weight ternarisation and packing (Algorithm 1, weight_quant; offline, once
+ * per weight tensor).
+ *   w_scale = max(mean over all N*K entries of |W|, 1e-5), the mean summed in
+ *             fp64 and rounded to fp32;
+ *   t[n][k] = clamp(round_half_even(W[n][k] * (1 / w_scale)), -1, 1), the
+ *             reciprocal and product in fp32;
+ * written to Wpacked in the format above and to w_scale[0].
+ * W: [N][K] float32 in; Wpacked: [K/16][N] uint32 out; w_scale: 1 float out.
+ * Allocates a small stream-ordered scratch buffer (hipMallocAsync).
+ */
+int mmf_ternarize_weights(const float *W, int64_t N, int64_t K,
+                          uint32_t *Wpacked, float *w_scale, hipStream_t stream);
+
+/*
+ * Fused RMSNorm + per-token absmax int8 quantisation (Algorithm 1,
+ * rms_norm_fwd and activation_quant; RMSNorm with the mean of squares,
+ * eps = 1e-6, learned scale gamma, as in the RMSNorm equation of the
+ * Loihi-methods section).  For each token m:
+ *   r        = fp32(1 / sqrt(sum_k x^2 / K + 1e-6))      (sum and root in fp64)
+ *   y_k      = (x_k * r) * gamma_k                         (fp32)
+ *   a        = max(max_k |y_k|, 1e-5)
+ *   q_k      = clamp(round_half_even(y_k * (127 / a)), -128, 127)
+ *   a_scale  = a / 127,   q_rowsum = sum_k q_k.
+ * x: [M][K] bf16 bits; gamma: [K] or NULL; q: [M][K] out; a_scale: [M] out;
+ * q_rowsum: [M] out (may be NULL).
+ */
+int mmf_act_quant(const uint16_t *x, const float *gamma, int8_t *q,
+                  float *a_scale, int32_t *q_rowsum, int64_t M, int64_t K,
+                  hipStream_t stream);
+/* The same for float32 activations. */
+int mmf_act_quant_f32(const float *x, const float *gamma, int8_t *q,
+                      float *a_scale, int32_t *q_rowsum, int64_t M, int64_t K,
+                      hipStream_t stream);
+
+/*
+ * The fused BitLinear forward (Algorithm 1, forward_pass, bias 0):
+ *   y[m][n] = a_scale[m] * w_scale * sum_k q[m][k] t[n][k]
+ * with q, a_scale from the act-quant step above and t from Wpacked.  The
+ * integer sum is exact; the product is fp32 (a_scale[m] * w_scale first).
+ * Tokens M <= 8 take the decode kernel (VALU dot products), larger M the
+ * int8 MFMA kernel.  Allocates its M*K + 8*M byte scratch stream-ordered
+ * (hipMallocAsync); mmf_bitlinear_fwd_ws takes caller scratch instead.
+ * x: [M][K] bf16 bits; gamma: [K] or NULL; Wpacked: [K/16][N]; w_scale: [1];
+ * y: [M][N] float32 out.
+ */
+int mmf_bitlinear_fwd(const uint16_t *x, const float *gamma,
+                      const uint32_t *Wpacked, const float *w_scale, float *y,
+                      int64_t M, int64_t K, int64_t N, hipStream_t stream);
+/* The same for float32 activations. */
+int mmf_bitlinear_fwd_f32(const float *x, const float *gamma,
+                          const uint32_t *Wpacked, const float *w_scale,
+                          float *y, int64_t M, int64_t K, int64_t N,
+                          hipStream_t stream);
+
+/* Bytes of caller scratch the _ws variants need for M tokens of K features. */
+size_t mmf_bitlinear_workspace_bytes(int64_t M, int64_t K);
+
+/* mmf_bitlinear_fwd with caller-provided scratch `workspace` of
+ * `workspace_bytes` bytes (device memory, 256-byte aligned, at least
+ * mmf_bitlinear_workspace_bytes(M, K); MMF_ERR_WORKSPACE otherwise).  The
+ * scratch must not be used by other work on another stream meanwhile.
+ * x_is_f32 selects float32 (1) or bf16 (0) activations. */
+int mmf_bitlinear_fwd_ws(const void *x, int x_is_f32, const float *gamma,
+                         const uint32_t *Wpacked, const float *w_scale,
+                         float *y, int64_t M, int64_t K, int64_t N,
+                         void *workspace, size_t workspace_bytes,
+                         hipStream_t stream);
+
+/*
+ * Ternary accumulation and dequantisation from already-quantised activations
+ * (the contraction stage of the forward on its own; Sec. "MatMul-free Dense
+ * Layers with Ternary Weights" and Algorithm 1):
+ *   y[m][n] = (q_rowsum-corrected int32 sum_k q[m][k] t[n][k]) * (a_scale[m] * w_scale)
+ * q: [M][K]; a_scale: [M]; q_rowsum: [M] = sum_k q[m][k] (as written by
+ * mmf_act_quant; a wrong value shifts every output of that row);
+ * Wpacked: [K/16][N]; w_scale: [1]; y: [M][N] out.  Allocates nothing.
+ */
+int mmf_ternary_gemm_dequant(const int8_t *q, const float *a_scale,
+                             const int32_t *q_rowsum, const uint32_t *Wpacked,
+                             const float *w_scale, float *y, int64_t M,
+                             int64_t K, int64_t N, hipStream_t stream);
+
+/*
+ * Raw ternary accumulation, acc[m][n] = sum_{k: t=+1} q[m][k] -
+ * sum_{k: t=-1} q[m][k], exact int32 (Sec. "MatMul-free Dense Layers with
+ * Ternary Weights").  Runs the same contraction kernels as the forward, with
+ * an integer epilogue.  q: [M][K]; Wpacked: [K/16][N]; acc: [M][N] int32 out.
+ * Allocates a 4*M byte stream-ordered scratch buffer (hipMallocAsync).
+ */
+int mmf_ternary_gemm_i32(const int8_t *q, const uint32_t *Wpacked,
+                         int32_t *acc, int64_t M, int64_t K, int64_t N,
+                         hipStream_t stream);
+
+/*
+ * Kernel selection for the contraction: MMF_PATH_AUTO (decode kernel for
+ * M <= 8, MFMA kernel otherwise), MMF_PATH_GEMV or MMF_PATH_GEMM force one
+ * kernel for every M (the decode kernel handles at most 8 tokens per launch
+ * and is launched once per 8-token slice when forced).  Process-wide; returns
+ * the previous setting, or -MMF_ERR_ARG for an unknown value.
+ */
+#define MMF_PATH_AUTO 0
+#define MMF_PATH_GEMV 1
+#define MMF_PATH_GEMM 2
+int mmf_set_path(int path);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MMF_H */

@@ -1,0 +1,234 @@
+"""MI355X (gfx950) fused BitLinear: Python binding of ``libmmf.so``.
+
+The forward pass of the BitLinear layer of "Scalable MatMul-free Language
+Modeling" (arXiv 2406.02528; Algorithm 1 with bias 0): RMSNorm, per-token
+absmax int8 quantisation, ternary accumulation with int32 sums and
+dequantisation.  Every step runs in the HIP kernels of ``libmmf.so``; this
+module only checks tensor shapes, dtypes and devices and passes raw pointers
+and the current HIP stream through the C ABI declared in ``include/mmf.h``.
+PyTorch is used for device memory and streams only.
+
+Functions carry the names of the C entry points.  There is no fallback: if
+the library is not built, importing this package raises ``ImportError``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libmmf.so")
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(
+        f"{LIB_PATH} is missing: build it with `python -c 'import __graft_entry__ as g; g.build()'` "
+        "(hipcc --offload-arch=gfx950); there is no CPU fallback")
+
+_lib = ctypes.CDLL(LIB_PATH)
+
+MMF_OK = 0
+MMF_PATH_AUTO, MMF_PATH_GEMV, MMF_PATH_GEMM = 0, 1, 2
+
+_P = ctypes.c_void_p
+_I64 = ctypes.c_int64
+_SZ = ctypes.c_size_t
+
+_SIGNATURES = {
+    "mmf_status_string": ([ctypes.c_int], ctypes.c_char_p),
+    "mmf_version": ([], ctypes.c_int),
+    "mmf_packed_weight_bytes": ([_I64, _I64], _SZ),
+    "mmf_ternarize_weights": ([_P, _I64, _I64, _P, _P, _P], ctypes.c_int),
+    "mmf_act_quant": ([_P, _P, _P, _P, _P, _I64, _I64, _P], ctypes.c_int),
+    "mmf_act_quant_f32": ([_P, _P, _P, _P, _P, _I64, _I64, _P], ctypes.c_int),
+    "mmf_bitlinear_fwd": ([_P, _P, _P, _P, _P, _I64, _I64, _I64, _P], ctypes.c_int),
+    "mmf_bitlinear_fwd_f32": ([_P, _P, _P, _P, _P, _I64, _I64, _I64, _P], ctypes.c_int),
+    "mmf_bitlinear_workspace_bytes": ([_I64, _I64], _SZ),
+    "mmf_bitlinear_fwd_ws": ([_P, ctypes.c_int, _P, _P, _P, _P, _I64, _I64, _I64, _P, _SZ, _P],
+                             ctypes.c_int),
+    "mmf_ternary_gemm_dequant": ([_P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _P], ctypes.c_int),
+    "mmf_ternary_gemm_i32": ([_P, _P, _P, _I64, _I64, _I64, _P], ctypes.c_int),
+    "mmf_set_path": ([ctypes.c_int], ctypes.c_int),
+}
+for _name, (_args, _res) in _SIGNATURES.items():
+    _f = getattr(_lib, _name)
+    _f.argtypes = _args
+    _f.restype = _res
+
+
+class MMFError(RuntimeError):
+    pass
+
+
+def _check(status: int) -> None:
+    if status != MMF_OK:
+        raise MMFError(_lib.mmf_status_string(status).decode())
+
+
+def _stream(stream) -> ctypes.c_void_p:
+    if stream is None:
+        return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    if isinstance(stream, torch.cuda.Stream):
+        return ctypes.c_void_p(stream.cuda_stream)
+    return ctypes.c_void_p(int(stream))
+
+
+def _ptr(t: torch.Tensor | None) -> ctypes.c_void_p:
+    return ctypes.c_void_p(0 if t is None else t.data_ptr())
+
+
+def _need(t: torch.Tensor, name: str, dtype, shape) -> None:
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be on a HIP device")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def _x_kind(x: torch.Tensor) -> bool:
+    """True for float32 activations, False for bfloat16."""
+    if x.dtype == torch.float32:
+        return True
+    if x.dtype == torch.bfloat16:
+        return False
+    raise TypeError(f"x must be bfloat16 or float32, got {x.dtype}")
+
+
+def mmf_version() -> int:
+    return int(_lib.mmf_version())
+
+
+def mmf_status_string(status: int) -> str:
+    return _lib.mmf_status_string(int(status)).decode()
+
+
+def mmf_packed_weight_bytes(N: int, K: int) -> int:
+    return int(_lib.mmf_packed_weight_bytes(N, K))
+
+
+def mmf_set_path(path: int) -> int:
+    prev = int(_lib.mmf_set_path(int(path)))
+    if prev < 0:
+        raise ValueError(f"unknown path {path}")
+    return prev
+
+
+def mmf_ternarize_weights(W: torch.Tensor, Wpacked: torch.Tensor, w_scale: torch.Tensor,
+                          stream=None) -> None:
+    """W float32 [N][K] -> Wpacked int32 [K/16][N] (uint32 bit patterns), w_scale float32 [1]."""
+    N, K = W.shape
+    _need(W, "W", torch.float32, (N, K))
+    _need(Wpacked, "Wpacked", torch.int32, (K // 16, N))
+    _need(w_scale, "w_scale", torch.float32, (1,))
+    _check(_lib.mmf_ternarize_weights(_ptr(W), N, K, _ptr(Wpacked), _ptr(w_scale), _stream(stream)))
+
+
+def mmf_act_quant(x: torch.Tensor, gamma: torch.Tensor | None, q: torch.Tensor,
+                  a_scale: torch.Tensor, q_rowsum: torch.Tensor | None = None,
+                  stream=None) -> None:
+    """x bf16/f32 [M][K], gamma f32 [K] or None -> q int8 [M][K], a_scale f32 [M], q_rowsum i32 [M]."""
+    M, K = x.shape
+    is_f32 = _x_kind(x)
+    _need(x, "x", x.dtype, (M, K))
+    if gamma is not None:
+        _need(gamma, "gamma", torch.float32, (K,))
+    _need(q, "q", torch.int8, (M, K))
+    _need(a_scale, "a_scale", torch.float32, (M,))
+    if q_rowsum is not None:
+        _need(q_rowsum, "q_rowsum", torch.int32, (M,))
+    fn = _lib.mmf_act_quant_f32 if is_f32 else _lib.mmf_act_quant
+    _check(fn(_ptr(x), _ptr(gamma), _ptr(q), _ptr(a_scale), _ptr(q_rowsum), M, K, _stream(stream)))
+
+
+def mmf_bitlinear_fwd(x: torch.Tensor, gamma: torch.Tensor | None, Wpacked: torch.Tensor,
+                      w_scale: torch.Tensor, y: torch.Tensor, stream=None) -> None:
+    """The fused forward: y f32 [M][N] from x bf16/f32 [M][K] and packed weights [K/16][N]."""
+    M, K = x.shape
+    N = Wpacked.shape[1]
+    is_f32 = _x_kind(x)
+    _need(x, "x", x.dtype, (M, K))
+    if gamma is not None:
+        _need(gamma, "gamma", torch.float32, (K,))
+    _need(Wpacked, "Wpacked", torch.int32, (K // 16, N))
+    _need(w_scale, "w_scale", torch.float32, (1,))
+    _need(y, "y", torch.float32, (M, N))
+    fn = _lib.mmf_bitlinear_fwd_f32 if is_f32 else _lib.mmf_bitlinear_fwd
+    _check(fn(_ptr(x), _ptr(gamma), _ptr(Wpacked), _ptr(w_scale), _ptr(y), M, K, N,
+              _stream(stream)))
+
+
+def mmf_bitlinear_workspace_bytes(M: int, K: int) -> int:
+    return int(_lib.mmf_bitlinear_workspace_bytes(M, K))
+
+
+def mmf_bitlinear_fwd_ws(x: torch.Tensor, gamma: torch.Tensor | None, Wpacked: torch.Tensor,
+                         w_scale: torch.Tensor, y: torch.Tensor, workspace: torch.Tensor,
+                         stream=None) -> None:
+    """The fused forward with caller scratch (a uint8 device tensor)."""
+    M, K = x.shape
+    N = Wpacked.shape[1]
+    is_f32 = _x_kind(x)
+    _need(x, "x", x.dtype, (M, K))
+    if gamma is not None:
+        _need(gamma, "gamma", torch.float32, (K,))
+    _need(Wpacked, "Wpacked", torch.int32, (K // 16, N))
+    _need(w_scale, "w_scale", torch.float32, (1,))
+    _need(y, "y", torch.float32, (M, N))
+    _need(workspace, "workspace", torch.uint8, (workspace.numel(),))
+    _check(_lib.mmf_bitlinear_fwd_ws(_ptr(x), int(is_f32), _ptr(gamma), _ptr(Wpacked),
+                                     _ptr(w_scale), _ptr(y), M, K, N, _ptr(workspace),
+                                     workspace.numel(), _stream(stream)))
+
+
+def mmf_ternary_gemm_dequant(q: torch.Tensor, a_scale: torch.Tensor, q_rowsum: torch.Tensor,
+                             Wpacked: torch.Tensor, w_scale: torch.Tensor, y: torch.Tensor,
+                             stream=None) -> None:
+    """Contraction + dequant from quantised activations (the forward after act-quant)."""
+    M, K = q.shape
+    N = Wpacked.shape[1]
+    _need(q, "q", torch.int8, (M, K))
+    _need(a_scale, "a_scale", torch.float32, (M,))
+    _need(q_rowsum, "q_rowsum", torch.int32, (M,))
+    _need(Wpacked, "Wpacked", torch.int32, (K // 16, N))
+    _need(w_scale, "w_scale", torch.float32, (1,))
+    _need(y, "y", torch.float32, (M, N))
+    _check(_lib.mmf_ternary_gemm_dequant(_ptr(q), _ptr(a_scale), _ptr(q_rowsum), _ptr(Wpacked),
+                                         _ptr(w_scale), _ptr(y), M, K, N, _stream(stream)))
+
+
+def mmf_ternary_gemm_i32(q: torch.Tensor, Wpacked: torch.Tensor, acc: torch.Tensor,
+                         stream=None) -> None:
+    """Raw int32 ternary sums acc [M][N] from q int8 [M][K] and packed weights."""
+    M, K = q.shape
+    N = Wpacked.shape[1]
+    _need(q, "q", torch.int8, (M, K))
+    _need(Wpacked, "Wpacked", torch.int32, (K // 16, N))
+    _need(acc, "acc", torch.int32, (M, N))
+    _check(_lib.mmf_ternary_gemm_i32(_ptr(q), _ptr(Wpacked), _ptr(acc), M, K, N, _stream(stream)))
+
+
+# ---------------------------------------------------------------------------
+# allocating conveniences (outputs allocated with torch on the inputs' device)
+# ---------------------------------------------------------------------------
+
+def ternarize(W: torch.Tensor, stream=None):
+    """Returns (Wpacked int32 [K/16][N], w_scale float32 [1])."""
+    N, K = W.shape
+    Wp = torch.empty((K // 16, N), dtype=torch.int32, device=W.device)
+    ws = torch.empty((1,), dtype=torch.float32, device=W.device)
+    mmf_ternarize_weights(W, Wp, ws, stream)
+    return Wp, ws
+
+
+def bitlinear(x: torch.Tensor, gamma: torch.Tensor | None, Wpacked: torch.Tensor,
+              w_scale: torch.Tensor, stream=None) -> torch.Tensor:
+    """Returns y float32 [M][N]."""
+    y = torch.empty((x.shape[0], Wpacked.shape[1]), dtype=torch.float32, device=x.device)
+    mmf_bitlinear_fwd(x, gamma, Wpacked, w_scale, y, stream)
+    return y

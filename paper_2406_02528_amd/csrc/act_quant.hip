@@ -1,0 +1,220 @@
+// Fused RMSNorm + per-token absmax int8 quantisation (Algorithm 1,
+// rms_norm_fwd + activation_quant; RMSNorm with the mean of squares and
+// eps = 1e-6, learned scale gamma).  One wave64 per token row; the row is read
+// from HBM once and kept in registers while the two row statistics (sum of
+// squares, then absmax of the normalised values) are reduced across the wave.
+#include "mmf_device.h"
+#include "mmf_launch.h"
+
+namespace mmf {
+namespace {
+
+constexpr int kRowsPerBlock = 4;  // 4 waves, one row each
+constexpr float kEps = 1e-6f;
+
+// 16-byte vector of activations: 8 bf16 or 4 fp32.
+template <typename XT> struct Vec;
+template <> struct Vec<uint16_t> {
+  static constexpr int kElems = 8;
+  using Raw = uint4;
+  __device__ static void to_f32(const Raw& r, float* f) {
+    const uint32_t w[4] = {r.x, r.y, r.z, r.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      f[2 * i] = __uint_as_float(w[i] << 16);
+      f[2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
+    }
+  }
+};
+template <> struct Vec<float> {
+  static constexpr int kElems = 4;
+  using Raw = float4;
+  __device__ static void to_f32(const Raw& r, float* f) {
+    f[0] = r.x; f[1] = r.y; f[2] = r.z; f[3] = r.w;
+  }
+};
+
+template <int E>
+__device__ __forceinline__ void store_q(int8_t* dst, const int* qi);
+template <>
+__device__ __forceinline__ void store_q<8>(int8_t* dst, const int* qi) {
+  uint2 v;
+  v.x = (qi[0] & 0xFF) | ((qi[1] & 0xFF) << 8) | ((qi[2] & 0xFF) << 16) | ((uint32_t)qi[3] << 24);
+  v.y = (qi[4] & 0xFF) | ((qi[5] & 0xFF) << 8) | ((qi[6] & 0xFF) << 16) | ((uint32_t)qi[7] << 24);
+  *reinterpret_cast<uint2*>(dst) = v;
+}
+template <>
+__device__ __forceinline__ void store_q<4>(int8_t* dst, const int* qi) {
+  uint32_t v = (qi[0] & 0xFF) | ((qi[1] & 0xFF) << 8) | ((qi[2] & 0xFF) << 16) | ((uint32_t)qi[3] << 24);
+  *reinterpret_cast<uint32_t*>(dst) = v;
+}
+
+__device__ __forceinline__ int quantise(float y, float s) {
+  float v = __builtin_rintf(y * s);  // round half to even
+  v = fminf(fmaxf(v, -128.0f), 127.0f);
+  return static_cast<int>(v);
+}
+
+__device__ __forceinline__ float row_rstd(double ss, int K) {
+  double ms = ss / static_cast<double>(K);
+  return static_cast<float>(1.0 / sqrt(ms + static_cast<double>(kEps)));
+}
+
+// VPL > 0: each lane keeps up to VPL 16-byte vectors of its row in registers
+// (rows of at most 64 * VPL vectors).  VPL == 0: any K; the row is re-read
+// from memory (L2) for each of the three passes.
+template <typename XT, int VPL>
+__global__ __launch_bounds__(256) void act_quant_kernel(
+    const XT* __restrict__ x, const float* __restrict__ gamma,
+    int8_t* __restrict__ q, float* __restrict__ a_scale,
+    int32_t* __restrict__ q_rowsum, int64_t M, int K) {
+  using V = Vec<XT>;
+  constexpr int E = V::kElems;
+  const int lane = threadIdx.x & 63;
+  const int64_t row = static_cast<int64_t>(blockIdx.x) * kRowsPerBlock + (threadIdx.x >> 6);
+  if (row >= M) return;  // whole wave leaves together
+  const int nvec = K / E;
+  const typename V::Raw* xr = reinterpret_cast<const typename V::Raw*>(x + row * K);
+  int8_t* qr = q + row * K;
+
+  if constexpr (VPL > 0) {
+    float xf[VPL][E];
+    double ss = 0.0;
+#pragma unroll
+    for (int i = 0; i < VPL; ++i) {
+      const int v = lane + kWave * i;
+      if (v < nvec) {
+        V::to_f32(xr[v], xf[i]);
+      } else {
+#pragma unroll
+        for (int e = 0; e < E; ++e) xf[i][e] = 0.0f;
+      }
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        const double d = static_cast<double>(xf[i][e]);
+        ss += d * d;  // exact product of an fp32 value in fp64
+      }
+    }
+    ss = wave_sum_f64(ss);
+    const float r = row_rstd(ss, K);
+
+    float amax = 0.0f;
+#pragma unroll
+    for (int i = 0; i < VPL; ++i) {
+      const int v = lane + kWave * i;
+      if (v < nvec) {
+        if (gamma != nullptr) {
+          const float* g = gamma + v * E;
+#pragma unroll
+          for (int e = 0; e < E; ++e) xf[i][e] = (xf[i][e] * r) * g[e];
+        } else {
+#pragma unroll
+          for (int e = 0; e < E; ++e) xf[i][e] = xf[i][e] * r;
+        }
+#pragma unroll
+        for (int e = 0; e < E; ++e) amax = fmaxf(amax, fabsf(xf[i][e]));
+      }
+    }
+    amax = fmaxf(wave_max_f32(amax), 1e-5f);
+    const float s = 127.0f / amax;
+
+    int rs = 0;
+#pragma unroll
+    for (int i = 0; i < VPL; ++i) {
+      const int v = lane + kWave * i;
+      if (v < nvec) {
+        int qi[E];
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          qi[e] = quantise(xf[i][e], s);
+          rs += qi[e];
+        }
+        store_q<E>(qr + v * E, qi);
+      }
+    }
+    rs = wave_sum_i32(rs);
+    if (lane == 0) {
+      a_scale[row] = amax / 127.0f;
+      if (q_rowsum != nullptr) q_rowsum[row] = rs;
+    }
+  } else {
+    // pass 1: sum of squares
+    double ss = 0.0;
+    for (int v = lane; v < nvec; v += kWave) {
+      float f[E];
+      V::to_f32(xr[v], f);
+#pragma unroll
+      for (int e = 0; e < E; ++e) ss += static_cast<double>(f[e]) * static_cast<double>(f[e]);
+    }
+    ss = wave_sum_f64(ss);
+    const float r = row_rstd(ss, K);
+    // pass 2: absmax of the normalised row
+    float amax = 0.0f;
+    for (int v = lane; v < nvec; v += kWave) {
+      float f[E];
+      V::to_f32(xr[v], f);
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        float y = f[e] * r;
+        if (gamma != nullptr) y = y * gamma[v * E + e];
+        amax = fmaxf(amax, fabsf(y));
+      }
+    }
+    amax = fmaxf(wave_max_f32(amax), 1e-5f);
+    const float s = 127.0f / amax;
+    // pass 3: quantise
+    int rs = 0;
+    for (int v = lane; v < nvec; v += kWave) {
+      float f[E];
+      V::to_f32(xr[v], f);
+      int qi[E];
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        float y = f[e] * r;
+        if (gamma != nullptr) y = y * gamma[v * E + e];
+        qi[e] = quantise(y, s);
+        rs += qi[e];
+      }
+      store_q<E>(qr + v * E, qi);
+    }
+    rs = wave_sum_i32(rs);
+    if (lane == 0) {
+      a_scale[row] = amax / 127.0f;
+      if (q_rowsum != nullptr) q_rowsum[row] = rs;
+    }
+  }
+}
+
+template <typename XT>
+hipError_t launch_typed(const XT* x, const float* gamma, int8_t* q, float* a_scale,
+                        int32_t* q_rowsum, int64_t M, int K, hipStream_t stream) {
+  constexpr int E = Vec<XT>::kElems;
+  const int nvec = K / E;
+  const int vpl = (nvec + kWave - 1) / kWave;
+  const dim3 grid(static_cast<unsigned>((M + kRowsPerBlock - 1) / kRowsPerBlock));
+  const dim3 block(kWave * kRowsPerBlock);
+#define MMF_AQ_LAUNCH(V)                                                          \
+  hipLaunchKernelGGL((act_quant_kernel<XT, V>), grid, block, 0, stream, x, gamma, \
+                     q, a_scale, q_rowsum, M, K)
+  if (vpl <= 1) MMF_AQ_LAUNCH(1);
+  else if (vpl <= 2) MMF_AQ_LAUNCH(2);
+  else if (vpl <= 4) MMF_AQ_LAUNCH(4);
+  else if (vpl <= 8) MMF_AQ_LAUNCH(8);
+  else if (vpl <= 12) MMF_AQ_LAUNCH(12);
+  else MMF_AQ_LAUNCH(0);
+#undef MMF_AQ_LAUNCH
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_act_quant(const void* x, bool x_is_f32, const float* gamma, int8_t* q,
+                            float* a_scale, int32_t* q_rowsum, int64_t M, int K,
+                            hipStream_t stream) {
+  if (M == 0) return hipSuccess;
+  if (x_is_f32)
+    return launch_typed(static_cast<const float*>(x), gamma, q, a_scale, q_rowsum, M, K, stream);
+  return launch_typed(static_cast<const uint16_t*>(x), gamma, q, a_scale, q_rowsum, M, K, stream);
+}
+
+}  // namespace mmf

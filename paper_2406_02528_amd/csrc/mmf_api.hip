@@ -1,0 +1,234 @@
+// C ABI of the fused BitLinear library: argument checks on the host, scratch
+// management and kernel dispatch.  Nothing is enqueued before every argument
+// has been checked.
+#include <atomic>
+#include <cstdint>
+#include <cstring>
+
+#include "../../include/mmf.h"
+#include "mmf_launch.h"
+
+namespace {
+
+constexpr int64_t kMaxK = int64_t(1) << 20;
+constexpr int64_t kMaxMN = 0x7FFFFFFF;
+constexpr int kDecodeMaxTokens = 8;
+constexpr size_t kScratchAlign = 256;
+
+std::atomic<int> g_path{MMF_PATH_AUTO};
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+// Shape rules shared by every entry point that takes K.
+int check_shape(int64_t M, int64_t K, int64_t N) {
+  if (K <= 0 || K > kMaxK || (K % 16) != 0) return MMF_ERR_SHAPE;
+  if (M < 0 || M > kMaxMN || N < 0 || N > kMaxMN) return MMF_ERR_SHAPE;
+  return MMF_OK;
+}
+
+int hip_status(hipError_t e) { return e == hipSuccess ? MMF_OK : MMF_ERR_HIP; }
+
+// Layout of the forward's scratch: q [M][K] int8, a_scale [M] f32, rowsum [M] i32.
+struct FwdScratch {
+  size_t q_off, a_off, r_off, total;
+};
+FwdScratch fwd_scratch(int64_t M, int64_t K) {
+  FwdScratch s;
+  s.q_off = 0;
+  s.a_off = round_up(static_cast<size_t>(M) * static_cast<size_t>(K), kScratchAlign);
+  s.r_off = s.a_off + round_up(static_cast<size_t>(M) * 4, kScratchAlign);
+  s.total = s.r_off + round_up(static_cast<size_t>(M) * 4, kScratchAlign);
+  return s;
+}
+
+bool use_gemv(int64_t M) {
+  const int p = g_path.load(std::memory_order_relaxed);
+  if (p == MMF_PATH_GEMV) return true;
+  if (p == MMF_PATH_GEMM) return false;
+  return M <= kDecodeMaxTokens;
+}
+
+hipError_t contract(const mmf::ContractArgs& a, hipStream_t stream) {
+  return use_gemv(a.M) ? mmf::launch_gemv(a, stream) : mmf::launch_gemm(a, stream);
+}
+
+// Checks of the forward's arguments shared by the allocating and _ws forms.
+int check_fwd(const void* x, const float* gamma, const uint32_t* Wpacked, const float* w_scale,
+              const float* y, int64_t M, int64_t K, int64_t N) {
+  if (int st = check_shape(M, K, N)) return st;
+  if (M == 0 || N == 0) return MMF_OK;
+  if (!x || !Wpacked || !w_scale || !y) return MMF_ERR_NULL;
+  if (!aligned16(x) || !aligned16(Wpacked) || !aligned16(y) || (gamma && !aligned16(gamma)))
+    return MMF_ERR_ALIGN;
+  return MMF_OK;
+}
+
+int run_fwd(const void* x, bool x_is_f32, const float* gamma, const uint32_t* Wpacked,
+            const float* w_scale, float* y, int64_t M, int64_t K, int64_t N, char* scratch,
+            hipStream_t stream) {
+  const FwdScratch s = fwd_scratch(M, K);
+  int8_t* q = reinterpret_cast<int8_t*>(scratch + s.q_off);
+  float* a_scale = reinterpret_cast<float*>(scratch + s.a_off);
+  int32_t* rowsum = reinterpret_cast<int32_t*>(scratch + s.r_off);
+  hipError_t e = mmf::launch_act_quant(x, x_is_f32, gamma, q, a_scale, rowsum, M,
+                                       static_cast<int>(K), stream);
+  if (e != hipSuccess) return MMF_ERR_HIP;
+  mmf::ContractArgs a{q, a_scale, rowsum, Wpacked, w_scale, y, M, static_cast<int>(K), N,
+                      mmf::Epilogue::kDequantF32};
+  return hip_status(contract(a, stream));
+}
+
+int fwd_alloc(const void* x, bool x_is_f32, const float* gamma, const uint32_t* Wpacked,
+              const float* w_scale, float* y, int64_t M, int64_t K, int64_t N,
+              hipStream_t stream) {
+  if (int st = check_fwd(x, gamma, Wpacked, w_scale, y, M, K, N)) return st;
+  if (M == 0 || N == 0) return MMF_OK;
+  const FwdScratch s = fwd_scratch(M, K);
+  void* scratch = nullptr;
+  if (hipMallocAsync(&scratch, s.total, stream) != hipSuccess) return MMF_ERR_HIP;
+  const int st = run_fwd(x, x_is_f32, gamma, Wpacked, w_scale, y, M, K, N,
+                         static_cast<char*>(scratch), stream);
+  const hipError_t fe = hipFreeAsync(scratch, stream);
+  if (st != MMF_OK) return st;
+  return hip_status(fe);
+}
+
+int act_quant_common(const void* x, bool x_is_f32, const float* gamma, int8_t* q,
+                     float* a_scale, int32_t* q_rowsum, int64_t M, int64_t K,
+                     hipStream_t stream) {
+  if (int st = check_shape(M, K, 0)) return st;
+  if (M == 0) return MMF_OK;
+  if (!x || !q || !a_scale) return MMF_ERR_NULL;
+  if (!aligned16(x) || !aligned16(q) || !aligned16(a_scale) || (gamma && !aligned16(gamma)) ||
+      (q_rowsum && !aligned16(q_rowsum)))
+    return MMF_ERR_ALIGN;
+  return hip_status(mmf::launch_act_quant(x, x_is_f32, gamma, q, a_scale, q_rowsum, M,
+                                          static_cast<int>(K), stream));
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* mmf_status_string(int status) {
+  switch (status) {
+    case MMF_OK: return "MMF_OK";
+    case MMF_ERR_NULL: return "MMF_ERR_NULL: a required pointer is NULL";
+    case MMF_ERR_SHAPE: return "MMF_ERR_SHAPE: size out of range (K must be a positive multiple of 16, at most 2^20; M, N in [0, 2^31-1])";
+    case MMF_ERR_ALIGN: return "MMF_ERR_ALIGN: an array pointer is not 16-byte aligned";
+    case MMF_ERR_WORKSPACE: return "MMF_ERR_WORKSPACE: workspace too small or misaligned";
+    case MMF_ERR_HIP: return "MMF_ERR_HIP: a HIP runtime call or kernel launch failed";
+    case MMF_ERR_ARG: return "MMF_ERR_ARG: invalid argument";
+    default: return "MMF: unknown status";
+  }
+}
+
+int mmf_version(void) { return 1; }
+
+size_t mmf_packed_weight_bytes(int64_t N, int64_t K) {
+  if (check_shape(0, K, N) != MMF_OK) return 0;
+  return static_cast<size_t>(K / 16) * static_cast<size_t>(N) * 4u;
+}
+
+int mmf_ternarize_weights(const float* W, int64_t N, int64_t K, uint32_t* Wpacked,
+                          float* w_scale, hipStream_t stream) {
+  if (int st = check_shape(0, K, N)) return st;
+  if (N == 0) return MMF_OK;
+  if (!W || !Wpacked || !w_scale) return MMF_ERR_NULL;
+  if (!aligned16(W) || !aligned16(Wpacked)) return MMF_ERR_ALIGN;
+  const int n_part = mmf::ternarize_partials_count(N * K);
+  void* partials = nullptr;
+  if (hipMallocAsync(&partials, sizeof(double) * n_part, stream) != hipSuccess) return MMF_ERR_HIP;
+  const hipError_t e = mmf::launch_ternarize(W, N, static_cast<int>(K), Wpacked, w_scale,
+                                             static_cast<double*>(partials), stream);
+  const hipError_t fe = hipFreeAsync(partials, stream);
+  if (e != hipSuccess) return MMF_ERR_HIP;
+  return hip_status(fe);
+}
+
+int mmf_act_quant(const uint16_t* x, const float* gamma, int8_t* q, float* a_scale,
+                  int32_t* q_rowsum, int64_t M, int64_t K, hipStream_t stream) {
+  return act_quant_common(x, false, gamma, q, a_scale, q_rowsum, M, K, stream);
+}
+
+int mmf_act_quant_f32(const float* x, const float* gamma, int8_t* q, float* a_scale,
+                      int32_t* q_rowsum, int64_t M, int64_t K, hipStream_t stream) {
+  return act_quant_common(x, true, gamma, q, a_scale, q_rowsum, M, K, stream);
+}
+
+int mmf_bitlinear_fwd(const uint16_t* x, const float* gamma, const uint32_t* Wpacked,
+                      const float* w_scale, float* y, int64_t M, int64_t K, int64_t N,
+                      hipStream_t stream) {
+  return fwd_alloc(x, false, gamma, Wpacked, w_scale, y, M, K, N, stream);
+}
+
+int mmf_bitlinear_fwd_f32(const float* x, const float* gamma, const uint32_t* Wpacked,
+                          const float* w_scale, float* y, int64_t M, int64_t K, int64_t N,
+                          hipStream_t stream) {
+  return fwd_alloc(x, true, gamma, Wpacked, w_scale, y, M, K, N, stream);
+}
+
+size_t mmf_bitlinear_workspace_bytes(int64_t M, int64_t K) {
+  if (check_shape(M, K, 0) != MMF_OK) return 0;
+  return fwd_scratch(M, K).total;
+}
+
+int mmf_bitlinear_fwd_ws(const void* x, int x_is_f32, const float* gamma,
+                         const uint32_t* Wpacked, const float* w_scale, float* y, int64_t M,
+                         int64_t K, int64_t N, void* workspace, size_t workspace_bytes,
+                         hipStream_t stream) {
+  if (x_is_f32 != 0 && x_is_f32 != 1) return MMF_ERR_ARG;
+  if (int st = check_fwd(x, gamma, Wpacked, w_scale, y, M, K, N)) return st;
+  if (M == 0 || N == 0) return MMF_OK;
+  if (!workspace) return MMF_ERR_NULL;
+  if ((reinterpret_cast<uintptr_t>(workspace) & (kScratchAlign - 1)) != 0 ||
+      workspace_bytes < fwd_scratch(M, K).total)
+    return MMF_ERR_WORKSPACE;
+  return run_fwd(x, x_is_f32 == 1, gamma, Wpacked, w_scale, y, M, K, N,
+                 static_cast<char*>(workspace), stream);
+}
+
+int mmf_ternary_gemm_dequant(const int8_t* q, const float* a_scale, const int32_t* q_rowsum,
+                             const uint32_t* Wpacked, const float* w_scale, float* y, int64_t M,
+                             int64_t K, int64_t N, hipStream_t stream) {
+  if (int st = check_shape(M, K, N)) return st;
+  if (M == 0 || N == 0) return MMF_OK;
+  if (!q || !a_scale || !q_rowsum || !Wpacked || !w_scale || !y) return MMF_ERR_NULL;
+  if (!aligned16(q) || !aligned16(a_scale) || !aligned16(q_rowsum) || !aligned16(Wpacked) ||
+      !aligned16(y))
+    return MMF_ERR_ALIGN;
+  mmf::ContractArgs a{q, a_scale, q_rowsum, Wpacked, w_scale, y, M, static_cast<int>(K), N,
+                      mmf::Epilogue::kDequantF32};
+  return hip_status(contract(a, stream));
+}
+
+int mmf_ternary_gemm_i32(const int8_t* q, const uint32_t* Wpacked, int32_t* acc, int64_t M,
+                         int64_t K, int64_t N, hipStream_t stream) {
+  if (int st = check_shape(M, K, N)) return st;
+  if (M == 0 || N == 0) return MMF_OK;
+  if (!q || !Wpacked || !acc) return MMF_ERR_NULL;
+  if (!aligned16(q) || !aligned16(Wpacked) || !aligned16(acc)) return MMF_ERR_ALIGN;
+  void* rowsum = nullptr;
+  if (hipMallocAsync(&rowsum, round_up(static_cast<size_t>(M) * 4, kScratchAlign), stream) !=
+      hipSuccess)
+    return MMF_ERR_HIP;
+  int32_t* rs = static_cast<int32_t*>(rowsum);
+  hipError_t e = mmf::launch_row_sum(q, rs, M, static_cast<int>(K), stream);
+  if (e == hipSuccess) {
+    mmf::ContractArgs a{q, nullptr, rs, Wpacked, nullptr, acc, M, static_cast<int>(K), N,
+                        mmf::Epilogue::kRawI32};
+    e = contract(a, stream);
+  }
+  const hipError_t fe = hipFreeAsync(rowsum, stream);
+  if (e != hipSuccess) return MMF_ERR_HIP;
+  return hip_status(fe);
+}
+
+int mmf_set_path(int path) {
+  if (path != MMF_PATH_AUTO && path != MMF_PATH_GEMV && path != MMF_PATH_GEMM)
+    return -MMF_ERR_ARG;
+  return g_path.exchange(path);
+}
+
+}  // extern "C"

@@ -1,0 +1,45 @@
+// Internal launchers of the gfx950 kernels.  Shapes are validated by the
+// C-ABI layer before any of these is called.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace mmf {
+
+// RMSNorm + absmax int8 quantisation of M rows of K features (K % 16 == 0).
+hipError_t launch_act_quant(const void* x, bool x_is_f32, const float* gamma, int8_t* q,
+                            float* a_scale, int32_t* q_rowsum, int64_t M, int K,
+                            hipStream_t stream);
+
+// q_rowsum[m] = sum_k q[m][k].
+hipError_t launch_row_sum(const int8_t* q, int32_t* q_rowsum, int64_t M, int K,
+                          hipStream_t stream);
+
+// Ternarisation: partial sums of |W| (fp64), finalise w_scale, pack.
+// `partials` must hold ternarize_partials_count(N*K) doubles.
+int ternarize_partials_count(int64_t count);
+hipError_t launch_ternarize(const float* W, int64_t N, int K, uint32_t* Wpacked,
+                            float* w_scale, double* partials, hipStream_t stream);
+
+// Output form of the contraction kernels.
+enum class Epilogue { kDequantF32, kRawI32 };
+
+struct ContractArgs {
+  const int8_t* q;          // [M][K]
+  const float* a_scale;     // [M]   (kDequantF32 only)
+  const int32_t* q_rowsum;  // [M]
+  const uint32_t* Wpacked;  // [K/16][N]
+  const float* w_scale;     // [1]   (kDequantF32 only)
+  void* out;                // [M][N] float or int32
+  int64_t M;
+  int K;
+  int64_t N;
+  Epilogue epilogue;
+};
+
+// Decode kernel: VALU dot products, M <= 8 tokens.
+hipError_t launch_gemv(const ContractArgs& a, hipStream_t stream);
+// Prefill kernel: int8 MFMA, any M.
+hipError_t launch_gemm(const ContractArgs& a, hipStream_t stream);
+
+}  // namespace mmf

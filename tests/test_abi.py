@@ -1,0 +1,144 @@
+"""C-ABI checks that need no GPU: the library loads, exports every function
+that include/mmf.h declares, and its host-side argument checks reject bad
+calls before anything is enqueued (no pointer is dereferenced on these paths,
+so stand-in addresses are used)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "mmf.h")
+
+
+@pytest.fixture(scope="module")
+def mmf():
+    import paper_2406_02528_amd as m
+    return m
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(mmf_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for required in ("mmf_ternarize_weights", "mmf_act_quant", "mmf_bitlinear_fwd",
+                     "mmf_ternary_gemm_i32"):
+        assert required in names
+
+
+def test_library_exports_every_declared_symbol(mmf):
+    lib = ctypes.CDLL(mmf.LIB_PATH)
+    missing = [n for n in declared_functions() if not hasattr(lib, n)]
+    assert not missing, missing
+
+
+def test_status_strings_and_sizes(mmf):
+    assert mmf.mmf_version() >= 1
+    assert mmf.mmf_status_string(0) == "MMF_OK"
+    for s in range(1, 7):
+        assert mmf.mmf_status_string(s).startswith("MMF_ERR")
+    assert "unknown" in mmf.mmf_status_string(99)
+    assert mmf.mmf_packed_weight_bytes(6144, 2048) == 6144 * 2048 // 4
+    assert mmf.mmf_packed_weight_bytes(3, 48) == 3 * 3 * 4
+    assert mmf.mmf_packed_weight_bytes(3, 40) == 0   # K % 16 != 0
+    assert mmf.mmf_packed_weight_bytes(3, 0) == 0
+    ws = mmf.mmf_bitlinear_workspace_bytes(8192, 2048)
+    assert ws >= 8192 * 2048 + 8 * 8192 and ws % 256 == 0
+    assert mmf.mmf_bitlinear_workspace_bytes(1, 17) == 0
+
+
+def test_set_path(mmf):
+    prev = mmf.mmf_set_path(mmf.MMF_PATH_GEMV)
+    assert mmf.mmf_set_path(mmf.MMF_PATH_GEMM) == mmf.MMF_PATH_GEMV
+    assert mmf.mmf_set_path(prev) == mmf.MMF_PATH_GEMM
+    with pytest.raises(ValueError):
+        mmf.mmf_set_path(7)
+
+
+A = 0x10000      # 16-byte aligned stand-in device addresses, never dereferenced
+B = 0x20000
+C = 0x30000
+D = 0x40000
+E = 0x50000
+BAD = 0x10004    # 4-byte aligned only
+S = None         # null stream
+
+
+def _c(mmf):
+    return mmf._lib
+
+
+@pytest.mark.parametrize("K", [0, -16, 8, 24, 2 ** 20 + 16])
+def test_bad_k_is_rejected(mmf, K):
+    lib = _c(mmf)
+    assert lib.mmf_bitlinear_fwd(A, B, C, D, E, 4, K, 4, S) == 2
+    assert lib.mmf_act_quant(A, B, C, D, E, 4, K, S) == 2
+    assert lib.mmf_ternarize_weights(A, 4, K, B, C, S) == 2
+    assert lib.mmf_ternary_gemm_i32(A, B, C, 4, K, 4, S) == 2
+    assert lib.mmf_ternary_gemm_dequant(A, B, C, D, E, A, 4, K, 4, S) == 2
+
+
+def test_bad_m_n_are_rejected(mmf):
+    lib = _c(mmf)
+    assert lib.mmf_bitlinear_fwd(A, B, C, D, E, -1, 16, 4, S) == 2
+    assert lib.mmf_bitlinear_fwd(A, B, C, D, E, 4, 16, 2 ** 31, S) == 2
+    assert lib.mmf_ternarize_weights(A, -5, 16, B, C, S) == 2
+
+
+def test_null_pointers(mmf):
+    lib = _c(mmf)
+    assert lib.mmf_bitlinear_fwd(None, B, C, D, E, 4, 16, 4, S) == 1
+    assert lib.mmf_bitlinear_fwd(A, B, None, D, E, 4, 16, 4, S) == 1
+    assert lib.mmf_bitlinear_fwd(A, B, C, None, E, 4, 16, 4, S) == 1
+    assert lib.mmf_bitlinear_fwd(A, B, C, D, None, 4, 16, 4, S) == 1
+    assert lib.mmf_act_quant(A, None, None, D, E, 4, 16, S) == 1
+    assert lib.mmf_act_quant(A, None, C, None, E, 4, 16, S) == 1
+    assert lib.mmf_ternarize_weights(None, 4, 16, B, C, S) == 1
+    assert lib.mmf_ternarize_weights(A, 4, 16, B, None, S) == 1
+    assert lib.mmf_ternary_gemm_i32(A, None, C, 4, 16, 4, S) == 1
+    assert lib.mmf_ternary_gemm_dequant(A, B, None, D, E, A, 4, 16, 4, S) == 1
+    assert lib.mmf_bitlinear_fwd_ws(A, 0, B, C, D, E, 4, 16, 4, None, 1 << 20, S) == 1
+
+
+def test_misaligned_pointers(mmf):
+    lib = _c(mmf)
+    assert lib.mmf_bitlinear_fwd(BAD, B, C, D, E, 4, 16, 4, S) == 3
+    assert lib.mmf_bitlinear_fwd(A, BAD, C, D, E, 4, 16, 4, S) == 3
+    assert lib.mmf_bitlinear_fwd(A, B, BAD, D, E, 4, 16, 4, S) == 3
+    assert lib.mmf_bitlinear_fwd(A, B, C, D, BAD, 4, 16, 4, S) == 3
+    assert lib.mmf_act_quant(A, B, BAD, D, E, 4, 16, S) == 3
+    assert lib.mmf_ternarize_weights(BAD, 4, 16, B, C, S) == 3
+    assert lib.mmf_ternary_gemm_i32(A, B, BAD, 4, 16, 4, S) == 3
+
+
+def test_workspace_checks(mmf):
+    lib = _c(mmf)
+    need = mmf.mmf_bitlinear_workspace_bytes(4, 16)
+    assert lib.mmf_bitlinear_fwd_ws(A, 0, B, C, D, E, 4, 16, 4, 0x100000, need - 1, S) == 4
+    assert lib.mmf_bitlinear_fwd_ws(A, 0, B, C, D, E, 4, 16, 4, 0x100010, need, S) == 4
+    assert lib.mmf_bitlinear_fwd_ws(A, 2, B, C, D, E, 4, 16, 4, 0x100000, need, S) == 6
+
+
+def test_empty_shapes_are_noops(mmf):
+    # M == 0 or N == 0 returns OK without touching (or even checking) buffers
+    lib = _c(mmf)
+    assert lib.mmf_bitlinear_fwd(None, None, None, None, None, 0, 16, 4, S) == 0
+    assert lib.mmf_bitlinear_fwd(None, None, None, None, None, 4, 16, 0, S) == 0
+    assert lib.mmf_act_quant(None, None, None, None, None, 0, 16, S) == 0
+    assert lib.mmf_ternarize_weights(None, 0, 16, None, None, S) == 0
+    assert lib.mmf_ternary_gemm_i32(None, None, None, 0, 16, 5, S) == 0
+
+
+def test_python_binding_rejects_cpu_tensors(mmf):
+    import torch
+    x = torch.zeros(2, 16, dtype=torch.bfloat16)
+    with pytest.raises(ValueError):
+        mmf.mmf_act_quant(x, None, torch.zeros(2, 16, dtype=torch.int8), torch.zeros(2))
+    with pytest.raises(TypeError):
+        mmf.mmf_act_quant(torch.zeros(2, 16, dtype=torch.float16), None,
+                          torch.zeros(2, 16, dtype=torch.int8), torch.zeros(2))
