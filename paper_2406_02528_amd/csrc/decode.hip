@@ -1,0 +1,512 @@
+// Fused decode forward (M <= 8 tokens): RMSNorm + absmax int8 quantisation +
+// ternary accumulation + dequantisation in one launch.
+//
+// Each workgroup owns C = 64/H output columns over the whole K dimension.
+// Weight layout [K/16][N] words: for a word row j the lanes of a wave read
+// consecutive columns, so each lane owns an output column and accumulates its
+// dot products without cross-lane traffic; H lanes share a column by taking
+// alternate words and the 16 waves split K into ranges.  The int32 partial
+// sums of a column are added in LDS (exact, order-free).
+//
+// Latency is what limits a decode launch, so the loads are ordered with care:
+// memory loads retire in issue order, hence the activation loads (x and gamma,
+// or the pre-quantised q) are issued first, then the packed weight words, and
+// only then does the kernel wait -- for the activations alone -- and
+// normalise/quantise the token rows into LDS while the weights stream in.
+// All of these loads are straight-line (clamped addresses, masked values), so
+// the compiler can keep them in flight together.
+//
+// Per word of 16 weights and per token: four v_dot4_i32_i8 of the codes
+// c = t + 1 against q (one broadcast ds_read_b128); the epilogue subtracts
+// sum_k q, giving the ternary sum of the paper (+q where t = 1, -q where
+// t = -1, nothing where t = 0), and dequantises.
+#include "mmf_device.h"
+#include "mmf_launch.h"
+
+namespace mmf {
+namespace {
+
+constexpr int kWaves = 16;
+constexpr int kThreads = kWaves * kWave;  // 1024
+constexpr int kMaxTokens = 8;
+constexpr int kPrefetch = 24;             // weight words per lane issued ahead
+constexpr int kMaxRowWaves = 4;           // waves that normalise one token row
+constexpr int kMaxQVecs = (kDecodeMaxLdsQ / 16 + kThreads - 1) / kThreads;  // q copy
+constexpr float kEps = 1e-6f;
+constexpr int kGridRound = 256;           // workgroups that run at once (one per CU)
+constexpr bool kEarlyNorm = true;         // row waves reduce x before issuing weight loads
+constexpr bool kXFirst = true;            // every wave waits for that before its weight loads
+
+enum class Src { kBf16, kF32, kQuantised };
+
+// Token rows are normalised and quantised by groups of G = min(16 / P, 4)
+// waves, P = MT rounded up to a power of two; group g owns row g and the
+// remaining waves only stream weights.  At most one wave per SIMD works on a
+// row: the per-row steps (reductions, the fp64 root) are latency chains, and
+// more waves on a SIMD would only serialise the same instructions.  Each
+// thread handles VP 16-byte vectors of its row.
+template <int MT>
+constexpr int row_groups() { return MT <= 1 ? 1 : MT <= 2 ? 2 : MT <= 4 ? 4 : 8; }
+template <int MT>
+constexpr int row_waves() {
+  return kWaves / row_groups<MT>() < kMaxRowWaves ? kWaves / row_groups<MT>() : kMaxRowWaves;
+}
+template <Src S>
+constexpr int vec_elems() { return S == Src::kF32 ? 4 : 8; }
+
+struct Shared {
+  int8_t* q;        // [MT][K]
+  int* red;         // [kMaxTokens][64] column sums (LDS atomics)
+  double* slot_d;   // [kWaves]
+  float* slot_f;    // [kWaves]
+  int* slot_i;      // [kWaves]
+  float* a_scale;   // [kMaxTokens]
+  int* rowsum;      // [kMaxTokens]
+};
+
+__device__ __forceinline__ Shared carve(char* base, int q_bytes) {
+  Shared s;
+  s.q = reinterpret_cast<int8_t*>(base);
+  char* p = base + q_bytes;
+  s.red = reinterpret_cast<int*>(p);
+  p += sizeof(int) * kMaxTokens * kWave;
+  s.slot_d = reinterpret_cast<double*>(p);
+  p += sizeof(double) * kWaves;
+  s.slot_f = reinterpret_cast<float*>(p);
+  p += sizeof(float) * kWaves;
+  s.slot_i = reinterpret_cast<int*>(p);
+  p += sizeof(int) * kWaves;
+  s.a_scale = reinterpret_cast<float*>(p);
+  p += sizeof(float) * kMaxTokens;
+  s.rowsum = reinterpret_cast<int*>(p);
+  return s;
+}
+
+constexpr int kScalarBytes = sizeof(int) * kMaxTokens * kWave +
+                             (sizeof(double) + sizeof(float) + sizeof(int)) * kWaves +
+                             (sizeof(float) + sizeof(int)) * kMaxTokens;
+
+__device__ __forceinline__ int quantise(float y, float s) {
+  float v = __builtin_rintf(y * s);  // round half to even
+  v = fminf(fmaxf(v, -128.0f), 127.0f);
+  return static_cast<int>(v);
+}
+
+__device__ __forceinline__ void unpack_bf16x8(const uint4& r, float* f) {
+  const uint32_t w[4] = {r.x, r.y, r.z, r.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    f[2 * i] = __uint_as_float(w[i] << 16);
+    f[2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
+  }
+}
+
+// Activation staging for the fused path: the raw x and gamma vectors of this
+// thread, loaded up front and left untouched until finish(), so that nothing
+// waits on them before the weight loads have been issued.
+template <int MT, Src S, int VP>
+struct RowStage {
+  static constexpr int E = vec_elems<S>();
+  static constexpr int G = row_waves<MT>();  // waves per row
+  uint4 xr[VP];
+  float4 gr[VP][E / 4];
+  int row, gtid, nvec;
+  bool active;
+
+  __device__ void load(const void* xv, const float* __restrict__ gamma, int K) {
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    row = wave / G;
+    gtid = threadIdx.x - row * G * kWave;
+    active = row < MT;  // waves past MT * G take no part in the row work
+    nvec = K / E;
+    const int srow = active ? row : 0;
+    const uint4* xrow = reinterpret_cast<const uint4*>(
+        static_cast<const char*>(xv) + static_cast<int64_t>(srow) * K * (16 / E));
+#pragma unroll
+    for (int p = 0; p < VP; ++p) {
+      const int v = gtid + G * kWave * p;
+      const int sv = (active && v < nvec) ? v : 0;
+      xr[p] = xrow[sv];
+    }
+    if (gamma != nullptr) {
+#pragma unroll
+      for (int p = 0; p < VP; ++p) {
+        const int v = gtid + G * kWave * p;
+        const int sv = (active && v < nvec) ? v : 0;
+#pragma unroll
+        for (int e4 = 0; e4 < E / 4; ++e4) gr[p][e4] = reinterpret_cast<const float4*>(gamma + sv * E)[e4];
+      }
+    }
+  }
+
+  // values of vector p as fp32 (zero outside the row)
+  __device__ void values(int p, float* f) const {
+    const int v = gtid + G * kWave * p;
+    const bool ok = active && v < nvec;
+    if constexpr (E == 8) {
+      const uint32_t w[4] = {xr[p].x, xr[p].y, xr[p].z, xr[p].w};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        f[2 * i] = ok ? __uint_as_float(w[i] << 16) : 0.0f;
+        f[2 * i + 1] = ok ? __uint_as_float(w[i] & 0xFFFF0000u) : 0.0f;
+      }
+    } else {
+      f[0] = ok ? __uint_as_float(xr[p].x) : 0.0f;
+      f[1] = ok ? __uint_as_float(xr[p].y) : 0.0f;
+      f[2] = ok ? __uint_as_float(xr[p].z) : 0.0f;
+      f[3] = ok ? __uint_as_float(xr[p].w) : 0.0f;
+    }
+  }
+  __device__ float gamma_at(int p, int e) const {
+    const float4 g = gr[p][e / 4];
+    const int k = e % 4;
+    return k == 0 ? g.x : k == 1 ? g.y : k == 2 ? g.z : g.w;
+  }
+
+  // RMSNorm, absmax and quantisation of the staged values into LDS, in two
+  // parts.  begin(): the local sum of squares and its wave reduction (this is
+  // where a row wave first waits for its activations).  finish(): two block
+  // barriers, which every wave reaches, while only the waves of a row group
+  // do the work (`active` is uniform across a wave).  The row sum of q is
+  // left in the per-wave slots.
+  float f[VP][E];
+  __device__ void begin(const Shared& sh) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    if (active) {
+#pragma unroll
+      for (int p = 0; p < VP; ++p) values(p, f[p]);
+      double ss = 0.0;
+#pragma unroll
+      for (int p = 0; p < VP; ++p)
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          const double d = static_cast<double>(f[p][e]);
+          ss += d * d;  // exact square of an fp32 value
+        }
+      ss = wave_sum_f64(ss);
+      if (lane == 0) sh.slot_d[wave] = ss;
+    }
+  }
+
+  __device__ void finish(bool has_gamma, int K, const Shared& sh, bool first_barrier = true) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int w0 = row * G;
+    if (first_barrier) __syncthreads();
+    if (active) {
+      double tot = 0.0;
+      for (int w = 0; w < G; ++w) tot += sh.slot_d[w0 + w];
+      const float r = static_cast<float>(1.0 / sqrt(tot / static_cast<double>(K) + static_cast<double>(kEps)));
+      float amax = 0.0f;
+#pragma unroll
+      for (int p = 0; p < VP; ++p)
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          float y = f[p][e] * r;
+          if (has_gamma) y = y * gamma_at(p, e);
+          f[p][e] = y;  // zero for vectors outside the row
+          amax = fmaxf(amax, fabsf(y));
+        }
+      amax = wave_max_f32(amax);
+      if (lane == 0) sh.slot_f[wave] = amax;
+    }
+    __syncthreads();
+    if (active) {
+      float a = 0.0f;
+      for (int w = 0; w < G; ++w) a = fmaxf(a, sh.slot_f[w0 + w]);
+      a = fmaxf(a, 1e-5f);
+      const float s = 127.0f / a;
+      int rs = 0;
+#pragma unroll
+      for (int p = 0; p < VP; ++p) {
+        const int v = gtid + G * kWave * p;
+        uint32_t packed[E / 4];
+#pragma unroll
+        for (int gq = 0; gq < E / 4; ++gq) {
+          uint32_t word = 0;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int qi = quantise(f[p][4 * gq + e], s);
+            rs += qi;
+            word |= (static_cast<uint32_t>(qi) & 0xFFu) << (8 * e);
+          }
+          packed[gq] = word;
+        }
+        if (v < nvec) {
+          int8_t* dst = sh.q + row * K + v * E;
+          if constexpr (E == 8)
+            *reinterpret_cast<uint2*>(dst) = make_uint2(packed[0], packed[1]);
+          else
+            *reinterpret_cast<uint32_t*>(dst) = packed[0];
+        }
+      }
+      rs = wave_sum_i32(rs);
+      if (lane == 0) sh.slot_i[wave] = rs;
+      if (gtid == 0) sh.a_scale[row] = a / 127.0f;
+    }
+  }
+};
+
+// Pre-quantised activations: q, a_scale and q_rowsum copied to LDS.  Loads and
+// stores are unconditional (threads past the end copy the last vector, or
+// token 0's scalars, writing the same bytes as the thread that owns them), so
+// the loads stay ahead of the weight loads instead of being sunk to their use.
+template <int MT>
+struct QStage {
+  uint4 v[kMaxQVecs];
+  float a;
+  int rs;
+  __device__ void load(const int8_t* __restrict__ q, const float* __restrict__ a_scale,
+                       const int32_t* __restrict__ q_rowsum, int K) {
+    const int last = (MT * K) / 16 - 1;
+#pragma unroll
+    for (int i = 0; i < kMaxQVecs; ++i)
+      v[i] = reinterpret_cast<const uint4*>(q)[min(static_cast<int>(threadIdx.x) + kThreads * i, last)];
+    const int t = threadIdx.x < MT ? threadIdx.x : 0;
+    a = a_scale != nullptr ? a_scale[t] : 0.0f;
+    rs = q_rowsum[t];
+  }
+  __device__ void store(int K, const Shared& sh) const {
+    const int last = (MT * K) / 16 - 1;
+#pragma unroll
+    for (int i = 0; i < kMaxQVecs; ++i)
+      reinterpret_cast<uint4*>(sh.q)[min(static_cast<int>(threadIdx.x) + kThreads * i, last)] = v[i];
+    const int t = threadIdx.x < MT ? threadIdx.x : 0;
+    sh.a_scale[t] = a;
+    sh.rowsum[t] = rs;
+  }
+};
+
+// Weight loads go through a buffer resource (base and size in SGPRs): the
+// load takes the lane's 32-bit offset in a VGPR and the slot's offset in an
+// SGPR, so no vector address arithmetic is spent per slot, and the hardware
+// range check returns 0 past the end of the packed array.
+constexpr int kBufferFlags = 0x00020000;  // gfx9 buffer descriptor word 3
+
+// Kernel arguments in one block, so that the scalar loads that fetch them are
+// issued together at entry.
+struct Params {
+  const uint32_t* Wp;
+  const void* x;
+  const float* gamma;
+  const int8_t* q;
+  const float* a_scale;
+  const int32_t* q_rowsum;
+  const float* w_scale;
+  void* out;
+  int64_t N;
+  int K;
+  int q_bytes;
+};
+
+// The weights of a workgroup's columns are streamed in "slots": wave w owns
+// the word rows [jb, je), both multiples of H (H divides K/16), and slot s of
+// lane (c, h) is word row jb + H s + h.  Whether a slot exists is therefore
+// the same for the whole wave, and its address is a scalar base
+// (Wp + (jb + H s) N) plus a per-lane offset (h N + column) computed once.
+template <int MT, int H, Src S, int VP, Epilogue EP>
+__global__ __launch_bounds__(kThreads) void decode_kernel(const Params prm) {
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  const int K = prm.K;
+  const int64_t N = prm.N;
+  const Shared sh = carve(smem, prm.q_bytes);
+  constexpr int C = kWave / H;  // columns per workgroup
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int c = lane % C, h = lane / C;
+  const int64_t n = static_cast<int64_t>(blockIdx.x) * C + c;
+  const bool col_ok = n < N;
+  const int J = K / 16;
+  const int per_wave = ((J + kWaves * H - 1) / (kWaves * H)) * H;
+  const int jb = min(wave * per_wave, J);
+  const int je = min(jb + per_wave, J);
+  const int ns = (je - jb) / H;  // slots of this wave (uniform)
+  // byte offsets from Wp: packed weights are < 4 GiB
+  const __amdgpu_buffer_rsrc_t wrsrc = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint32_t*>(prm.Wp), 0, static_cast<int>(static_cast<uint32_t>(J) * 4u * static_cast<uint32_t>(N)),
+      kBufferFlags);
+  const uint32_t row_bytes = 4u * static_cast<uint32_t>(N);
+  const uint32_t lane_off = static_cast<uint32_t>(h) * row_bytes +
+                            4u * static_cast<uint32_t>(col_ok ? n : 0);
+  const uint32_t slot_bytes = static_cast<uint32_t>(H) * row_bytes;
+  const uint32_t wave_bytes = static_cast<uint32_t>(jb) * row_bytes;
+
+  // 1. activation loads
+  RowStage<MT, S == Src::kQuantised ? Src::kBf16 : S, VP> rows;
+  QStage<MT> qs;
+  if constexpr (S == Src::kQuantised)
+    qs.load(prm.q, prm.a_scale, prm.q_rowsum, K);
+  else
+    rows.load(prm.x, prm.gamma, K);
+  __builtin_amdgcn_sched_barrier(0);  // keep these loads ahead of the weight loads
+  // The row waves wait for their activations before issuing weight loads:
+  // x then crosses a quiet memory system instead of queueing behind every
+  // CU's weight misses, and the norm below overlaps the weight stream.  The
+  // other waves issue their weight loads at once.
+  if constexpr (kEarlyNorm && S != Src::kQuantised) rows.begin(sh);
+  if constexpr (kXFirst && S != Src::kQuantised) __syncthreads();
+  __builtin_amdgcn_sched_barrier(0);
+
+  // 2. the first weight slots (slots past the wave's range repeat its last
+  //    slot and are not used)
+  uint32_t wbuf[kPrefetch];
+  if (ns > 0) {
+#pragma unroll
+    for (int p = 0; p < kPrefetch; ++p) {
+      const uint32_t sp = static_cast<uint32_t>(p < ns ? p : ns - 1);
+      wbuf[p] = __builtin_amdgcn_raw_buffer_load_b32(wrsrc, lane_off, wave_bytes + sp * slot_bytes, 0);
+    }
+  }
+
+  // 3. quantised activations into LDS (waits for the activation loads only)
+  if (tid < kMaxTokens * kWave) sh.red[tid] = 0;
+  if constexpr (S == Src::kQuantised) {
+    qs.store(K, sh);
+  } else {
+    if constexpr (!kEarlyNorm) rows.begin(sh);
+    rows.finish(prm.gamma != nullptr, K, sh, !kXFirst);
+  }
+  __syncthreads();
+
+  // 4. contraction
+  int acc[MT];
+#pragma unroll
+  for (int m = 0; m < MT; ++m) acc[m] = 0;
+  for (int base = 0; base < ns; base += kPrefetch) {
+    uint32_t cur[kPrefetch];
+#pragma unroll
+    for (int p = 0; p < kPrefetch; ++p) cur[p] = wbuf[p];
+    const int nb = base + kPrefetch;
+    if (nb < ns) {
+#pragma unroll
+      for (int p = 0; p < kPrefetch; ++p) {
+        const uint32_t sp = static_cast<uint32_t>(nb + p < ns ? nb + p : ns - 1);
+        wbuf[p] = __builtin_amdgcn_raw_buffer_load_b32(wrsrc, lane_off, wave_bytes + sp * slot_bytes, 0);
+      }
+    }
+#pragma unroll
+    for (int p = 0; p < kPrefetch; ++p) {
+      if (base + p < ns) {
+        const int j = jb + H * (base + p) + h;
+        const uint32_t w = cur[p];
+        const uint32_t c0 = codes4(w, 0), c1 = codes4(w, 1), c2 = codes4(w, 2), c3 = codes4(w, 3);
+#pragma unroll
+        for (int m = 0; m < MT; ++m) {
+          const uint4 qv = *reinterpret_cast<const uint4*>(sh.q + m * K + 16 * j);
+          int a = acc[m];
+          a = dot4(c0, qv.x, a);
+          a = dot4(c1, qv.y, a);
+          a = dot4(c2, qv.z, a);
+          a = dot4(c3, qv.w, a);
+          acc[m] = a;
+        }
+      }
+    }
+  }
+
+  // 5. column sums over (wave, h) with LDS atomics, then dequantise
+#pragma unroll
+  for (int m = 0; m < MT; ++m) atomicAdd(&sh.red[m * kWave + c], acc[m]);
+  __syncthreads();
+  if (tid < MT * C) {
+    const int m = tid / C, cc = tid % C;
+    const int64_t nn = static_cast<int64_t>(blockIdx.x) * C + cc;
+    int rsum;
+    if constexpr (S == Src::kQuantised) {
+      rsum = sh.rowsum[m];
+    } else {
+      constexpr int G = row_waves<MT>();
+      rsum = 0;
+#pragma unroll
+      for (int w = 0; w < G; ++w) rsum += sh.slot_i[m * G + w];
+    }
+    if (nn < N) {
+      const int v = sh.red[m * kWave + cc] - rsum;
+      if constexpr (EP == Epilogue::kDequantF32)
+        static_cast<float*>(prm.out)[m * N + nn] = static_cast<float>(v) * (sh.a_scale[m] * prm.w_scale[0]);
+      else
+        static_cast<int32_t*>(prm.out)[m * N + nn] = v;
+    }
+  }
+}
+
+template <int MT, int H, Src S, int VP, Epilogue EP>
+hipError_t launch_one(const DecodeArgs& a, hipStream_t stream) {
+  constexpr int C = kWave / H;
+  const int region = ((MT * a.K + 15) / 16) * 16;
+  const dim3 grid(static_cast<unsigned>((a.N + C - 1) / C));
+  const Params prm{a.Wpacked, a.x, a.gamma, a.q, a.a_scale, a.q_rowsum, a.w_scale, a.out,
+                   a.N, a.K, region};
+  hipLaunchKernelGGL((decode_kernel<MT, H, S, VP, EP>), grid, dim3(kThreads), region + kScalarBytes,
+                     stream, prm);
+  return hipGetLastError();
+}
+
+// vectors of 16 bytes per thread a row needs: ceil(K / E / (G * 64))
+inline int needed_vp(int64_t mt, int K, bool f32) {
+  const int64_t p = mt <= 1 ? 1 : mt <= 2 ? 2 : mt <= 4 ? 4 : 8;
+  const int64_t g = kWaves / p < kMaxRowWaves ? kWaves / p : kMaxRowWaves;
+  const int64_t lanes = g * kWave;
+  const int64_t nvec = K / (f32 ? 4 : 8);
+  return static_cast<int>((nvec + lanes - 1) / lanes);
+}
+
+template <int MT, int H, Src S, Epilogue EP>
+hipError_t dispatch_vp(const DecodeArgs& a, hipStream_t stream) {
+  if constexpr (S == Src::kQuantised) {
+    return launch_one<MT, H, S, 1, EP>(a, stream);
+  } else {
+    const int vp = needed_vp(MT, a.K, S == Src::kF32);
+    if (vp <= 1) return launch_one<MT, H, S, 1, EP>(a, stream);
+    if (vp <= 2) return launch_one<MT, H, S, 2, EP>(a, stream);
+    if (vp <= 4) return launch_one<MT, H, S, 4, EP>(a, stream);
+    return hipErrorInvalidValue;  // excluded by decode_fits
+  }
+}
+
+template <int MT, Src S, Epilogue EP>
+hipError_t dispatch_h(const DecodeArgs& a, hipStream_t stream) {
+  // A 1024-thread workgroup fills a CU, so the grid should stay within one
+  // round of the 256 CUs: the most lanes per column (more workgroups, fewer
+  // words per lane) that still does and that divides K/16.
+  const int J = a.K / 16;
+  if (J % 4 == 0 && (a.N + 15) / 16 <= kGridRound) return dispatch_vp<MT, 4, S, EP>(a, stream);
+  if (J % 2 == 0 && (a.N + 31) / 32 <= kGridRound) return dispatch_vp<MT, 2, S, EP>(a, stream);
+  return dispatch_vp<MT, 1, S, EP>(a, stream);
+}
+
+template <Src S, Epilogue EP>
+hipError_t dispatch_mt(int mt, const DecodeArgs& a, hipStream_t stream) {
+  switch (mt) {
+    case 1: return dispatch_h<1, S, EP>(a, stream);
+    case 2: return dispatch_h<2, S, EP>(a, stream);
+    case 3: return dispatch_h<3, S, EP>(a, stream);
+    case 4: return dispatch_h<4, S, EP>(a, stream);
+    case 5: return dispatch_h<5, S, EP>(a, stream);
+    case 6: return dispatch_h<6, S, EP>(a, stream);
+    case 7: return dispatch_h<7, S, EP>(a, stream);
+    case 8: return dispatch_h<8, S, EP>(a, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace
+
+bool decode_fits(int64_t mt, int K, int64_t N, bool from_x, bool x_is_f32) {
+  if (mt < 1 || mt > kMaxTokens || mt * K > kDecodeMaxLdsQ) return false;
+  if (static_cast<int64_t>(K / 16) * N * 4 >= (int64_t(1) << 32)) return false;  // 32-bit offsets
+  if (!from_x) return true;
+  return needed_vp(mt, K, x_is_f32) <= 4;
+}
+
+hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream) {
+  const int mt = static_cast<int>(a.M);  // 1..8; the caller slices larger M
+  if (a.q != nullptr) {
+    if (a.epilogue == Epilogue::kDequantF32)
+      return dispatch_mt<Src::kQuantised, Epilogue::kDequantF32>(mt, a, stream);
+    return dispatch_mt<Src::kQuantised, Epilogue::kRawI32>(mt, a, stream);
+  }
+  if (a.x_is_f32) return dispatch_mt<Src::kF32, Epilogue::kDequantF32>(mt, a, stream);
+  return dispatch_mt<Src::kBf16, Epilogue::kDequantF32>(mt, a, stream);
+}
+
+}  // namespace mmf

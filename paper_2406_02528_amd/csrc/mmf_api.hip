@@ -5,7 +5,7 @@
 #include <cstdint>
 #include <cstring>
 
-#include "../../include/mmf.h"
+#include "mmf.h"
 #include "mmf_launch.h"
 
 namespace {
@@ -49,8 +49,52 @@ bool use_gemv(int64_t M) {
   return M <= kDecodeMaxTokens;
 }
 
+// Contraction from quantised activations.  Decode-sized slices of at most 8
+// tokens keep q in LDS when it fits, else read it from global memory.
 hipError_t contract(const mmf::ContractArgs& a, hipStream_t stream) {
-  return use_gemv(a.M) ? mmf::launch_gemv(a, stream) : mmf::launch_gemm(a, stream);
+  if (!use_gemv(a.M)) return mmf::launch_gemm(a, stream);
+  for (int64_t m0 = 0; m0 < a.M; m0 += kDecodeMaxTokens) {
+    const int64_t mt = a.M - m0 < kDecodeMaxTokens ? a.M - m0 : kDecodeMaxTokens;
+    const bool raw = a.epilogue == mmf::Epilogue::kRawI32;
+    void* out = raw ? static_cast<void*>(static_cast<int32_t*>(a.out) + m0 * a.N)
+                    : static_cast<void*>(static_cast<float*>(a.out) + m0 * a.N);
+    const float* as = a.a_scale ? a.a_scale + m0 : nullptr;
+    hipError_t e;
+    if (mmf::decode_fits(mt, a.K, a.N, false, false)) {
+      mmf::DecodeArgs d{nullptr, false, nullptr, a.q + m0 * a.K, as, a.q_rowsum + m0,
+                        a.Wpacked, a.w_scale, out, mt, a.K, a.N, a.epilogue};
+      e = mmf::launch_decode(d, stream);
+    } else {
+      mmf::ContractArgs s{a.q + m0 * a.K, as, a.q_rowsum + m0, a.Wpacked, a.w_scale, out,
+                          mt, a.K, a.N, a.epilogue};
+      e = mmf::launch_gemv(s, stream);
+    }
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+// The whole forward runs as fused decode launches (no scratch) when every
+// slice of at most 8 tokens fits the fused kernel.
+bool fused_decode(int64_t M, int64_t K, int64_t N, bool x_is_f32) {
+  if (!use_gemv(M)) return false;
+  const int64_t mt = M < kDecodeMaxTokens ? M : kDecodeMaxTokens;
+  return mmf::decode_fits(mt, static_cast<int>(K), N, true, x_is_f32);
+}
+
+hipError_t run_fused_decode(const void* x, bool x_is_f32, const float* gamma,
+                            const uint32_t* Wpacked, const float* w_scale, float* y, int64_t M,
+                            int64_t K, int64_t N, hipStream_t stream) {
+  const size_t xsz = x_is_f32 ? 4 : 2;
+  for (int64_t m0 = 0; m0 < M; m0 += kDecodeMaxTokens) {
+    const int64_t mt = M - m0 < kDecodeMaxTokens ? M - m0 : kDecodeMaxTokens;
+    mmf::DecodeArgs d{static_cast<const char*>(x) + m0 * K * xsz, x_is_f32, gamma, nullptr,
+                      nullptr, nullptr, Wpacked, w_scale, y + m0 * N, mt,
+                      static_cast<int>(K), N, mmf::Epilogue::kDequantF32};
+    const hipError_t e = mmf::launch_decode(d, stream);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 // Checks of the forward's arguments shared by the allocating and _ws forms.
@@ -67,6 +111,8 @@ int check_fwd(const void* x, const float* gamma, const uint32_t* Wpacked, const 
 int run_fwd(const void* x, bool x_is_f32, const float* gamma, const uint32_t* Wpacked,
             const float* w_scale, float* y, int64_t M, int64_t K, int64_t N, char* scratch,
             hipStream_t stream) {
+  if (fused_decode(M, K, N, x_is_f32))
+    return hip_status(run_fused_decode(x, x_is_f32, gamma, Wpacked, w_scale, y, M, K, N, stream));
   const FwdScratch s = fwd_scratch(M, K);
   int8_t* q = reinterpret_cast<int8_t*>(scratch + s.q_off);
   float* a_scale = reinterpret_cast<float*>(scratch + s.a_off);
@@ -84,6 +130,8 @@ int fwd_alloc(const void* x, bool x_is_f32, const float* gamma, const uint32_t* 
               hipStream_t stream) {
   if (int st = check_fwd(x, gamma, Wpacked, w_scale, y, M, K, N)) return st;
   if (M == 0 || N == 0) return MMF_OK;
+  if (fused_decode(M, K, N, x_is_f32))
+    return hip_status(run_fused_decode(x, x_is_f32, gamma, Wpacked, w_scale, y, M, K, N, stream));
   const FwdScratch s = fwd_scratch(M, K);
   void* scratch = nullptr;
   if (hipMallocAsync(&scratch, s.total, stream) != hipSuccess) return MMF_ERR_HIP;

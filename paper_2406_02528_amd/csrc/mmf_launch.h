@@ -37,8 +37,31 @@ struct ContractArgs {
   Epilogue epilogue;
 };
 
-// Decode kernel: VALU dot products, M <= 8 tokens.
+// Decode contraction with q read from global memory (scalar loads); any K,
+// M <= 8 per launch (larger M is sliced).
 hipError_t launch_gemv(const ContractArgs& a, hipStream_t stream);
+
+// Fused decode forward: up to 8 tokens, q kept in LDS (M*K <= kDecodeMaxLdsQ).
+// With q == nullptr it normalises and quantises x itself (dequant epilogue
+// only); otherwise it contracts the given q / a_scale / q_rowsum.
+constexpr int kDecodeMaxLdsQ = 61440;
+struct DecodeArgs {
+  const void* x;            // [M][K] bf16 or f32 (q == nullptr)
+  bool x_is_f32;
+  const float* gamma;       // [K] or nullptr
+  const int8_t* q;          // [M][K] or nullptr
+  const float* a_scale;     // [M] (q path, dequant epilogue)
+  const int32_t* q_rowsum;  // [M] (q path)
+  const uint32_t* Wpacked;  // [K/16][N]
+  const float* w_scale;     // [1]
+  void* out;                // [M][N]
+  int64_t M;                // 1..8
+  int K;
+  int64_t N;
+  Epilogue epilogue;
+};
+bool decode_fits(int64_t mt, int K, int64_t N, bool from_x, bool x_is_f32);
+hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream);
 // Prefill kernel: int8 MFMA, any M.
 hipError_t launch_gemm(const ContractArgs& a, hipStream_t stream);
 

@@ -328,3 +328,28 @@ def test_dequant_entry_matches_forward(mmf):
             assert torch.equal(y1, y2)
         finally:
             mmf.mmf_set_path(prev)
+
+
+@pytest.mark.parametrize("M,K,N", [(8, 8192, 300), (3, 24576, 70), (1, 32768, 129)])
+def test_decode_fallback_shapes(mmf, M, K, N):
+    """Decode shapes whose quantised rows do not fit the fused kernel's LDS
+    take the two-launch path (act-quant kernel + global-q contraction)."""
+    rs = np.random.default_rng(M * 7 + K)
+    bits, xf, g, W = workloads.random_case(rs, M, K, N)
+    case = Case(bits, xf, g, W, f"fallback M{M}K{K}N{N}")
+    case.oracle_weights()
+    case.oracle_act()
+    acc_ref = oracle.ternary_accumulate(case.q_ref, case.t)
+    y_ref = oracle.dequant(acc_ref, case.a_ref, case.ws_ref)
+    case.upload()
+    log(f"[fallback] M={M} K={K} N={N}")
+    Wp, ws = gpu_weights(mmf, case)
+    check_weights(case, Wp, ws)
+    q, a, r = gpu_act(mmf, case)
+    qn, flip_rows, _ = check_act(case, q, a, r)
+    flip = np.zeros(M, bool)
+    flip[flip_rows] = True
+    acc = run_i32(mmf, torch.from_numpy(case.q_ref).to(dev()), Wp, M, N, "auto").cpu().numpy()
+    assert np.array_equal(acc, acc_ref)
+    y = run_forward(mmf, case, Wp, ws, "auto").cpu().numpy()
+    compare_y(y, y_ref, acc_ref, flip)
