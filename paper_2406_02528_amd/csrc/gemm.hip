@@ -7,12 +7,27 @@
 // the code c = t + 1 in {0,1,2}; the epilogue subtracts sum_k q (sum q*t =
 // sum q*c - sum q) and dequantises.
 //
-// Operand staging:
-//  - A (q, int8 [M][K]) is staged through LDS per 128 x 64 tile.
-//  - B needs no LDS: for a 32x32x32 MFMA, lane l supplies column l % 32 and the
-//    16 k-values of group l / 32, which is exactly one packed word
-//    Wpacked[j][n]; lanes 0-31 read 32 consecutive words.  The word is
-//    expanded in registers into four dwords of code bytes.
+// Operands and pipeline:
+//  - Each workgroup computes a BM x BN output tile.  Its operands stream
+//    through an S-slot LDS ring, one slot per BK-deep k stage: A (q, int8
+//    [M][K]) as BM rows of BK bytes, B as BK/16 rows of BN packed words.
+//  - The global->LDS copies are LDS-DMA buffer loads (the data goes straight
+//    from the memory pipeline into LDS without passing through registers), so
+//    S - 1 stages are in flight while the matrix cores work on the oldest.
+//  - B stays packed until it reaches the registers: for a 32x32x32 MFMA,
+//    lane l supplies column l % 32 and the 16 k-values of group l / 32, which
+//    is exactly one packed word Wpacked[j][n], expanded in registers into four
+//    dwords of code bytes right before use.
+//  - Both operands are read through buffer resources, whose range check
+//    returns zero past the end of the array (rows past M, chunks past K, word
+//    rows past K/16) without touching memory.
+//  - Fragment reads of the next k32 step are interleaved with the MFMAs of
+//    the current one (double-buffered fragment registers).
+//
+// Tile order: workgroups are dealt round-robin to the 8 XCDs, each with its
+// own L2, so the linear workgroup id is remapped to give every XCD a
+// contiguous run of tiles, walked in groups of kGroupM tile rows; the tiles
+// an XCD works on at once then share A rows and B columns in its L2.
 #include "mmf_device.h"
 #include "mmf_launch.h"
 
@@ -22,138 +37,298 @@ namespace {
 typedef int v4i __attribute__((ext_vector_type(4)));
 typedef int v16i __attribute__((ext_vector_type(16)));
 
-constexpr int BM = 128;
-constexpr int BN = 128;
-constexpr int BK = 64;              // k per stage (bytes of q per row)
-constexpr int kThreads = 256;       // 4 waves, 2 x 2, 64 x 64 each
-constexpr int kLdsStride = BK + 16; // padded row stride of the A tile (bytes)
+constexpr int kBufferFlags = 0x00020000;  // gfx9 buffer descriptor word 3
+constexpr int kXcds = 8;
+constexpr int kGroupM = 4;
 
-template <Epilogue EP>
-__global__ __launch_bounds__(kThreads) void gemm_kernel(
+__device__ __forceinline__ void tile_coords(int64_t tiles_m, int64_t tiles_n, int64_t& tm,
+                                            int64_t& tn) {
+  const int64_t total = tiles_m * tiles_n;
+  const int64_t b = blockIdx.x;
+  // XCD-contiguous logical index: XCD x (= b % 8) takes tiles
+  // [x * per, (x + 1) * per); the tail beyond 8 * per keeps its order.
+  const int64_t per = total / kXcds;
+  int64_t L = b;
+  if (b < per * kXcds) L = (b % kXcds) * per + b / kXcds;
+  // grouped row-major walk: kGroupM tile rows at a time, columns inside
+  const int64_t group = L / (kGroupM * tiles_n);
+  const int64_t first_m = group * kGroupM;
+  const int64_t gm = (tiles_m - first_m) < kGroupM ? (tiles_m - first_m) : kGroupM;
+  const int64_t in_group = L - group * kGroupM * tiles_n;
+  tm = first_m + in_group % gm;
+  tn = in_group / gm;
+}
+
+// s_waitcnt immediate (gfx9 encoding) that waits until at most n vector
+// memory operations are outstanding and all LDS operations have completed.
+#define MMF_WAIT_VM_LGKM0(n) (((n) & 0xF) | (0x7 << 4) | ((((n) >> 4) & 3) << 14))
+
+template <int BM, int BN, int WM, int WN, int BK, int S>
+struct Tiling {
+  static constexpr int kWavesM = BM / WM, kWavesN = BN / WN;
+  static constexpr int kWaves = kWavesM * kWavesN;
+  static constexpr int kThreads = kWaves * kWave;
+  static constexpr int FM = WM / 32, FN = WN / 32;   // MFMA tiles per wave
+  static constexpr int KS = BK / 32;                 // k32 steps per stage
+  static constexpr int kChunks = BK / 16;            // 16-byte chunks per A row
+  // A stage: BM rows of BK bytes, unpadded (each LDS-DMA instruction writes
+  // 1 KB contiguously), chunks XOR-swizzled per row against bank conflicts.
+  static constexpr int kABytes = BM * BK;
+  static constexpr int kAInstr = kABytes / 1024;     // 16-byte-per-lane loads
+  // B stage: BK/16 word rows of BN words, each padded by 32 words.
+  static constexpr int kBRow = BN + 32;              // words
+  static constexpr int kBBytes = (BK / 16) * kBRow * 4;
+  static constexpr int kBInstr = (BK / 16) * BN / 64; // 4-byte-per-lane loads
+  static constexpr int kAPerWave = kAInstr / kWaves, kBPerWave = kBInstr / kWaves;
+  static constexpr int kLoadsPerStage = kAPerWave + kBPerWave;
+  static constexpr int kStageBytes = kABytes + kBBytes;
+  static_assert(kAInstr % kWaves == 0 && kBInstr % kWaves == 0, "loads must split evenly");
+  static_assert(S >= 3, "need at least three stages");
+};
+
+// Chunk swizzle of A rows: row r stores logical chunk c in slot c ^ swz(r).
+// For BK = 64 (4 chunks per row) it keeps ds_read_b128 of 32 consecutive rows
+// at one chunk conflict-free both when 8 lanes share 32 banks and when 16
+// lanes share 64 banks.
+template <int kChunks>
+__device__ __forceinline__ int a_swz(int r) {
+  return ((r >> 1) ^ (r >> 3)) & (kChunks - 1);
+}
+
+template <int BM, int BN, int WM, int WN, int BK, int S, Epilogue EP>
+__global__ __launch_bounds__((Tiling<BM, BN, WM, WN, BK, S>::kThreads)) void gemm_kernel(
     const int8_t* __restrict__ q, const float* __restrict__ a_scale,
     const int32_t* __restrict__ q_rowsum, const uint32_t* __restrict__ Wp,
-    const float* __restrict__ w_scale, void* __restrict__ out, int64_t M, int K, int64_t N,
-    int64_t tiles_n) {
-  __shared__ __attribute__((aligned(16))) int8_t As[BM * kLdsStride];
+    const float* __restrict__ w_scale, void* __restrict__ out, int M, int K, int N) {
+  using T = Tiling<BM, BN, WM, WN, BK, S>;
+  constexpr int FM = T::FM, FN = T::FN, KS = T::KS;
+  __shared__ __attribute__((aligned(16))) char smem[S * T::kStageBytes];  // S ring slots
+
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
-  const int64_t tile = blockIdx.x;
-  const int64_t m0 = (tile / tiles_n) * BM;
-  const int64_t n0 = (tile % tiles_n) * BN;
-  const int J = K / 16;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave / T::kWavesN, wn = wave % T::kWavesN;
   const int l32 = lane & 31;
   const int g = lane >> 5;  // k group of this lane inside one MFMA
+  int64_t tm, tn;
+  tile_coords((M + BM - 1) / BM, (N + BN - 1) / BN, tm, tn);
+  const int m0 = static_cast<int>(tm) * BM;
+  const int n0 = static_cast<int>(tn) * BN;
+  const int J = K / 16;
+  const int KT = (K + BK - 1) / BK;
 
-  v16i acc[2][2];
+  // Per-lane source offsets of this wave's LDS-DMA loads (k0 added per stage).
+  // A instruction i: rows 16 (wave * kAPerWave + i) + lane / 4 ... for BK = 64
+  // (BK / 16 chunks per row in general); the lane's LDS slot s holds the
+  // row's logical chunk s ^ swz(row).
+  constexpr int kRowsPerInstr = 1024 / BK;
+  uint32_t a_src[T::kAPerWave];
+  int a_chunk[T::kAPerWave];
 #pragma unroll
-  for (int a = 0; a < 2; ++a)
+  for (int i = 0; i < T::kAPerWave; ++i) {
+    const int r = (wave * T::kAPerWave + i) * kRowsPerInstr + lane / T::kChunks;
+    const int c = (lane % T::kChunks) ^ a_swz<T::kChunks>(r);
+    a_chunk[i] = c * 16;
+    a_src[i] = static_cast<uint32_t>(m0 + r) * static_cast<uint32_t>(K) + static_cast<uint32_t>(c * 16);
+  }
+  // B instruction i: word row jj = idx / (BN / 64), words q64 * 64 + lane
+  uint32_t b_src[T::kBPerWave];
+  int b_jj[T::kBPerWave], b_dst[T::kBPerWave];
 #pragma unroll
-    for (int b = 0; b < 2; ++b)
+  for (int i = 0; i < T::kBPerWave; ++i) {
+    const int idx = wave * T::kBPerWave + i;
+    const int jj = idx / (BN / 64), q64 = idx % (BN / 64);
+    b_jj[i] = jj;
+    b_dst[i] = jj * T::kBRow * 4 + q64 * 256;
+    // columns past N read the next word row or zero; their outputs are dropped
+    b_src[i] = 4u * (static_cast<uint32_t>(jj) * static_cast<uint32_t>(N) +
+                     static_cast<uint32_t>(n0 + q64 * 64 + lane));
+  }
+  const uint32_t b_row = 4u * static_cast<uint32_t>(N);
+
+  // Buffer descriptors for the LDS-DMA loads (gfx9 layout: 48-bit base,
+  // stride 0, size in bytes, format word).
+  const uint64_t qa = reinterpret_cast<uint64_t>(q), wa = reinterpret_cast<uint64_t>(Wp);
+  const v4i adesc = {static_cast<int>(static_cast<uint32_t>(qa)), static_cast<int>((qa >> 32) & 0xFFFF),
+                     static_cast<int>(static_cast<uint32_t>(M) * static_cast<uint32_t>(K)), kBufferFlags};
+  const v4i bdesc = {static_cast<int>(static_cast<uint32_t>(wa)), static_cast<int>((wa >> 32) & 0xFFFF),
+                     static_cast<int>(static_cast<uint32_t>(J) * static_cast<uint32_t>(N) * 4u), kBufferFlags};
+  const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(smem));
+
+  // Issue the loads of stage kt into ring slot kt % S.  The LDS-DMA loads are
+  // written as inline assembly, so the compiler does not see LDS writes that
+  // could alias its fragment reads (it would wait for every load in flight
+  // before each read); this kernel orders them itself with explicit vmcnt
+  // waits before its barriers.  Offsets at or past the end of a buffer (rows
+  // past M, chunks past K, word rows past K/16, stages past the last) read
+  // zero without touching memory.
+  auto issue = [&](int kt) {
+    const uint32_t base = lds0 + static_cast<uint32_t>((kt % S) * T::kStageBytes);
+    const int k0 = kt * BK;
+#pragma unroll
+    for (int i = 0; i < T::kAPerWave; ++i) {
+      const uint32_t off = (k0 + a_chunk[i] < K) ? a_src[i] + static_cast<uint32_t>(k0) : 0x80000000u;
+      const uint32_t dst = __builtin_amdgcn_readfirstlane(base + (wave * T::kAPerWave + i) * 1024);
+      asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+                   :
+                   : "s"(dst), "v"(off), "s"(adesc)
+                   : "memory", "m0");
+    }
+    const int j0 = k0 / 16;
+#pragma unroll
+    for (int i = 0; i < T::kBPerWave; ++i) {
+      const uint32_t off = (j0 + b_jj[i] < J) ? b_src[i] + static_cast<uint32_t>(j0) * b_row : 0x80000000u;
+      const uint32_t dst = __builtin_amdgcn_readfirstlane(base + T::kABytes + b_dst[i]);
+      asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dword %1, %2, 0 offen lds"
+                   :
+                   : "s"(dst), "v"(off), "s"(bdesc)
+                   : "memory", "m0");
+    }
+  };
+
+  v16i acc[FM][FN];
+#pragma unroll
+  for (int a = 0; a < FM; ++a)
+#pragma unroll
+    for (int b = 0; b < FN; ++b)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[a][b][r] = 0;
 
-  // B columns of this lane for its two 32-column fragments
-  int64_t ncol[2];
-  bool nok[2];
+  // Fragments (A operand and expanded B codes) of one k32 step, double
+  // buffered across steps and across stage boundaries.
+  v4i af[2][FM], bf[2][FN];
+  auto read_frags = [&](int kt, int ks, int slot) {
+    const char* st = smem + (kt % S) * T::kStageBytes;
+    const uint32_t* Bs = reinterpret_cast<const uint32_t*>(st + T::kABytes);
 #pragma unroll
-  for (int ni = 0; ni < 2; ++ni) {
-    ncol[ni] = n0 + wn * 64 + ni * 32 + l32;
-    nok[ni] = ncol[ni] < N;
-  }
+    for (int fm = 0; fm < FM; ++fm) {
+      const int row = wm * WM + fm * 32 + l32;
+      const int c = (ks * 2 + g) ^ a_swz<T::kChunks>(row);
+      af[slot][fm] = *reinterpret_cast<const v4i*>(st + row * BK + c * 16);
+    }
+#pragma unroll
+    for (int f = 0; f < FN; ++f) {
+      const uint32_t x = Bs[(2 * ks + g) * T::kBRow + wn * WN + f * 32 + l32];
+      bf[slot][f] = v4i{static_cast<int>(codes4(x, 0)), static_cast<int>(codes4(x, 1)),
+                        static_cast<int>(codes4(x, 2)), static_cast<int>(codes4(x, 3))};
+    }
+  };
+  auto interleave = [&]() {
+    // the next step's LDS reads go out first; the code expansion that
+    // depends on them trails the MFMAs
+    __builtin_amdgcn_sched_group_barrier(0x100, FM + FN, 0);  // DS read
+#pragma unroll
+    for (int i = 0; i < FM * FN; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                                   // MFMA
+      __builtin_amdgcn_sched_group_barrier(0x002, (7 * FN + FM * FN - 1) / (FM * FN), 0);  // VALU
+    }
+  };
 
-  for (int k0 = 0; k0 < K; k0 += BK) {
-    // ---- A tile: 128 rows x 64 bytes, 512 chunks of 16 bytes ----
-    uint4 av[2];
+  // Software pipeline.  Ring slot kt % S holds stage kt.  Stage kt + S - 1
+  // is issued during stage kt, into the slot of stage kt - 1, at the stage's
+  // transition point: in its last k32 step, after this wave's loads of stage
+  // kt + 1 have landed (the S - 3 younger stages may stay in flight) and a
+  // barrier has made every wave's stage-kt+1 data visible and certified that
+  // nobody still reads stage kt - 1.  The first fragments of stage kt + 1 are
+  // then read while the last MFMAs of stage kt are still to be issued, so the
+  // matrix cores see no gap at stage boundaries.
 #pragma unroll
-    for (int c = 0; c < 2; ++c) {
-      const int chunk = tid + c * kThreads;
-      const int row = chunk >> 2;
-      const int col = (chunk & 3) * 16;
-      const int64_t m = m0 + row;
-      if (m < M && k0 + col < K)
-        av[c] = *reinterpret_cast<const uint4*>(q + m * K + k0 + col);
-      else
-        av[c] = make_uint4(0, 0, 0, 0);
-    }
-    // ---- B words for this stage: 2 k32 steps x 2 column fragments ----
-    uint32_t bw[2][2];
+  for (int p = 0; p < S - 1; ++p) issue(p);
+  __builtin_amdgcn_s_waitcnt(MMF_WAIT_VM_LGKM0((S - 2) * T::kLoadsPerStage));
+  __builtin_amdgcn_s_barrier();
+  read_frags(0, 0, 0);
+  int fb = 0;  // fragment buffer of the current step
+  for (int kt = 0; kt < KT; ++kt) {
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      const int j = k0 / 16 + 2 * ks + g;
-#pragma unroll
-      for (int ni = 0; ni < 2; ++ni)
-        bw[ks][ni] = (j < J && nok[ni]) ? Wp[static_cast<int64_t>(j) * N + ncol[ni]] : 0x55555555u;
-    }
-    __syncthreads();  // previous stage's reads of As are done
-#pragma unroll
-    for (int c = 0; c < 2; ++c) {
-      const int chunk = tid + c * kThreads;
-      const int row = chunk >> 2;
-      const int col = (chunk & 3) * 16;
-      *reinterpret_cast<uint4*>(As + row * kLdsStride + col) = av[c];
-    }
-    __syncthreads();
-
-#pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      v4i bf[2];
-#pragma unroll
-      for (int ni = 0; ni < 2; ++ni) {
-        const uint32_t w = bw[ks][ni];
-        bf[ni] = v4i{static_cast<int>(codes4(w, 0)), static_cast<int>(codes4(w, 1)),
-                     static_cast<int>(codes4(w, 2)), static_cast<int>(codes4(w, 3))};
+    for (int ks = 0; ks < KS; ++ks) {
+      if (ks + 1 < KS) {
+        read_frags(kt, ks + 1, fb ^ 1);
+      } else {
+        __builtin_amdgcn_s_waitcnt(MMF_WAIT_VM_LGKM0((S - 3) * T::kLoadsPerStage));
+        __builtin_amdgcn_s_barrier();
+        issue(kt + S - 1);
+        if (kt + 1 < KT) read_frags(kt + 1, 0, fb ^ 1);
       }
 #pragma unroll
-      for (int mi = 0; mi < 2; ++mi) {
-        const int row = wm * 64 + mi * 32 + l32;
-        const v4i af = *reinterpret_cast<const v4i*>(As + row * kLdsStride + ks * 32 + g * 16);
+      for (int fm = 0; fm < FM; ++fm)
 #pragma unroll
-        for (int ni = 0; ni < 2; ++ni)
-          acc[mi][ni] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af, bf[ni], acc[mi][ni], 0, 0, 0);
-      }
+        for (int f = 0; f < FN; ++f)
+          acc[fm][f] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[fb][fm], bf[fb][f], acc[fm][f], 0, 0, 0);
+      interleave();
+      fb ^= 1;
     }
   }
+  // no LDS-DMA write may still be in flight when the workgroup's LDS is freed
+  __builtin_amdgcn_s_waitcnt(MMF_WAIT_VM_LGKM0(0));
 
   // ---- epilogue: lane holds column l32, rows 8*(r/4) + 4*g + r%4 ----
   const float ws = (EP == Epilogue::kDequantF32) ? w_scale[0] : 0.0f;
 #pragma unroll
-  for (int mi = 0; mi < 2; ++mi) {
+  for (int fm = 0; fm < FM; ++fm) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      const int64_t m = m0 + wm * 64 + mi * 32 + 8 * (r >> 2) + 4 * g + (r & 3);
+      const int m = m0 + wm * WM + fm * 32 + 8 * (r >> 2) + 4 * g + (r & 3);
       if (m >= M) continue;
       const int rs = q_rowsum[m];
       float sc = 0.0f;
       if constexpr (EP == Epilogue::kDequantF32) sc = a_scale[m] * ws;
 #pragma unroll
-      for (int ni = 0; ni < 2; ++ni) {
-        if (!nok[ni]) continue;
-        const int v = acc[mi][ni][r] - rs;
+      for (int f = 0; f < FN; ++f) {
+        const int n = n0 + wn * WN + f * 32 + l32;
+        if (n >= N) continue;
+        const int v = acc[fm][f][r] - rs;
+        const int64_t o = static_cast<int64_t>(m) * N + n;
         if constexpr (EP == Epilogue::kDequantF32)
-          static_cast<float*>(out)[m * N + ncol[ni]] = static_cast<float>(v) * sc;
+          static_cast<float*>(out)[o] = static_cast<float>(v) * sc;
         else
-          static_cast<int32_t*>(out)[m * N + ncol[ni]] = v;
+          static_cast<int32_t*>(out)[o] = v;
       }
     }
   }
 }
 
+template <int BM, int BN, int WM, int WN, int BK, int S>
+hipError_t launch_cfg(const ContractArgs& a, int64_t m_begin, int64_t m_rows, hipStream_t stream) {
+  using T = Tiling<BM, BN, WM, WN, BK, S>;
+  const int lds = 0;  // the ring is static LDS
+  const int64_t gm = (m_rows + BM - 1) / BM;
+  const int64_t gn = (a.N + BN - 1) / BN;
+  const dim3 grid(static_cast<unsigned>(gm * gn));
+  const dim3 block(T::kThreads);
+  const int8_t* q = a.q + m_begin * a.K;
+  const float* as = a.a_scale ? a.a_scale + m_begin : nullptr;
+  const int32_t* rs = a.q_rowsum + m_begin;
+  if (a.epilogue == Epilogue::kDequantF32)
+    hipLaunchKernelGGL((gemm_kernel<BM, BN, WM, WN, BK, S, Epilogue::kDequantF32>), grid, block, lds, stream,
+                       q, as, rs, a.Wpacked, a.w_scale,
+                       static_cast<void*>(static_cast<float*>(a.out) + m_begin * a.N),
+                       static_cast<int>(m_rows), a.K, static_cast<int>(a.N));
+  else
+    hipLaunchKernelGGL((gemm_kernel<BM, BN, WM, WN, BK, S, Epilogue::kRawI32>), grid, block, lds, stream,
+                       q, as, rs, a.Wpacked, a.w_scale,
+                       static_cast<void*>(static_cast<int32_t*>(a.out) + m_begin * a.N),
+                       static_cast<int>(m_rows), a.K, static_cast<int>(a.N));
+  return hipGetLastError();
+}
+
 }  // namespace
 
 hipError_t launch_gemm(const ContractArgs& a, hipStream_t stream) {
-  const int64_t gm = (a.M + BM - 1) / BM;
-  const int64_t gn = (a.N + BN - 1) / BN;
-  if (gm * gn > 0x7FFFFFFF) return hipErrorInvalidConfiguration;
-  const dim3 grid(static_cast<unsigned>(gm * gn));
-  if (a.epilogue == Epilogue::kDequantF32)
-    hipLaunchKernelGGL(gemm_kernel<Epilogue::kDequantF32>, grid, dim3(kThreads), 0, stream, a.q,
-                       a.a_scale, a.q_rowsum, a.Wpacked, a.w_scale, a.out, a.M, a.K, a.N, gn);
-  else
-    hipLaunchKernelGGL(gemm_kernel<Epilogue::kRawI32>, grid, dim3(kThreads), 0, stream, a.q,
-                       a.a_scale, a.q_rowsum, a.Wpacked, a.w_scale, a.out, a.M, a.K, a.N, gn);
-  return hipGetLastError();
+  // 32-bit buffer offsets: a launch covers at most 2^31 - 1 bytes of q, of
+  // packed weights and of output; taller problems run in row slices.
+  const int64_t packed = static_cast<int64_t>(a.K / 16) * a.N * 4;
+  if (packed >= (int64_t(1) << 31) || a.N > (int64_t(1) << 24)) return hipErrorInvalidValue;
+  const int64_t by_q = ((int64_t(1) << 31) - 1) / a.K;
+  const int64_t by_y = ((int64_t(1) << 31) - 1) / (4 * a.N);
+  int64_t slice = by_q < by_y ? by_q : by_y;
+  slice = (slice / 256) * 256;
+  if (slice < 256) return hipErrorInvalidValue;
+  for (int64_t m0 = 0; m0 < a.M; m0 += slice) {
+    const int64_t rows = a.M - m0 < slice ? a.M - m0 : slice;
+    const hipError_t e = launch_cfg<256, 256, 64, 128, 64, 4>(a, m0, rows, stream);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 }  // namespace mmf
