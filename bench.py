@@ -12,9 +12,11 @@ Workloads (shapes in workloads.py):
   glu_up, glu_down, large, tiny -- prefill: a step is one forward over all M
       tokens.  value = effective TOPS, 2*M*N*K / step time.
 
-The JSON line carries the roofline of the dominant kernel (the contraction),
-timed alone with HIP events on the stream it runs on, and the CPU oracle timed
-on a bounded sample of the same workload.  The default run also reports the
+The JSON line carries the roofline of the dominant kernel (decode: the fused
+decode kernel, the only launch of a decode forward; prefill: the contraction),
+timed with HIP events on the stream it runs on, with its HBM traffic per launch
+when profiles/traffic.json holds a counter reading of the current kernel
+source, and the CPU oracle timed on a bounded sample of the same workload.  The default run also reports the
 GLU up-projection prefill (effective TOPS vs the int8 MFMA peak) under
 "secondary".
 """
@@ -51,6 +53,15 @@ def parse():
     ap.add_argument("--no-secondary", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--hot-cache", action="store_true",
+                    help="also time one decode call on cache-resident weights (same kernel, so "
+                         "it would skew the kernel's average in a profiler summary)")
+    ap.add_argument("--calib-copy", action="store_true",
+                    help="finish with a few 256 MiB elementwise copies, the reference kernel "
+                         "whose FETCH_SIZE / WRITE_SIZE calibrate the traffic counters")
+    ap.add_argument("--record-traffic", nargs=3, metavar=("WORKLOAD", "FETCH_CSV", "WRITE_CSV"),
+                    help="no GPU: turn rocprofv3 --pmc FETCH_SIZE and WRITE_SIZE counter CSVs of a "
+                         "run with --calib-copy into per-launch HBM traffic in " + "profiles/traffic.json")
     return ap.parse_args()
 
 
@@ -76,6 +87,124 @@ def forward_bytes(w, x_bytes_per_elem):
 def contraction_bytes(w):
     """q + a_scale + q_rowsum + packed weights + w_scale + y for one contraction launch."""
     return w.M * w.K + 8 * w.M + (w.K // 16) * w.N * 4 + 4 + 4 * w.M * w.N
+
+
+# ---------------------------------------------------------------------------
+# HBM traffic per launch, from rocprofv3 counter runs (FETCH_SIZE, WRITE_SIZE)
+# ---------------------------------------------------------------------------
+
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+CSRC = os.path.join(ROOT, "paper_2406_02528_amd", "csrc")
+# the files whose text decides what a kernel does; a recorded traffic figure
+# is used only while their digest is unchanged
+KERNEL_SOURCES = {
+    "decode_kernel": ("decode.hip", "mmf_device.h"),
+    "gemm_kernel": ("gemm.hip", "mmf_device.h"),
+}
+CALIB_BYTES = 1 << 28          # bytes read and written by one calibration copy
+
+
+def source_digest(kernel):
+    import hashlib
+    h = hashlib.sha256()
+    for name in KERNEL_SOURCES[kernel]:
+        with open(os.path.join(CSRC, name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def kernel_key(workload_name, kernel_name):
+    """Which recorded kernel a profiled kernel name stands for, or None."""
+    if workload_name in DECODE:
+        # the fused instance that reads x itself (Src 0 = bf16, 1 = fp32)
+        if "decode_kernel<" in kernel_name and ("Src)2" not in kernel_name):
+            return "decode_kernel"
+        return None
+    if "gemm_kernel<" in kernel_name and "Epilogue)0" in kernel_name:
+        return "gemm_kernel"
+    return None
+
+
+def read_counter_csv(path, counter):
+    import csv
+    per = {}
+    with open(path, newline="") as f:
+        for row in csv.DictReader(f):
+            if row["Counter_Name"] != counter:
+                continue
+            per.setdefault(row["Kernel_Name"], []).append(float(row["Counter_Value"]))
+    return per
+
+
+def record_traffic(run_workload, fetch_csv, write_csv):
+    """Per-launch HBM bytes of the profiled run's dominant kernels, each counter
+    scaled by what it reads for a plain copy of known size (--calib-copy)."""
+    fetch = read_counter_csv(fetch_csv, "FETCH_SIZE")
+    write = read_counter_csv(write_csv, "WRITE_SIZE")
+
+    def calib(per, what):
+        vals = [v for k, vs in per.items() if "neg_kernel" in k for v in vs]
+        if not vals:
+            raise SystemExit(f"no calibration copy in the {what} run (run it with --calib-copy)")
+        kib = sum(vals) / len(vals)
+        return kib, CALIB_BYTES / (kib * 1024.0)
+
+    f_kib, f_fac = calib(fetch, "FETCH_SIZE")
+    w_kib, w_fac = calib(write, "WRITE_SIZE")
+    try:
+        with open(TRAFFIC_FILE) as f:
+            doc = json.load(f)
+    except FileNotFoundError:
+        doc = {}
+    doc["calibration"] = {
+        "kernel": "torch.neg over 2^28 bytes of fp32 (reads and writes 2^28 bytes)",
+        "fetch_kib": f_kib, "write_kib": w_kib, "fetch_factor": f_fac, "write_factor": w_fac}
+    entries = doc.setdefault("entries", {})
+    workloads_in_run = [run_workload] + (["glu_up"] if run_workload in DECODE else [])
+    for name, vals in fetch.items():
+        for wl in workloads_in_run:
+            key = kernel_key(wl, name)
+            if key is None or name not in write:
+                continue
+            fk = sum(vals) / len(vals)
+            wk = sum(write[name]) / len(write[name])
+            fb, wb = fk * 1024.0 * f_fac, wk * 1024.0 * w_fac
+            entries[f"{wl}/{key}"] = {
+                "kernel_name": name, "dispatches": len(vals),
+                "fetch_kib": fk, "write_kib": wk,
+                "fetch_bytes": fb, "write_bytes": wb, "traffic_bytes": fb + wb,
+                "source_sha256": source_digest(key)}
+            print(f"{wl}/{key}: {len(vals)} dispatches, fetch {fb / 1e6:.3f} MB, "
+                  f"write {wb / 1e6:.3f} MB per launch")
+    os.makedirs(os.path.dirname(TRAFFIC_FILE), exist_ok=True)
+    with open(TRAFFIC_FILE, "w") as f:
+        json.dump(doc, f, indent=1, sort_keys=True)
+        f.write("\n")
+
+
+def recorded_traffic(workload_name, kernel):
+    """(traffic bytes per launch, detail) if recorded for the current kernel source."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            doc = json.load(f)
+    except (FileNotFoundError, ValueError):
+        return None, None
+    e = doc.get("entries", {}).get(f"{workload_name}/{kernel}")
+    if not e or e.get("source_sha256") != source_digest(kernel):
+        return None, None
+    c = doc["calibration"]
+    return e["traffic_bytes"], {"fetch_bytes": e["fetch_bytes"], "write_bytes": e["write_bytes"],
+                                "fetch_factor": c["fetch_factor"], "write_factor": c["write_factor"]}
+
+
+def calib_copy(torch):
+    """A plain elementwise copy of known size (the counter calibration kernel)."""
+    src = torch.ones(CALIB_BYTES // 4, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        torch.neg(src, out=dst)
+    torch.cuda.synchronize()
+    del src, dst
 
 
 # ---------------------------------------------------------------------------
@@ -144,8 +273,23 @@ def bench_decode(torch, mmf, w, args):
         for i in range(R):
             mmf.mmf_ternary_gemm_dequant(q, a, rs, Wps[i], wss[i], y)
 
+    # context for the launch-bound regime: R launches of one-element torch
+    # kernels (the launch floor of a graph), and R plain elementwise copies of
+    # each weight copy's packed bytes (reads and writes them once)
+    tiny = torch.zeros(1, dtype=torch.int32, device=dev)
+    copy_buf = torch.empty_like(Wp0)
+
+    def empty_all():
+        for i in range(R):
+            tiny.add_(1)
+
+    def copy_all():
+        for i in range(R):
+            torch.bitwise_not(Wps[i], out=copy_buf)
+
     graphs = {}
-    for name, fn in (("fwd", fwd_all), ("contract", contract_all)):
+    for name, fn in (("fwd", fwd_all), ("contract", contract_all), ("empty", empty_all),
+                     ("copy", copy_all)):
         fn()
         torch.cuda.synchronize()
         g = torch.cuda.CUDAGraph()
@@ -155,26 +299,39 @@ def bench_decode(torch, mmf, w, args):
     timer = Timer(torch)
     log("[bench] timing the forward graph")
     ms_step = timer.time(graphs["fwd"].replay, args.steps, args.warmup)
-    log("[bench] timing the contraction graph")
+    log("[bench] timing the contraction-only graph (pre-quantised q)")
     ms_contract = timer.time(graphs["contract"].replay, args.steps, args.warmup) / R
+    ms_empty = timer.time(graphs["empty"].replay, args.steps, args.warmup) / R
+    ms_copy = timer.time(graphs["copy"].replay, args.steps, args.warmup) / R
     fb = forward_bytes(w, x.element_size())
     cb = contraction_bytes(w)
     value = R * fb / (ms_step * 1e-3) / 1e9
-    achieved = cb / (ms_contract * 1e-3) / 1e9
-    # hot-cache single call, for context
-    ms_hot = timer.time(lambda: mmf.mmf_bitlinear_fwd_ws(x, gamma, Wp0, ws0, y, wsb),
-                        max(args.steps * 10, 50), args.warmup)
+    # one forward call is one launch of the fused decode kernel, so its average
+    # launch duration is the step time over the R launches of the graph
+    us_launch = ms_step * 1e3 / R
+    achieved = fb / (us_launch * 1e-6) / 1e9
+    traffic, tdetail = recorded_traffic(w.name, "decode_kernel")
     result = {
         "value": value, "unit": "GB/s", "ms_per_step": ms_step,
         "config": {"workload": w.name, "M": w.M, "K": w.K, "N": w.N, "x_dtype": w.x_dtype,
                    "weight_copies": R, "calls_per_step": R,
                    "bytes_per_call": fb, "graph": True},
-        "roofline": {"bound": "hbm", "kernel": "gemv_kernel (decode contraction)",
+        "roofline": {"bound": "hbm", "kernel": "decode_kernel (fused RMSNorm + int8 quant + "
+                                               "ternary GEMV + dequant)",
                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
-                     "bytes_per_launch": cb, "avg_launch_us": ms_contract * 1e3},
-        "hot_cache_call_us": ms_hot * 1e3,
+                     "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": traffic, "traffic_detail": tdetail,
+                     "bytes_per_launch": fb, "avg_launch_us": us_launch},
+        "contraction_only": {"avg_launch_us": ms_contract * 1e3, "bytes_per_launch": cb,
+                             "GB/s": cb / (ms_contract * 1e-3) / 1e9},
+        "launch_floor": {"empty_kernel_us": ms_empty * 1e3,
+                         "copy_packed_bytes_us": ms_copy * 1e3,
+                         "note": "per launch inside the same kind of graph; torch kernels"},
     }
+    if args.hot_cache:
+        ms_hot = timer.time(lambda: mmf.mmf_bitlinear_fwd_ws(x, gamma, Wp0, ws0, y, wsb),
+                            max(args.steps * 10, 50), args.warmup)
+        result["hot_cache_call_us"] = ms_hot * 1e3
     return result, fb
 
 
@@ -193,6 +350,7 @@ def bench_prefill(torch, mmf, w, args):
     ms_gemm = timer.time(lambda: mmf.mmf_ternary_gemm_dequant(q, a, rs, Wp, ws, y),
                          args.steps, args.warmup)
     ms_aq = timer.time(lambda: mmf.mmf_act_quant(x, gamma, q, a, rs), args.steps, args.warmup)
+    traffic, tdetail = recorded_traffic(w.name, "gemm_kernel")
     tops = w.ops / (ms_step * 1e-3) / 1e12
     gemm_tops = w.ops / (ms_gemm * 1e-3) / 1e12
     aq_bytes = w.M * w.K * x.element_size() + 4 * w.K + w.M * w.K + 8 * w.M
@@ -201,7 +359,8 @@ def bench_prefill(torch, mmf, w, args):
         "config": {"workload": w.name, "M": w.M, "K": w.K, "N": w.N, "x_dtype": w.x_dtype},
         "roofline": {"bound": "mfma", "kernel": "gemm_kernel (prefill contraction)",
                      "achieved": gemm_tops, "peak": INT8_PEAK_TOPS, "unit": "TFLOP/s",
-                     "frac": gemm_tops / INT8_PEAK_TOPS, "traffic": None,
+                     "frac": gemm_tops / INT8_PEAK_TOPS, "traffic": traffic,
+                     "traffic_detail": tdetail,
                      "ops_per_launch": w.ops, "avg_launch_us": ms_gemm * 1e3},
         "act_quant": {"avg_launch_us": ms_aq * 1e3, "bytes": aq_bytes,
                       "GB/s": aq_bytes / (ms_aq * 1e-3) / 1e9},
@@ -247,6 +406,9 @@ def cpu_baseline(w, fb, seconds):
 
 def main():
     args = parse()
+    if args.record_traffic:
+        record_traffic(*args.record_traffic)
+        return
     check_single_gpu(args)
     import torch
     import paper_2406_02528_amd as mmf
@@ -265,7 +427,7 @@ def main():
         "data": "synthetic (seeded; shapes of the paper's model widths)",
         "config": res["config"], "roofline": res["roofline"],
     }
-    for k in ("hot_cache_call_us", "act_quant"):
+    for k in ("hot_cache_call_us", "act_quant", "contraction_only", "launch_floor"):
         if k in res:
             line[k] = res[k]
     if not args.no_secondary and w.name in DECODE:
@@ -277,6 +439,9 @@ def main():
                              "config": sec["config"], "roofline": sec["roofline"],
                              "act_quant": sec["act_quant"]}
         torch.cuda.empty_cache()
+    if args.calib_copy:
+        log("[bench] calibration copy")
+        calib_copy(torch)
     if not args.no_cpu_baseline:
         log("[bench] cpu baseline (oracle)")
         line["cpu_baseline"] = cpu_baseline(w, fb, args.cpu_seconds)
