@@ -59,8 +59,10 @@ __device__ __forceinline__ void tile_coords(int64_t tiles_m, int64_t tiles_n, in
   tn = in_group / gm;
 }
 
-// s_waitcnt immediate (gfx9 encoding) that waits until at most n vector
-// memory operations are outstanding and all LDS operations have completed.
+// s_waitcnt immediates (gfx9 encoding): at most n vector memory operations
+// outstanding; with LGKM0 also every LDS operation completed, without it no
+// wait on LDS (lgkmcnt field at its maximum).
+#define MMF_WAIT_VM(n) (((n) & 0xF) | (0x7 << 4) | (0xF << 8) | ((((n) >> 4) & 3) << 14))
 #define MMF_WAIT_VM_LGKM0(n) (((n) & 0xF) | (0x7 << 4) | ((((n) >> 4) & 3) << 14))
 
 template <int BM, int BN, int WM, int WN, int BK, int S>
@@ -102,7 +104,8 @@ __global__ __launch_bounds__((Tiling<BM, BN, WM, WN, BK, S>::kThreads)) void gem
     const float* __restrict__ w_scale, void* __restrict__ out, int M, int K, int N) {
   using T = Tiling<BM, BN, WM, WN, BK, S>;
   constexpr int FM = T::FM, FN = T::FN, KS = T::KS;
-  __shared__ __attribute__((aligned(16))) char smem[S * T::kStageBytes];  // S ring slots
+  // S ring slots, then the tile's per-row dequantisation factors
+  __shared__ __attribute__((aligned(16))) char smem[S * T::kStageBytes + 8 * BM];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -116,6 +119,7 @@ __global__ __launch_bounds__((Tiling<BM, BN, WM, WN, BK, S>::kThreads)) void gem
   const int n0 = static_cast<int>(tn) * BN;
   const int J = K / 16;
   const int KT = (K + BK - 1) / BK;
+
 
   // Per-lane source offsets of this wave's LDS-DMA loads (k0 added per stage).
   // A instruction i: rows 16 (wave * kAPerWave + i) + lane / 4 ... for BK = 64
@@ -194,9 +198,11 @@ __global__ __launch_bounds__((Tiling<BM, BN, WM, WN, BK, S>::kThreads)) void gem
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[a][b][r] = 0;
 
-  // Fragments (A operand and expanded B codes) of one k32 step, double
-  // buffered across steps and across stage boundaries.
+  // Fragments of one k32 step, double buffered across steps and across stage
+  // boundaries: A operands straight from LDS, B as raw packed words (bw) and
+  // as expanded code dwords (bf).
   v4i af[2][FM], bf[2][FN];
+  uint32_t bw[2][FN];
   auto read_frags = [&](int kt, int ks, int slot) {
     const char* st = smem + (kt % S) * T::kStageBytes;
     const uint32_t* Bs = reinterpret_cast<const uint32_t*>(st + T::kABytes);
@@ -207,20 +213,14 @@ __global__ __launch_bounds__((Tiling<BM, BN, WM, WN, BK, S>::kThreads)) void gem
       af[slot][fm] = *reinterpret_cast<const v4i*>(st + row * BK + c * 16);
     }
 #pragma unroll
+    for (int f = 0; f < FN; ++f) bw[slot][f] = Bs[(2 * ks + g) * T::kBRow + wn * WN + f * 32 + l32];
+  };
+  auto unpack = [&](int slot) {
+#pragma unroll
     for (int f = 0; f < FN; ++f) {
-      const uint32_t x = Bs[(2 * ks + g) * T::kBRow + wn * WN + f * 32 + l32];
+      const uint32_t x = bw[slot][f];
       bf[slot][f] = v4i{static_cast<int>(codes4(x, 0)), static_cast<int>(codes4(x, 1)),
                         static_cast<int>(codes4(x, 2)), static_cast<int>(codes4(x, 3))};
-    }
-  };
-  auto interleave = [&]() {
-    // the next step's LDS reads go out first; the code expansion that
-    // depends on them trails the MFMAs
-    __builtin_amdgcn_sched_group_barrier(0x100, FM + FN, 0);  // DS read
-#pragma unroll
-    for (int i = 0; i < FM * FN; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                                   // MFMA
-      __builtin_amdgcn_sched_group_barrier(0x002, (7 * FN + FM * FN - 1) / (FM * FN), 0);  // VALU
     }
   };
 
@@ -228,33 +228,78 @@ __global__ __launch_bounds__((Tiling<BM, BN, WM, WN, BK, S>::kThreads)) void gem
   // is issued during stage kt, into the slot of stage kt - 1, at the stage's
   // transition point: in its last k32 step, after this wave's loads of stage
   // kt + 1 have landed (the S - 3 younger stages may stay in flight) and a
-  // barrier has made every wave's stage-kt+1 data visible and certified that
-  // nobody still reads stage kt - 1.  The first fragments of stage kt + 1 are
-  // then read while the last MFMAs of stage kt are still to be issued, so the
-  // matrix cores see no gap at stage boundaries.
+  // barrier has made every wave's stage-kt+1 data visible.  Every read of
+  // slot kt - 1 has been consumed by an earlier MFMA or unpack, so it is
+  // complete before the barrier and the slot can be refilled.
+  //
+  // Each k32 step is fenced into three phases the compiler may not reorder:
+  // the LDS reads of the next step, the MFMAs of the first A fragment (which
+  // cover the read latency), and the remaining MFMAs with the expansion of
+  // the next step's B words slotted between them.
+  constexpr int kFirst = FN;                     // MFMAs in phase 2
+  constexpr int kRest = FM * FN - kFirst;        // MFMAs in phase 3
+  constexpr int kUnpackValu = 7 * FN;            // VALU of one unpack
+  // The tile's per-row dequantisation inputs (q_rowsum, then a_scale) go
+  // into LDS by LDS-DMA too, one 64-row chunk per wave, ahead of the ring's
+  // first stages, so the prologue's wait covers them and the epilogue finds
+  // them there.  Rows past M read zero.
+  {
+    static_assert(2 * BM == 64 * T::kWaves, "one row-factor chunk per wave");
+    const int arr = wave / (BM / 64), chunk = wave % (BM / 64);
+    const int row = m0 + chunk * 64 + lane;
+    const uint32_t off = row < M ? 4u * static_cast<uint32_t>(row) : 0x80000000u;
+    const uint64_t base = arr == 0 ? reinterpret_cast<uint64_t>(q_rowsum) : reinterpret_cast<uint64_t>(a_scale);
+    const int bytes = (arr == 0 || EP == Epilogue::kDequantF32) ? M * 4 : 0;
+    const v4i desc = {static_cast<int>(static_cast<uint32_t>(base)), static_cast<int>((base >> 32) & 0xFFFF),
+                      bytes, kBufferFlags};
+    const uint32_t dst = __builtin_amdgcn_readfirstlane(
+        lds0 + static_cast<uint32_t>(S * T::kStageBytes + arr * BM * 4 + chunk * 256));
+    asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dword %1, %2, 0 offen lds"
+                 :
+                 : "s"(dst), "v"(off), "s"(desc)
+                 : "memory", "m0");
+  }
 #pragma unroll
   for (int p = 0; p < S - 1; ++p) issue(p);
-  __builtin_amdgcn_s_waitcnt(MMF_WAIT_VM_LGKM0((S - 2) * T::kLoadsPerStage));
+  __builtin_amdgcn_s_waitcnt(MMF_WAIT_VM((S - 2) * T::kLoadsPerStage));
   __builtin_amdgcn_s_barrier();
   read_frags(0, 0, 0);
+  unpack(0);
   int fb = 0;  // fragment buffer of the current step
   for (int kt = 0; kt < KT; ++kt) {
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
+      __builtin_amdgcn_sched_barrier(0);
       if (ks + 1 < KS) {
         read_frags(kt, ks + 1, fb ^ 1);
       } else {
-        __builtin_amdgcn_s_waitcnt(MMF_WAIT_VM_LGKM0((S - 3) * T::kLoadsPerStage));
+        __builtin_amdgcn_s_waitcnt(MMF_WAIT_VM((S - 3) * T::kLoadsPerStage));
         __builtin_amdgcn_s_barrier();
         issue(kt + S - 1);
-        if (kt + 1 < KT) read_frags(kt + 1, 0, fb ^ 1);
+        // unconditional (after the last stage it reads a slot of zeros), so
+        // that the loop body stays one block the fences can order
+        read_frags(kt + 1, 0, fb ^ 1);
       }
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int fm = 0; fm < FM; ++fm)
+      for (int f = 0; f < FN; ++f)
+        acc[0][f] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[fb][0], bf[fb][f], acc[0][f], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int fm = 1; fm < FM; ++fm)
 #pragma unroll
         for (int f = 0; f < FN; ++f)
           acc[fm][f] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[fb][fm], bf[fb][f], acc[fm][f], 0, 0, 0);
-      interleave();
+      unpack(fb ^ 1);
+      if constexpr (kRest > 0) {
+#pragma unroll
+        for (int i = 0; i < kRest; ++i) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                                  // MFMA
+          __builtin_amdgcn_sched_group_barrier(0x002, (kUnpackValu + kRest - 1) / kRest, 0);  // VALU
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      (void)kFirst;
       fb ^= 1;
     }
   }
@@ -262,26 +307,33 @@ __global__ __launch_bounds__((Tiling<BM, BN, WM, WN, BK, S>::kThreads)) void gem
   __builtin_amdgcn_s_waitcnt(MMF_WAIT_VM_LGKM0(0));
 
   // ---- epilogue: lane holds column l32, rows 8*(r/4) + 4*g + r%4 ----
+  const int* s_rsum = reinterpret_cast<const int*>(smem + S * T::kStageBytes);
+  const float* s_scale = reinterpret_cast<const float*>(smem + S * T::kStageBytes + 4 * BM);
   const float ws = (EP == Epilogue::kDequantF32) ? w_scale[0] : 0.0f;
+  __syncthreads();
+  // Range-checked buffer stores: rows past M fall outside the output's
+  // range, columns past N are sent there explicitly; no branches.
+  const uint32_t out_bytes = static_cast<uint32_t>(M) * static_cast<uint32_t>(N) * 4u;
+  const __amdgpu_buffer_rsrc_t orsrc =
+      __builtin_amdgcn_make_buffer_rsrc(out, 0, static_cast<int>(out_bytes), kBufferFlags);
 #pragma unroll
   for (int fm = 0; fm < FM; ++fm) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      const int m = m0 + wm * WM + fm * 32 + 8 * (r >> 2) + 4 * g + (r & 3);
-      if (m >= M) continue;
-      const int rs = q_rowsum[m];
-      float sc = 0.0f;
-      if constexpr (EP == Epilogue::kDequantF32) sc = a_scale[m] * ws;
+      const int lr = wm * WM + fm * 32 + 8 * (r >> 2) + 4 * g + (r & 3);
+      const int rs = s_rsum[lr];
+      const float sc = s_scale[lr] * ws;
+      const uint32_t row_bytes = static_cast<uint32_t>(m0 + lr) * static_cast<uint32_t>(N) * 4u;
 #pragma unroll
       for (int f = 0; f < FN; ++f) {
         const int n = n0 + wn * WN + f * 32 + l32;
-        if (n >= N) continue;
+        const uint32_t off = (m0 + lr < M && n < N) ? row_bytes + 4u * static_cast<uint32_t>(n) : 0x80000000u;
         const int v = acc[fm][f][r] - rs;
-        const int64_t o = static_cast<int64_t>(m) * N + n;
         if constexpr (EP == Epilogue::kDequantF32)
-          static_cast<float*>(out)[o] = static_cast<float>(v) * sc;
+          __builtin_amdgcn_raw_buffer_store_b32(static_cast<uint32_t>(__float_as_int(static_cast<float>(v) * sc)),
+                                                orsrc, off, 0, 0);
         else
-          static_cast<int32_t*>(out)[o] = v;
+          __builtin_amdgcn_raw_buffer_store_b32(static_cast<uint32_t>(v), orsrc, off, 0, 0);
       }
     }
   }
