@@ -29,9 +29,9 @@ namespace {
 constexpr int kWaves = 16;
 constexpr int kThreads = kWaves * kWave;  // 1024
 constexpr int kMaxTokens = 8;
-constexpr int kPrefetch = 24;             // weight words per lane issued ahead
 constexpr int kMaxRowWaves = 4;           // waves that normalise one token row
-constexpr int kMaxQVecs = (kDecodeMaxLdsQ / 16 + kThreads - 1) / kThreads;  // q copy
+constexpr int kLdsDmaChunk = 1024;        // bytes of q one LDS-DMA wave instruction copies
+constexpr int kMaxQChunks = (kDecodeMaxLdsQ / kLdsDmaChunk + kWaves - 1) / kWaves;  // per wave
 constexpr float kEps = 1e-6f;
 constexpr int kGridRound = 256;           // workgroups that run at once (one per CU)
 constexpr bool kEarlyNorm = true;         // row waves reduce x before issuing weight loads
@@ -246,30 +246,47 @@ struct RowStage {
   }
 };
 
-// Pre-quantised activations: q, a_scale and q_rowsum copied to LDS.  Loads and
-// stores are unconditional (threads past the end copy the last vector, or
-// token 0's scalars, writing the same bytes as the thread that owns them), so
-// the loads stay ahead of the weight loads instead of being sunk to their use.
+// Pre-quantised activations: q copied into LDS by LDS-DMA (global memory
+// straight to LDS, 16 bytes per lane and 1 KB per wave instruction, no
+// registers involved; the range check of the buffer resource returns zero
+// past the end of q), a_scale and q_rowsum by the first MT threads.  The copy
+// is complete once the issuing wave has waited for all its vector memory
+// operations and passed a barrier.
+constexpr int kBufferFlags = 0x00020000;  // gfx9 buffer descriptor word 3
+typedef int v4i __attribute__((ext_vector_type(4)));
 template <int MT>
 struct QStage {
-  uint4 v[kMaxQVecs];
   float a;
   int rs;
-  __device__ void load(const int8_t* __restrict__ q, const float* __restrict__ a_scale,
-                       const int32_t* __restrict__ q_rowsum, int K) {
-    const int last = (MT * K) / 16 - 1;
+  __device__ __forceinline__ void load(const int8_t* __restrict__ q, const float* __restrict__ a_scale,
+                                       const int32_t* __restrict__ q_rowsum, int K, const Shared& sh) {
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int bytes = MT * K;
+    const int chunks = (bytes + kLdsDmaChunk - 1) / kLdsDmaChunk;
+    const uint64_t qa = reinterpret_cast<uint64_t>(q);
+    const v4i desc = {static_cast<int>(static_cast<uint32_t>(qa)), static_cast<int>((qa >> 32) & 0xFFFF), bytes,
+                      kBufferFlags};
+    const uint32_t lds_q = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(sh.q));
 #pragma unroll
-    for (int i = 0; i < kMaxQVecs; ++i)
-      v[i] = reinterpret_cast<const uint4*>(q)[min(static_cast<int>(threadIdx.x) + kThreads * i, last)];
+    for (int i = 0; i < kMaxQChunks; ++i) {
+      const int ch = wave + kWaves * i;
+      if (ch < chunks) {  // wave-uniform
+        const uint32_t off = static_cast<uint32_t>(ch * kLdsDmaChunk + lane * 16);
+        const uint32_t dst = __builtin_amdgcn_readfirstlane(lds_q + static_cast<uint32_t>(ch * kLdsDmaChunk));
+        asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+                     :
+                     : "s"(dst), "v"(off), "s"(desc)
+                     : "memory", "m0");
+      }
+    }
     const int t = threadIdx.x < MT ? threadIdx.x : 0;
     a = a_scale != nullptr ? a_scale[t] : 0.0f;
     rs = q_rowsum[t];
   }
-  __device__ void store(int K, const Shared& sh) const {
-    const int last = (MT * K) / 16 - 1;
-#pragma unroll
-    for (int i = 0; i < kMaxQVecs; ++i)
-      reinterpret_cast<uint4*>(sh.q)[min(static_cast<int>(threadIdx.x) + kThreads * i, last)] = v[i];
+  __device__ __forceinline__ void store(const Shared& sh) const {
+    // every LDS-DMA write of this wave has landed
+    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0); no wait on the other counters
     const int t = threadIdx.x < MT ? threadIdx.x : 0;
     sh.a_scale[t] = a;
     sh.rowsum[t] = rs;
@@ -280,7 +297,6 @@ struct QStage {
 // load takes the lane's 32-bit offset in a VGPR and the slot's offset in an
 // SGPR, so no vector address arithmetic is spent per slot, and the hardware
 // range check returns 0 past the end of the packed array.
-constexpr int kBufferFlags = 0x00020000;  // gfx9 buffer descriptor word 3
 
 // Kernel arguments in one block, so that the scalar loads that fetch them are
 // issued together at entry.
@@ -303,8 +319,9 @@ struct Params {
 // lane (c, h) is word row jb + H s + h.  Whether a slot exists is therefore
 // the same for the whole wave, and its address is a scalar base
 // (Wp + (jb + H s) N) plus a per-lane offset (h N + column) computed once.
-template <int MT, int H, Src S, int VP, Epilogue EP>
+template <int MT, int H, Src S, int VP, int kPrefetch, Epilogue EP>
 __global__ __launch_bounds__(kThreads) void decode_kernel(const Params prm) {
+  static_assert(kPrefetch % 4 == 0, "prefetch goes in groups of four");
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const int K = prm.K;
   const int64_t N = prm.N;
@@ -334,7 +351,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(const Params prm) {
   RowStage<MT, S == Src::kQuantised ? Src::kBf16 : S, VP> rows;
   QStage<MT> qs;
   if constexpr (S == Src::kQuantised)
-    qs.load(prm.q, prm.a_scale, prm.q_rowsum, K);
+    qs.load(prm.q, prm.a_scale, prm.q_rowsum, K, sh);
   else
     rows.load(prm.x, prm.gamma, K);
   __builtin_amdgcn_sched_barrier(0);  // keep these loads ahead of the weight loads
@@ -346,21 +363,28 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(const Params prm) {
   if constexpr (kXFirst && S != Src::kQuantised) __syncthreads();
   __builtin_amdgcn_sched_barrier(0);
 
-  // 2. the first weight slots (slots past the wave's range repeat its last
-  //    slot and are not used)
+  // 2. the first weight slots, kPrefetch words per lane ahead of their use,
+  //    in groups of four: a group is issued only when the wave has a slot in
+  //    it (a wave-uniform branch); inside the last group, slots past the
+  //    wave's range repeat its last slot and are not used.
   uint32_t wbuf[kPrefetch];
   if (ns > 0) {
 #pragma unroll
-    for (int p = 0; p < kPrefetch; ++p) {
-      const uint32_t sp = static_cast<uint32_t>(p < ns ? p : ns - 1);
-      wbuf[p] = __builtin_amdgcn_raw_buffer_load_b32(wrsrc, lane_off, wave_bytes + sp * slot_bytes, 0);
+    for (int p0 = 0; p0 < kPrefetch; p0 += 4) {
+      if (p0 == 0 || p0 < ns) {
+#pragma unroll
+        for (int p = p0; p < p0 + 4; ++p) {
+          const uint32_t sp = static_cast<uint32_t>(p < ns ? p : ns - 1);
+          wbuf[p] = __builtin_amdgcn_raw_buffer_load_b32(wrsrc, lane_off, wave_bytes + sp * slot_bytes, 0);
+        }
+      }
     }
   }
 
   // 3. quantised activations into LDS (waits for the activation loads only)
   if (tid < kMaxTokens * kWave) sh.red[tid] = 0;
   if constexpr (S == Src::kQuantised) {
-    qs.store(K, sh);
+    qs.store(sh);
   } else {
     if constexpr (!kEarlyNorm) rows.begin(sh);
     rows.finish(prm.gamma != nullptr, K, sh, !kXFirst);
@@ -376,11 +400,14 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(const Params prm) {
 #pragma unroll
     for (int p = 0; p < kPrefetch; ++p) cur[p] = wbuf[p];
     const int nb = base + kPrefetch;
-    if (nb < ns) {
 #pragma unroll
-      for (int p = 0; p < kPrefetch; ++p) {
-        const uint32_t sp = static_cast<uint32_t>(nb + p < ns ? nb + p : ns - 1);
-        wbuf[p] = __builtin_amdgcn_raw_buffer_load_b32(wrsrc, lane_off, wave_bytes + sp * slot_bytes, 0);
+    for (int p0 = 0; p0 < kPrefetch; p0 += 4) {
+      if (nb + p0 < ns) {
+#pragma unroll
+        for (int p = p0; p < p0 + 4; ++p) {
+          const uint32_t sp = static_cast<uint32_t>(nb + p < ns ? nb + p : ns - 1);
+          wbuf[p] = __builtin_amdgcn_raw_buffer_load_b32(wrsrc, lane_off, wave_bytes + sp * slot_bytes, 0);
+        }
       }
     }
 #pragma unroll
@@ -429,16 +456,28 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(const Params prm) {
   }
 }
 
-template <int MT, int H, Src S, int VP, Epilogue EP>
+template <int MT, int H, Src S, int VP, int PF, Epilogue EP>
 hipError_t launch_one(const DecodeArgs& a, hipStream_t stream) {
   constexpr int C = kWave / H;
-  const int region = ((MT * a.K + 15) / 16) * 16;
+  // the q region is whole LDS-DMA chunks
+  const int region = ((MT * a.K + kLdsDmaChunk - 1) / kLdsDmaChunk) * kLdsDmaChunk;
   const dim3 grid(static_cast<unsigned>((a.N + C - 1) / C));
   const Params prm{a.Wpacked, a.x, a.gamma, a.q, a.a_scale, a.q_rowsum, a.w_scale, a.out,
                    a.N, a.K, region};
-  hipLaunchKernelGGL((decode_kernel<MT, H, S, VP, EP>), grid, dim3(kThreads), region + kScalarBytes,
+  hipLaunchKernelGGL((decode_kernel<MT, H, S, VP, PF, EP>), grid, dim3(kThreads), region + kScalarBytes,
                      stream, prm);
   return hipGetLastError();
+}
+
+// Weight words in flight per lane: a wave's whole range when it holds at most
+// four slots, else eight at a time (measured: deeper prefetch only delays
+// the loads of the waves that also normalise the token rows).
+template <int MT, int H, Src S, int VP, Epilogue EP>
+hipError_t dispatch_pf(const DecodeArgs& a, hipStream_t stream) {
+  const int J = a.K / 16;
+  const int slots = (J + kWaves * H - 1) / (kWaves * H);
+  if (slots <= 4) return launch_one<MT, H, S, VP, 4, EP>(a, stream);
+  return launch_one<MT, H, S, VP, 8, EP>(a, stream);
 }
 
 // vectors of 16 bytes per thread a row needs: ceil(K / E / (G * 64))
@@ -453,12 +492,12 @@ inline int needed_vp(int64_t mt, int K, bool f32) {
 template <int MT, int H, Src S, Epilogue EP>
 hipError_t dispatch_vp(const DecodeArgs& a, hipStream_t stream) {
   if constexpr (S == Src::kQuantised) {
-    return launch_one<MT, H, S, 1, EP>(a, stream);
+    return dispatch_pf<MT, H, S, 1, EP>(a, stream);
   } else {
     const int vp = needed_vp(MT, a.K, S == Src::kF32);
-    if (vp <= 1) return launch_one<MT, H, S, 1, EP>(a, stream);
-    if (vp <= 2) return launch_one<MT, H, S, 2, EP>(a, stream);
-    if (vp <= 4) return launch_one<MT, H, S, 4, EP>(a, stream);
+    if (vp <= 1) return dispatch_pf<MT, H, S, 1, EP>(a, stream);
+    if (vp <= 2) return dispatch_pf<MT, H, S, 2, EP>(a, stream);
+    if (vp <= 4) return dispatch_pf<MT, H, S, 4, EP>(a, stream);
     return hipErrorInvalidValue;  // excluded by decode_fits
   }
 }
