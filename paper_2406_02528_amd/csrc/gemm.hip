@@ -3,26 +3,36 @@
 //
 // At thousands of tokens the ternary accumulation is a dense contraction of
 // int8 activations against {-1,0,1} weights, so it runs on
-// v_mfma_i32_32x32x32_i8 with exact int32 accumulation.  The weight operand is
+// v_mfma_i32_16x16x64_i8 with exact int32 accumulation.  The weight operand is
 // the code c = t + 1 in {0,1,2}; the epilogue subtracts sum_k q (sum q*t =
 // sum q*c - sum q) and dequantises.
 //
+// Tiling: a workgroup of 8 waves computes a 256 x 256 output tile; wave
+// (wm, wn) owns a 128 x 64 block as 8 x 4 MFMA tiles of 16 x 16.  Each
+// expanded weight fragment therefore feeds eight MFMAs, which keeps the VALU
+// work of the 2-bit expansion small against the matrix work.
+//
 // Operands and pipeline:
-//  - Each workgroup computes a BM x BN output tile.  Its operands stream
-//    through an S-slot LDS ring, one slot per BK-deep k stage: A (q, int8
-//    [M][K]) as BM rows of BK bytes, B as BK/16 rows of BN packed words.
-//  - The global->LDS copies are LDS-DMA buffer loads (the data goes straight
-//    from the memory pipeline into LDS without passing through registers), so
-//    S - 1 stages are in flight while the matrix cores work on the oldest.
-//  - B stays packed until it reaches the registers: for a 32x32x32 MFMA,
-//    lane l supplies column l % 32 and the 16 k-values of group l / 32, which
-//    is exactly one packed word Wpacked[j][n], expanded in registers into four
-//    dwords of code bytes right before use.
+//  - The operands of one BK = 128 deep k stage stream through a 3-slot LDS
+//    ring: A (q, int8 [M][K]) as 256 rows of 128 bytes, B as 8 rows of 256
+//    packed words.  The global->LDS copies are LDS-DMA buffer loads (the data
+//    goes from the memory pipeline straight into LDS, not through registers).
+//  - The copies of a stage are issued one per group of MFMAs through the step
+//    that retires a slot, not in one burst: a burst of LDS-DMA instructions
+//    from all waves at a barrier fills the vector memory queue, and a wave
+//    stalled on a memory issue cannot issue its MFMAs.
+//  - B stays packed until it reaches the registers: for a 16x16x64 MFMA lane
+//    l supplies column l % 16 and the 16 k-values of group l / 16, which is
+//    exactly one packed word Wpacked[j][n], expanded in registers into four
+//    dwords of code bytes.  The words of the next k64 step are read one step
+//    ahead, so the expansion never waits for LDS.
 //  - Both operands are read through buffer resources, whose range check
 //    returns zero past the end of the array (rows past M, chunks past K, word
 //    rows past K/16) without touching memory.
-//  - Fragment reads of the next k32 step are interleaved with the MFMAs of
-//    the current one (double-buffered fragment registers).
+//  - The MFMA takes the weights as its first operand and the activations as
+//    its second, i.e. it computes the transposed tile: lane (g, l16) then ends
+//    up with four consecutive output columns of one row, stored with one
+//    16-byte write per 16 x 16 block.
 //
 // Tile order: workgroups are dealt round-robin to the 8 XCDs, each with its
 // own L2, so the linear workgroup id is remapped to give every XCD a
@@ -35,7 +45,6 @@ namespace mmf {
 namespace {
 
 typedef int v4i __attribute__((ext_vector_type(4)));
-typedef int v16i __attribute__((ext_vector_type(16)));
 
 constexpr int kBufferFlags = 0x00020000;  // gfx9 buffer descriptor word 3
 constexpr int kXcds = 8;
@@ -65,44 +74,47 @@ __device__ __forceinline__ void tile_coords(int64_t tiles_m, int64_t tiles_n, in
 #define MMF_WAIT_VM(n) (((n) & 0xF) | (0x7 << 4) | (0xF << 8) | ((((n) >> 4) & 3) << 14))
 #define MMF_WAIT_VM_LGKM0(n) (((n) & 0xF) | (0x7 << 4) | ((((n) >> 4) & 3) << 14))
 
-template <int BM, int BN, int WM, int WN, int BK, int S>
+// BX4: B rows are copied 16 bytes per lane (one word row per instruction),
+// which needs N % 4 == 0 for aligned rows; otherwise 4 bytes per lane.
+template <int BM, int BN, int WM, int WN, int BK, int S, bool BX4>
 struct Tiling {
   static constexpr int kWavesM = BM / WM, kWavesN = BN / WN;
   static constexpr int kWaves = kWavesM * kWavesN;
   static constexpr int kThreads = kWaves * kWave;
-  static constexpr int FM = WM / 32, FN = WN / 32;   // MFMA tiles per wave
-  static constexpr int KS = BK / 32;                 // k32 steps per stage
+  static constexpr int FM = WM / 16, FN = WN / 16;   // 16 x 16 MFMA tiles per wave
+  static constexpr int KS = BK / 64;                 // k64 steps per stage
   static constexpr int kChunks = BK / 16;            // 16-byte chunks per A row
   // A stage: BM rows of BK bytes, unpadded (each LDS-DMA instruction writes
   // 1 KB contiguously), chunks XOR-swizzled per row against bank conflicts.
   static constexpr int kABytes = BM * BK;
-  static constexpr int kAInstr = kABytes / 1024;     // 16-byte-per-lane loads
-  // B stage: BK/16 word rows of BN words, each padded by 32 words.
-  static constexpr int kBRow = BN + 32;              // words
+  static constexpr int kAInstr = kABytes / 1024;
+  // B stage: BK/16 word rows of BN words, each padded by 16 words so that the
+  // four word rows one MFMA operand read spans fall on different banks.
+  static constexpr int kBRow = BN + 16;
   static constexpr int kBBytes = (BK / 16) * kBRow * 4;
-  static constexpr int kBInstr = (BK / 16) * BN / 64; // 4-byte-per-lane loads
+  static constexpr int kBInstr = BX4 ? (BK / 16) * BN / 256 : (BK / 16) * BN / 64;
   static constexpr int kAPerWave = kAInstr / kWaves, kBPerWave = kBInstr / kWaves;
   static constexpr int kLoadsPerStage = kAPerWave + kBPerWave;
   static constexpr int kStageBytes = kABytes + kBBytes;
   static_assert(kAInstr % kWaves == 0 && kBInstr % kWaves == 0, "loads must split evenly");
-  static_assert(S >= 3, "need at least three stages");
+  static_assert(S == 3, "the stage waits below assume a 3-slot ring");
+  static_assert(FN == 4 && FM >= 2 * FN, "expansion schedule: four words, one per late fragment");
+  static_assert(kLoadsPerStage <= FM, "one stage load per fragment group");
+  static_assert(BK == 128, "A swizzle is for 8 chunks per row");
 };
 
-// Chunk swizzle of A rows: row r stores logical chunk c in slot c ^ swz(r).
-// For BK = 64 (4 chunks per row) it keeps ds_read_b128 of 32 consecutive rows
-// at one chunk conflict-free both when 8 lanes share 32 banks and when 16
-// lanes share 64 banks.
-template <int kChunks>
-__device__ __forceinline__ int a_swz(int r) {
-  return ((r >> 1) ^ (r >> 3)) & (kChunks - 1);
-}
+// Chunk swizzle of A rows (8 chunks of 16 bytes per row): row r stores logical
+// chunk c in slot c ^ swz(r).  Sixteen consecutive rows at one chunk then hit
+// distinct bank groups both when 8 lanes share 32 banks and when 16 lanes
+// share 64 banks; swz(r + 16) = swz(r).
+__device__ __forceinline__ int a_swz(int r) { return ((r >> 1) ^ (r << 2)) & 7; }
 
-template <int BM, int BN, int WM, int WN, int BK, int S, Epilogue EP>
-__global__ __launch_bounds__((Tiling<BM, BN, WM, WN, BK, S>::kThreads)) void gemm_kernel(
+template <int BM, int BN, int WM, int WN, int BK, int S, bool BX4, Epilogue EP>
+__global__ __launch_bounds__((Tiling<BM, BN, WM, WN, BK, S, BX4>::kThreads)) void gemm_kernel(
     const int8_t* __restrict__ q, const float* __restrict__ a_scale,
     const int32_t* __restrict__ q_rowsum, const uint32_t* __restrict__ Wp,
     const float* __restrict__ w_scale, void* __restrict__ out, int M, int K, int N) {
-  using T = Tiling<BM, BN, WM, WN, BK, S>;
+  using T = Tiling<BM, BN, WM, WN, BK, S, BX4>;
   constexpr int FM = T::FM, FN = T::FN, KS = T::KS;
   // S ring slots, then the tile's per-row dequantisation factors
   __shared__ __attribute__((aligned(16))) char smem[S * T::kStageBytes + 8 * BM];
@@ -111,8 +123,8 @@ __global__ __launch_bounds__((Tiling<BM, BN, WM, WN, BK, S>::kThreads)) void gem
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave / T::kWavesN, wn = wave % T::kWavesN;
-  const int l32 = lane & 31;
-  const int g = lane >> 5;  // k group of this lane inside one MFMA
+  const int l16 = lane & 15;
+  const int g = lane >> 4;  // k group of this lane inside one MFMA
   int64_t tm, tn;
   tile_coords((M + BM - 1) / BM, (N + BN - 1) / BN, tm, tn);
   const int m0 = static_cast<int>(tm) * BM;
@@ -120,33 +132,39 @@ __global__ __launch_bounds__((Tiling<BM, BN, WM, WN, BK, S>::kThreads)) void gem
   const int J = K / 16;
   const int KT = (K + BK - 1) / BK;
 
-
   // Per-lane source offsets of this wave's LDS-DMA loads (k0 added per stage).
-  // A instruction i: rows 16 (wave * kAPerWave + i) + lane / 4 ... for BK = 64
-  // (BK / 16 chunks per row in general); the lane's LDS slot s holds the
-  // row's logical chunk s ^ swz(row).
+  // A instruction i covers rows 8 (wave * kAPerWave + i) .. + 7; the lane's
+  // LDS slot s holds the row's logical chunk s ^ swz(row).
   constexpr int kRowsPerInstr = 1024 / BK;
   uint32_t a_src[T::kAPerWave];
   int a_chunk[T::kAPerWave];
 #pragma unroll
   for (int i = 0; i < T::kAPerWave; ++i) {
     const int r = (wave * T::kAPerWave + i) * kRowsPerInstr + lane / T::kChunks;
-    const int c = (lane % T::kChunks) ^ a_swz<T::kChunks>(r);
+    const int c = (lane % T::kChunks) ^ a_swz(r);
     a_chunk[i] = c * 16;
     a_src[i] = static_cast<uint32_t>(m0 + r) * static_cast<uint32_t>(K) + static_cast<uint32_t>(c * 16);
   }
-  // B instruction i: word row jj = idx / (BN / 64), words q64 * 64 + lane
+  // B instruction i: word row jj, columns of this tile.  Columns past N read
+  // the next word row or zero; their outputs are dropped.
   uint32_t b_src[T::kBPerWave];
   int b_jj[T::kBPerWave], b_dst[T::kBPerWave];
 #pragma unroll
   for (int i = 0; i < T::kBPerWave; ++i) {
     const int idx = wave * T::kBPerWave + i;
-    const int jj = idx / (BN / 64), q64 = idx % (BN / 64);
-    b_jj[i] = jj;
-    b_dst[i] = jj * T::kBRow * 4 + q64 * 256;
-    // columns past N read the next word row or zero; their outputs are dropped
-    b_src[i] = 4u * (static_cast<uint32_t>(jj) * static_cast<uint32_t>(N) +
-                     static_cast<uint32_t>(n0 + q64 * 64 + lane));
+    if constexpr (BX4) {
+      const int jj = idx;
+      b_jj[i] = jj;
+      b_dst[i] = jj * T::kBRow * 4;
+      b_src[i] = 4u * (static_cast<uint32_t>(jj) * static_cast<uint32_t>(N) +
+                       static_cast<uint32_t>(n0 + 4 * lane));
+    } else {
+      const int jj = idx / (BN / 64), q64 = idx % (BN / 64);
+      b_jj[i] = jj;
+      b_dst[i] = jj * T::kBRow * 4 + q64 * 256;
+      b_src[i] = 4u * (static_cast<uint32_t>(jj) * static_cast<uint32_t>(N) +
+                       static_cast<uint32_t>(n0 + q64 * 64 + lane));
+    }
   }
   const uint32_t b_row = 4u * static_cast<uint32_t>(N);
 
@@ -159,86 +177,70 @@ __global__ __launch_bounds__((Tiling<BM, BN, WM, WN, BK, S>::kThreads)) void gem
                      static_cast<int>(static_cast<uint32_t>(J) * static_cast<uint32_t>(N) * 4u), kBufferFlags};
   const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(smem));
 
-  // Issue the loads of stage kt into ring slot kt % S.  The LDS-DMA loads are
-  // written as inline assembly, so the compiler does not see LDS writes that
-  // could alias its fragment reads (it would wait for every load in flight
-  // before each read); this kernel orders them itself with explicit vmcnt
-  // waits before its barriers.  Offsets at or past the end of a buffer (rows
-  // past M, chunks past K, word rows past K/16, stages past the last) read
-  // zero without touching memory.
-  auto issue = [&](int kt) {
+  // Load i of stage kt into ring slot kt % S (i < kAPerWave: an A load, else
+  // a B load).  The LDS-DMA loads are written as inline assembly, so the
+  // compiler does not see LDS writes that could alias its fragment reads (it
+  // would wait for every load in flight before each read); this kernel orders
+  // them itself with explicit vmcnt waits before its barriers.  Offsets at or
+  // past the end of a buffer (rows past M, chunks past K, word rows past
+  // K/16, stages past the last) read zero without touching memory.
+  auto issue_one = [&](int kt, int i) {
     const uint32_t base = lds0 + static_cast<uint32_t>((kt % S) * T::kStageBytes);
     const int k0 = kt * BK;
-#pragma unroll
-    for (int i = 0; i < T::kAPerWave; ++i) {
+    if (i < T::kAPerWave) {
       const uint32_t off = (k0 + a_chunk[i] < K) ? a_src[i] + static_cast<uint32_t>(k0) : 0x80000000u;
       const uint32_t dst = __builtin_amdgcn_readfirstlane(base + (wave * T::kAPerWave + i) * 1024);
       asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
                    :
                    : "s"(dst), "v"(off), "s"(adesc)
                    : "memory", "m0");
-    }
-    const int j0 = k0 / 16;
-#pragma unroll
-    for (int i = 0; i < T::kBPerWave; ++i) {
-      const uint32_t off = (j0 + b_jj[i] < J) ? b_src[i] + static_cast<uint32_t>(j0) * b_row : 0x80000000u;
-      const uint32_t dst = __builtin_amdgcn_readfirstlane(base + T::kABytes + b_dst[i]);
-      asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dword %1, %2, 0 offen lds"
-                   :
-                   : "s"(dst), "v"(off), "s"(bdesc)
-                   : "memory", "m0");
+    } else {
+      const int b = i - T::kAPerWave;
+      const int j0 = k0 / 16;
+      const uint32_t off = (j0 + b_jj[b] < J) ? b_src[b] + static_cast<uint32_t>(j0) * b_row : 0x80000000u;
+      const uint32_t dst = __builtin_amdgcn_readfirstlane(base + T::kABytes + b_dst[b]);
+      if constexpr (BX4)
+        asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+                     :
+                     : "s"(dst), "v"(off), "s"(bdesc)
+                     : "memory", "m0");
+      else
+        asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dword %1, %2, 0 offen lds"
+                     :
+                     : "s"(dst), "v"(off), "s"(bdesc)
+                     : "memory", "m0");
     }
   };
 
-  v16i acc[FM][FN];
+  v4i acc[FM][FN];
 #pragma unroll
   for (int a = 0; a < FM; ++a)
 #pragma unroll
-    for (int b = 0; b < FN; ++b)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[a][b][r] = 0;
+    for (int b = 0; b < FN; ++b) acc[a][b] = v4i{0, 0, 0, 0};
 
-  // Fragments of one k32 step, double buffered across steps and across stage
-  // boundaries: A operands straight from LDS, B as raw packed words (bw) and
-  // as expanded code dwords (bf).
-  v4i af[2][FM], bf[2][FN];
-  uint32_t bw[2][FN];
-  auto read_frags = [&](int kt, int ks, int slot) {
+  // Fragments: A (16 rows x 64 k per lane group) refilled fragment by
+  // fragment after each fragment's last use in the step; raw B words of the
+  // next step; expanded code dwords of the current and the next step.
+  v4i af[FM];
+  uint32_t bw[FN];
+  v4i be[2][FN];
+  auto a_read = [&](int s, int fm) -> v4i {
+    const int kt = s / KS, ks = s % KS;
     const char* st = smem + (kt % S) * T::kStageBytes;
-    const uint32_t* Bs = reinterpret_cast<const uint32_t*>(st + T::kABytes);
-#pragma unroll
-    for (int fm = 0; fm < FM; ++fm) {
-      const int row = wm * WM + fm * 32 + l32;
-      const int c = (ks * 2 + g) ^ a_swz<T::kChunks>(row);
-      af[slot][fm] = *reinterpret_cast<const v4i*>(st + row * BK + c * 16);
-    }
-#pragma unroll
-    for (int f = 0; f < FN; ++f) bw[slot][f] = Bs[(2 * ks + g) * T::kBRow + wn * WN + f * 32 + l32];
+    const int row = wm * WM + fm * 16 + l16;
+    const int c = (ks * 4 + g) ^ a_swz(row);
+    return *reinterpret_cast<const v4i*>(st + row * BK + c * 16);
   };
-  auto unpack = [&](int slot) {
-#pragma unroll
-    for (int f = 0; f < FN; ++f) {
-      const uint32_t x = bw[slot][f];
-      bf[slot][f] = v4i{static_cast<int>(codes4(x, 0)), static_cast<int>(codes4(x, 1)),
-                        static_cast<int>(codes4(x, 2)), static_cast<int>(codes4(x, 3))};
-    }
+  auto b_read = [&](int s, int f) -> uint32_t {
+    const int kt = s / KS, ks = s % KS;
+    const uint32_t* Bs = reinterpret_cast<const uint32_t*>(smem + (kt % S) * T::kStageBytes + T::kABytes);
+    return Bs[(ks * 4 + g) * T::kBRow + wn * WN + f * 16 + l16];
+  };
+  auto expand = [](uint32_t x) -> v4i {
+    return v4i{static_cast<int>(codes4(x, 0)), static_cast<int>(codes4(x, 1)),
+               static_cast<int>(codes4(x, 2)), static_cast<int>(codes4(x, 3))};
   };
 
-  // Software pipeline.  Ring slot kt % S holds stage kt.  Stage kt + S - 1
-  // is issued during stage kt, into the slot of stage kt - 1, at the stage's
-  // transition point: in its last k32 step, after this wave's loads of stage
-  // kt + 1 have landed (the S - 3 younger stages may stay in flight) and a
-  // barrier has made every wave's stage-kt+1 data visible.  Every read of
-  // slot kt - 1 has been consumed by an earlier MFMA or unpack, so it is
-  // complete before the barrier and the slot can be refilled.
-  //
-  // Each k32 step is fenced into three phases the compiler may not reorder:
-  // the LDS reads of the next step, the MFMAs of the first A fragment (which
-  // cover the read latency), and the remaining MFMAs with the expansion of
-  // the next step's B words slotted between them.
-  constexpr int kFirst = FN;                     // MFMAs in phase 2
-  constexpr int kRest = FM * FN - kFirst;        // MFMAs in phase 3
-  constexpr int kUnpackValu = 7 * FN;            // VALU of one unpack
   // The tile's per-row dequantisation inputs (q_rowsum, then a_scale) go
   // into LDS by LDS-DMA too, one 64-row chunk per wave, ahead of the ring's
   // first stages, so the prologue's wait covers them and the epilogue finds
@@ -259,54 +261,61 @@ __global__ __launch_bounds__((Tiling<BM, BN, WM, WN, BK, S>::kThreads)) void gem
                  : "s"(dst), "v"(off), "s"(desc)
                  : "memory", "m0");
   }
+  // Prologue: stages 0 .. S-2, wait for stage 0 (and the row factors).
 #pragma unroll
-  for (int p = 0; p < S - 1; ++p) issue(p);
+  for (int p = 0; p < S - 1; ++p)
+#pragma unroll
+    for (int i = 0; i < T::kLoadsPerStage; ++i) issue_one(p, i);
   __builtin_amdgcn_s_waitcnt(MMF_WAIT_VM((S - 2) * T::kLoadsPerStage));
   __builtin_amdgcn_s_barrier();
-  read_frags(0, 0, 0);
-  unpack(0);
-  int fb = 0;  // fragment buffer of the current step
-  for (int kt = 0; kt < KT; ++kt) {
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      __builtin_amdgcn_sched_barrier(0);
-      if (ks + 1 < KS) {
-        read_frags(kt, ks + 1, fb ^ 1);
-      } else {
-        __builtin_amdgcn_s_waitcnt(MMF_WAIT_VM((S - 3) * T::kLoadsPerStage));
-        __builtin_amdgcn_s_barrier();
-        issue(kt + S - 1);
-        // unconditional (after the last stage it reads a slot of zeros), so
-        // that the loop body stays one block the fences can order
-        read_frags(kt + 1, 0, fb ^ 1);
-      }
-      __builtin_amdgcn_sched_barrier(0);
+  for (int fm = 0; fm < FM; ++fm) af[fm] = a_read(0, fm);
+#pragma unroll
+  for (int f = 0; f < FN; ++f) bw[f] = b_read(0, f);
+#pragma unroll
+  for (int f = 0; f < FN; ++f) be[0][f] = expand(bw[f]);
+
+  // One k64 step s (stage kt = s / KS): the MFMAs of step s, the fragment
+  // reads of step s + 1 and the expansion of its words.  The last step of a
+  // stage reads the next stage: it first waits for its own loads of that
+  // stage (with S = 3 nothing younger is in flight) and passes a barrier,
+  // which makes every wave's loads visible and certifies that every wave has
+  // consumed the oldest slot (its data fed MFMAs of earlier steps); that
+  // slot is then refilled with stage kt + S - 1, one load per fragment group.
+  auto step = [&](int s, v4i (&bc)[FN], v4i (&bn)[FN]) {
+    const int kt = s / KS, ks = s % KS;
+    const bool refill = (ks == KS - 1);
+    __builtin_amdgcn_sched_barrier(0);
+    if (refill) {
+      __builtin_amdgcn_s_waitcnt(MMF_WAIT_VM((S - 3) * T::kLoadsPerStage));
+      __builtin_amdgcn_s_barrier();
+    }
+#pragma unroll
+    for (int f = 0; f < FN; ++f) bw[f] = b_read(s + 1, f);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int fm = 0; fm < FM; ++fm) {
 #pragma unroll
       for (int f = 0; f < FN; ++f)
-        acc[0][f] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[fb][0], bf[fb][f], acc[0][f], 0, 0, 0);
+        acc[fm][f] = __builtin_amdgcn_mfma_i32_16x16x64_i8(bc[f], af[fm], acc[fm][f], 0, 0, 0);
+      af[fm] = a_read(s + 1, fm);
+      if (refill && fm < T::kLoadsPerStage) issue_one(kt + S - 1, fm);
+      if (fm >= FM - FN) bn[fm - (FM - FN)] = expand(bw[fm - (FM - FN)]);
       __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-      for (int fm = 1; fm < FM; ++fm)
-#pragma unroll
-        for (int f = 0; f < FN; ++f)
-          acc[fm][f] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[fb][fm], bf[fb][f], acc[fm][f], 0, 0, 0);
-      unpack(fb ^ 1);
-      if constexpr (kRest > 0) {
-#pragma unroll
-        for (int i = 0; i < kRest; ++i) {
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                                  // MFMA
-          __builtin_amdgcn_sched_group_barrier(0x002, (kUnpackValu + kRest - 1) / kRest, 0);  // VALU
-        }
-      }
-      __builtin_amdgcn_sched_barrier(0);
-      (void)kFirst;
-      fb ^= 1;
     }
+  };
+  const int steps = KT * KS;
+  int s = 0;
+  for (; s + 1 < steps; s += 2) {
+    step(s, be[0], be[1]);
+    step(s + 1, be[1], be[0]);
   }
+  if (s < steps) step(s, be[0], be[1]);
   // no LDS-DMA write may still be in flight when the workgroup's LDS is freed
   __builtin_amdgcn_s_waitcnt(MMF_WAIT_VM_LGKM0(0));
 
-  // ---- epilogue: lane holds column l32, rows 8*(r/4) + 4*g + r%4 ----
+  // ---- epilogue: the MFMA computed the transposed product, so lane
+  // (g, l16) holds row l16 and columns 4 g .. 4 g + 3 of each 16 x 16 block ----
   const int* s_rsum = reinterpret_cast<const int*>(smem + S * T::kStageBytes);
   const float* s_scale = reinterpret_cast<const float*>(smem + S * T::kStageBytes + 4 * BM);
   const float ws = (EP == Epilogue::kDequantF32) ? w_scale[0] : 0.0f;
@@ -316,33 +325,41 @@ __global__ __launch_bounds__((Tiling<BM, BN, WM, WN, BK, S>::kThreads)) void gem
   const uint32_t out_bytes = static_cast<uint32_t>(M) * static_cast<uint32_t>(N) * 4u;
   const __amdgpu_buffer_rsrc_t orsrc =
       __builtin_amdgcn_make_buffer_rsrc(out, 0, static_cast<int>(out_bytes), kBufferFlags);
+  constexpr uint32_t kOut = 0x80000000u;
 #pragma unroll
   for (int fm = 0; fm < FM; ++fm) {
+    const int lr = wm * WM + fm * 16 + l16;
+    const bool row_ok = m0 + lr < M;
+    const int rs = s_rsum[lr];
+    const float sc = s_scale[lr] * ws;
+    const uint32_t row_bytes = static_cast<uint32_t>(m0 + lr) * static_cast<uint32_t>(N) * 4u;
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int lr = wm * WM + fm * 32 + 8 * (r >> 2) + 4 * g + (r & 3);
-      const int rs = s_rsum[lr];
-      const float sc = s_scale[lr] * ws;
-      const uint32_t row_bytes = static_cast<uint32_t>(m0 + lr) * static_cast<uint32_t>(N) * 4u;
+    for (int f = 0; f < FN; ++f) {
+      const int n = n0 + wn * WN + f * 16 + 4 * g;
+      v4i v;
 #pragma unroll
-      for (int f = 0; f < FN; ++f) {
-        const int n = n0 + wn * WN + f * 32 + l32;
-        const uint32_t off = (m0 + lr < M && n < N) ? row_bytes + 4u * static_cast<uint32_t>(n) : 0x80000000u;
-        const int v = acc[fm][f][r] - rs;
-        if constexpr (EP == Epilogue::kDequantF32)
-          __builtin_amdgcn_raw_buffer_store_b32(static_cast<uint32_t>(__float_as_int(static_cast<float>(v) * sc)),
-                                                orsrc, off, 0, 0);
-        else
-          __builtin_amdgcn_raw_buffer_store_b32(static_cast<uint32_t>(v), orsrc, off, 0, 0);
+      for (int r = 0; r < 4; ++r) {
+        const int d = acc[fm][f][r] - rs;
+        v[r] = (EP == Epilogue::kDequantF32) ? __float_as_int(static_cast<float>(d) * sc) : d;
+      }
+      if constexpr (BX4) {
+        // N % 4 == 0: the four columns are all inside or all past N
+        const uint32_t off = (row_ok && n < N) ? row_bytes + 4u * static_cast<uint32_t>(n) : kOut;
+        __builtin_amdgcn_raw_buffer_store_b128(v, orsrc, off, 0, 0);
+      } else {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const uint32_t off = (row_ok && n + r < N) ? row_bytes + 4u * static_cast<uint32_t>(n + r) : kOut;
+          __builtin_amdgcn_raw_buffer_store_b32(static_cast<uint32_t>(v[r]), orsrc, off, 0, 0);
+        }
       }
     }
   }
 }
 
-template <int BM, int BN, int WM, int WN, int BK, int S>
+template <int BM, int BN, int WM, int WN, int BK, int S, bool BX4>
 hipError_t launch_cfg(const ContractArgs& a, int64_t m_begin, int64_t m_rows, hipStream_t stream) {
-  using T = Tiling<BM, BN, WM, WN, BK, S>;
-  const int lds = 0;  // the ring is static LDS
+  using T = Tiling<BM, BN, WM, WN, BK, S, BX4>;
   const int64_t gm = (m_rows + BM - 1) / BM;
   const int64_t gn = (a.N + BN - 1) / BN;
   const dim3 grid(static_cast<unsigned>(gm * gn));
@@ -351,13 +368,13 @@ hipError_t launch_cfg(const ContractArgs& a, int64_t m_begin, int64_t m_rows, hi
   const float* as = a.a_scale ? a.a_scale + m_begin : nullptr;
   const int32_t* rs = a.q_rowsum + m_begin;
   if (a.epilogue == Epilogue::kDequantF32)
-    hipLaunchKernelGGL((gemm_kernel<BM, BN, WM, WN, BK, S, Epilogue::kDequantF32>), grid, block, lds, stream,
-                       q, as, rs, a.Wpacked, a.w_scale,
+    hipLaunchKernelGGL((gemm_kernel<BM, BN, WM, WN, BK, S, BX4, Epilogue::kDequantF32>), grid, block, 0,
+                       stream, q, as, rs, a.Wpacked, a.w_scale,
                        static_cast<void*>(static_cast<float*>(a.out) + m_begin * a.N),
                        static_cast<int>(m_rows), a.K, static_cast<int>(a.N));
   else
-    hipLaunchKernelGGL((gemm_kernel<BM, BN, WM, WN, BK, S, Epilogue::kRawI32>), grid, block, lds, stream,
-                       q, as, rs, a.Wpacked, a.w_scale,
+    hipLaunchKernelGGL((gemm_kernel<BM, BN, WM, WN, BK, S, BX4, Epilogue::kRawI32>), grid, block, 0,
+                       stream, q, as, rs, a.Wpacked, a.w_scale,
                        static_cast<void*>(static_cast<int32_t*>(a.out) + m_begin * a.N),
                        static_cast<int>(m_rows), a.K, static_cast<int>(a.N));
   return hipGetLastError();
@@ -375,9 +392,11 @@ hipError_t launch_gemm(const ContractArgs& a, hipStream_t stream) {
   int64_t slice = by_q < by_y ? by_q : by_y;
   slice = (slice / 256) * 256;
   if (slice < 256) return hipErrorInvalidValue;
+  const bool bx4 = (a.N % 4) == 0;
   for (int64_t m0 = 0; m0 < a.M; m0 += slice) {
     const int64_t rows = a.M - m0 < slice ? a.M - m0 : slice;
-    const hipError_t e = launch_cfg<256, 256, 64, 128, 64, 4>(a, m0, rows, stream);
+    const hipError_t e = bx4 ? launch_cfg<256, 256, 128, 64, 128, 3, true>(a, m0, rows, stream)
+                             : launch_cfg<256, 256, 128, 64, 128, 3, false>(a, m0, rows, stream);
     if (e != hipSuccess) return e;
   }
   return hipSuccess;
