@@ -10,7 +10,6 @@ namespace mmf {
 namespace {
 
 constexpr int kRowsPerBlock = 4;  // 4 waves, one row each
-constexpr float kEps = 1e-6f;
 
 // 16-byte vector of activations: 8 bf16 or 4 fp32.
 template <typename XT> struct Vec;
@@ -55,10 +54,7 @@ __device__ __forceinline__ int quantise(float y, float s) {
   return static_cast<int>(v);
 }
 
-__device__ __forceinline__ float row_rstd(double ss, int K) {
-  double ms = ss / static_cast<double>(K);
-  return static_cast<float>(1.0 / sqrt(ms + static_cast<double>(kEps)));
-}
+__device__ __forceinline__ float row_rstd(double ss, int K) { return rms_rstd(ss, K); }
 
 // VPL > 0: each lane keeps up to VPL 16-byte vectors of its row in registers
 // (rows of at most 64 * VPL vectors).  VPL == 0: any K; the row is re-read

@@ -32,10 +32,8 @@ constexpr int kMaxTokens = 8;
 constexpr int kMaxRowWaves = 4;           // waves that normalise one token row
 constexpr int kLdsDmaChunk = 1024;        // bytes of q one LDS-DMA wave instruction copies
 constexpr int kMaxQChunks = (kDecodeMaxLdsQ / kLdsDmaChunk + kWaves - 1) / kWaves;  // per wave
-constexpr float kEps = 1e-6f;
+constexpr int kWeightDelay = -1;         // < 0: all waves wait for the row waves' x
 constexpr int kGridRound = 256;           // workgroups that run at once (one per CU)
-constexpr bool kEarlyNorm = true;         // row waves reduce x before issuing weight loads
-constexpr bool kXFirst = true;            // every wave waits for that before its weight loads
 
 enum class Src { kBf16, kF32, kQuantised };
 
@@ -128,13 +126,20 @@ struct RowStage {
       const int sv = (active && v < nvec) ? v : 0;
       xr[p] = xrow[sv];
     }
-    if (gamma != nullptr) {
+    // gamma through a buffer resource of size 0 when it is NULL: the loads
+    // then return zeros without touching memory, and no branch separates them
+    // from the weight loads that follow (so a wait for x and gamma need not
+    // wait for the weights too)
+    const __amdgpu_buffer_rsrc_t grsrc = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float*>(gamma), 0, gamma != nullptr ? K * 4 : 0, 0x00020000);
 #pragma unroll
-      for (int p = 0; p < VP; ++p) {
-        const int v = gtid + G * kWave * p;
-        const int sv = (active && v < nvec) ? v : 0;
+    for (int p = 0; p < VP; ++p) {
+      const int v = gtid + G * kWave * p;
+      const int sv = (active && v < nvec) ? v : 0;
 #pragma unroll
-        for (int e4 = 0; e4 < E / 4; ++e4) gr[p][e4] = reinterpret_cast<const float4*>(gamma + sv * E)[e4];
+      for (int e4 = 0; e4 < E / 4; ++e4) {
+        const uint32_t off = static_cast<uint32_t>((sv * E + 4 * e4) * 4);
+        gr[p][e4] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(grsrc, off, 0, 0));
       }
     }
   }
@@ -195,7 +200,7 @@ struct RowStage {
     if (active) {
       double tot = 0.0;
       for (int w = 0; w < G; ++w) tot += sh.slot_d[w0 + w];
-      const float r = static_cast<float>(1.0 / sqrt(tot / static_cast<double>(K) + static_cast<double>(kEps)));
+      const float r = rms_rstd(tot, K);
       float amax = 0.0f;
 #pragma unroll
       for (int p = 0; p < VP; ++p)
@@ -326,6 +331,8 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(const Params prm) {
   const int K = prm.K;
   const int64_t N = prm.N;
   const Shared sh = carve(smem, prm.q_bytes);
+  // read at entry: its latency then overlaps the rest of the kernel
+  const float wscale = EP == Epilogue::kDequantF32 ? prm.w_scale[0] : 0.0f;
   constexpr int C = kWave / H;  // columns per workgroup
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -347,58 +354,61 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(const Params prm) {
   const uint32_t slot_bytes = static_cast<uint32_t>(H) * row_bytes;
   const uint32_t wave_bytes = static_cast<uint32_t>(jb) * row_bytes;
 
-  // 1. activation loads
+  // 1. activation loads.  The waves that normalise the token rows wait for
+  //    them and reduce sum x^2 before any weight load is issued, and every
+  //    wave waits for that: x and gamma then cross a quiet memory system
+  //    (issued together with 3 MB of weight misses they return late), and
+  //    the rest of the norm overlaps the weight stream.
   RowStage<MT, S == Src::kQuantised ? Src::kBf16 : S, VP> rows;
   QStage<MT> qs;
-  if constexpr (S == Src::kQuantised)
+  if constexpr (S == Src::kQuantised) {
     qs.load(prm.q, prm.a_scale, prm.q_rowsum, K, sh);
-  else
+  } else {
     rows.load(prm.x, prm.gamma, K);
-  __builtin_amdgcn_sched_barrier(0);  // keep these loads ahead of the weight loads
-  // The row waves wait for their activations before issuing weight loads:
-  // x then crosses a quiet memory system instead of queueing behind every
-  // CU's weight misses, and the norm below overlaps the weight stream.  The
-  // other waves issue their weight loads at once.
-  if constexpr (kEarlyNorm && S != Src::kQuantised) rows.begin(sh);
-  if constexpr (kXFirst && S != Src::kQuantised) __syncthreads();
-  __builtin_amdgcn_sched_barrier(0);
-
-  // 2. the first weight slots, kPrefetch words per lane ahead of their use,
-  //    in groups of four: a group is issued only when the wave has a slot in
-  //    it (a wave-uniform branch); inside the last group, slots past the
-  //    wave's range repeat its last slot and are not used.
-  uint32_t wbuf[kPrefetch];
-  if (ns > 0) {
-#pragma unroll
-    for (int p0 = 0; p0 < kPrefetch; p0 += 4) {
-      if (p0 == 0 || p0 < ns) {
-#pragma unroll
-        for (int p = p0; p < p0 + 4; ++p) {
-          const uint32_t sp = static_cast<uint32_t>(p < ns ? p : ns - 1);
-          wbuf[p] = __builtin_amdgcn_raw_buffer_load_b32(wrsrc, lane_off, wave_bytes + sp * slot_bytes, 0);
-        }
-      }
+    if constexpr (kWeightDelay < 0) {
+      rows.begin(sh);
+      __syncthreads();
+    } else {
+      rows.begin(sh);
+      if (!rows.active) __builtin_amdgcn_s_sleep(kWeightDelay);
     }
   }
+  __builtin_amdgcn_sched_barrier(0);
+
+  // 2. every weight slot of the first prefetch group, straight-line code
+  //    (loads retire in issue order, so later waits can count them).  Slots
+  //    past the wave's range repeat its last slot (they are not used); a wave
+  //    without slots reads past the end of the buffer, which returns zeros
+  //    without a memory access.
+  uint32_t wbuf[kPrefetch];
+  const int last = ns > 0 ? ns - 1 : 0;
+#pragma unroll
+  for (int p = 0; p < kPrefetch; ++p) {
+    const uint32_t sp = static_cast<uint32_t>(p < last ? p : last);
+    wbuf[p] = __builtin_amdgcn_raw_buffer_load_b32(wrsrc, lane_off, wave_bytes + sp * slot_bytes, 0);
+  }
+  __builtin_amdgcn_sched_barrier(0);
 
   // 3. quantised activations into LDS (waits for the activation loads only)
   if (tid < kMaxTokens * kWave) sh.red[tid] = 0;
   if constexpr (S == Src::kQuantised) {
     qs.store(sh);
   } else {
-    if constexpr (!kEarlyNorm) rows.begin(sh);
-    rows.finish(prm.gamma != nullptr, K, sh, !kXFirst);
+    rows.finish(prm.gamma != nullptr, K, sh, kWeightDelay >= 0);
   }
   __syncthreads();
 
-  // 4. contraction
+  // 4. contraction.  A slot past the wave's range gets the word 0 (code 0
+  // for every k, so its dot products add nothing) and reads q at a valid
+  // row, which keeps the loop free of branches; the q vectors of the next
+  // word are read from LDS while the current word is accumulated.
   int acc[MT];
 #pragma unroll
   for (int m = 0; m < MT; ++m) acc[m] = 0;
   for (int base = 0; base < ns; base += kPrefetch) {
     uint32_t cur[kPrefetch];
 #pragma unroll
-    for (int p = 0; p < kPrefetch; ++p) cur[p] = wbuf[p];
+    for (int p = 0; p < kPrefetch; ++p) cur[p] = base + p < ns ? wbuf[p] : 0u;
     const int nb = base + kPrefetch;
 #pragma unroll
     for (int p0 = 0; p0 < kPrefetch; p0 += 4) {
@@ -410,22 +420,30 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(const Params prm) {
         }
       }
     }
+    auto q_at = [&](int p, int m) -> uint4 {
+      const int j = base + p < ns ? jb + H * (base + p) + h : jb + h;
+      return *reinterpret_cast<const uint4*>(sh.q + m * K + 16 * j);
+    };
+    uint4 qv[2][MT];
+#pragma unroll
+    for (int m = 0; m < MT; ++m) qv[0][m] = q_at(0, m);
 #pragma unroll
     for (int p = 0; p < kPrefetch; ++p) {
-      if (base + p < ns) {
-        const int j = jb + H * (base + p) + h;
-        const uint32_t w = cur[p];
-        const uint32_t c0 = codes4(w, 0), c1 = codes4(w, 1), c2 = codes4(w, 2), c3 = codes4(w, 3);
+      if (p + 1 < kPrefetch) {
 #pragma unroll
-        for (int m = 0; m < MT; ++m) {
-          const uint4 qv = *reinterpret_cast<const uint4*>(sh.q + m * K + 16 * j);
-          int a = acc[m];
-          a = dot4(c0, qv.x, a);
-          a = dot4(c1, qv.y, a);
-          a = dot4(c2, qv.z, a);
-          a = dot4(c3, qv.w, a);
-          acc[m] = a;
-        }
+        for (int m = 0; m < MT; ++m) qv[(p + 1) & 1][m] = q_at(p + 1, m);
+      }
+      const uint32_t w = cur[p];
+      const uint32_t c0 = codes4(w, 0), c1 = codes4(w, 1), c2 = codes4(w, 2), c3 = codes4(w, 3);
+#pragma unroll
+      for (int m = 0; m < MT; ++m) {
+        const uint4 q4 = qv[p & 1][m];
+        int a = acc[m];
+        a = dot4(c0, q4.x, a);
+        a = dot4(c1, q4.y, a);
+        a = dot4(c2, q4.z, a);
+        a = dot4(c3, q4.w, a);
+        acc[m] = a;
       }
     }
   }
@@ -449,7 +467,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(const Params prm) {
     if (nn < N) {
       const int v = sh.red[m * kWave + cc] - rsum;
       if constexpr (EP == Epilogue::kDequantF32)
-        static_cast<float*>(prm.out)[m * N + nn] = static_cast<float>(v) * (sh.a_scale[m] * prm.w_scale[0]);
+        static_cast<float*>(prm.out)[m * N + nn] = static_cast<float>(v) * (sh.a_scale[m] * wscale);
       else
         static_cast<int32_t*>(prm.out)[m * N + nn] = v;
     }
@@ -532,7 +550,8 @@ hipError_t dispatch_mt(int mt, const DecodeArgs& a, hipStream_t stream) {
 
 bool decode_fits(int64_t mt, int K, int64_t N, bool from_x, bool x_is_f32) {
   if (mt < 1 || mt > kMaxTokens || mt * K > kDecodeMaxLdsQ) return false;
-  if (static_cast<int64_t>(K / 16) * N * 4 >= (int64_t(1) << 32)) return false;  // 32-bit offsets
+  // 32-bit offsets: the packed array plus the slack of clamped slot offsets
+  if (static_cast<int64_t>(K / 16 + 8) * N * 4 >= (int64_t(1) << 32)) return false;
   if (!from_x) return true;
   return needed_vp(mt, K, x_is_f32) <= 4;
 }

@@ -10,9 +10,10 @@ constexpr int kWave = 64;
 
 // ---------------------------------------------------------------------------
 // wave64 all-reductions.  Steps: DPP quad_perm xor 1, xor 2, row_half_mirror,
-// row_mirror (each row of 16 lanes then holds its total), ds_swizzle xor 16
-// (each half-wave holds its total), and a readlane of lanes 0 and 32.  The
-// combination order is fixed, so every call returns the same bits.
+// row_mirror (each row of 16 lanes then holds its total), then readlane of
+// lanes 0, 16, 32 and 48 and the combination (r0 + r1) + (r2 + r3) on
+// wave-uniform values.  The combination order is fixed, so every call
+// returns the same bits; no LDS round trip is involved.
 // ---------------------------------------------------------------------------
 template <int CTRL>
 __device__ __forceinline__ int dpp_i32(int v) {
@@ -23,7 +24,6 @@ constexpr int kDppXor1 = 0xB1;        // quad_perm [1,0,3,2]
 constexpr int kDppXor2 = 0x4E;        // quad_perm [2,3,0,1]
 constexpr int kDppHalfMirror = 0x141; // row_half_mirror
 constexpr int kDppMirror = 0x140;     // row_mirror
-constexpr int kSwizzleXor16 = 0x401F; // ds_swizzle bit mode: and 0x1F, xor 0x10
 
 struct I32Parts {
   int lo, hi;
@@ -50,21 +50,14 @@ __device__ __forceinline__ float dpp_f32(float v) {
   return __int_as_float(dpp_i32<CTRL>(__float_as_int(v)));
 }
 
-__device__ __forceinline__ int swz_xor16_i32(int v) {
-  return __builtin_amdgcn_ds_swizzle(v, kSwizzleXor16);
-}
-__device__ __forceinline__ double swz_xor16_f64(double v) {
-  I32Parts p = split(v);
-  p.lo = swz_xor16_i32(p.lo);
-  p.hi = swz_xor16_i32(p.hi);
-  return join(p);
-}
-
 __device__ __forceinline__ double readlane_f64(double v, int lane) {
   I32Parts p = split(v);
   p.lo = __builtin_amdgcn_readlane(p.lo, lane);
   p.hi = __builtin_amdgcn_readlane(p.hi, lane);
   return join(p);
+}
+__device__ __forceinline__ float readlane_f32(float v, int lane) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), lane));
 }
 
 __device__ __forceinline__ double wave_sum_f64(double v) {
@@ -72,8 +65,7 @@ __device__ __forceinline__ double wave_sum_f64(double v) {
   v += dpp_f64<kDppXor2>(v);
   v += dpp_f64<kDppHalfMirror>(v);
   v += dpp_f64<kDppMirror>(v);
-  v += swz_xor16_f64(v);
-  return readlane_f64(v, 0) + readlane_f64(v, 32);
+  return (readlane_f64(v, 0) + readlane_f64(v, 16)) + (readlane_f64(v, 32) + readlane_f64(v, 48));
 }
 
 __device__ __forceinline__ float wave_max_f32(float v) {
@@ -81,9 +73,7 @@ __device__ __forceinline__ float wave_max_f32(float v) {
   v = fmaxf(v, dpp_f32<kDppXor2>(v));
   v = fmaxf(v, dpp_f32<kDppHalfMirror>(v));
   v = fmaxf(v, dpp_f32<kDppMirror>(v));
-  v = fmaxf(v, __int_as_float(swz_xor16_i32(__float_as_int(v))));
-  return fmaxf(__int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0)),
-               __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32)));
+  return fmaxf(fmaxf(readlane_f32(v, 0), readlane_f32(v, 16)), fmaxf(readlane_f32(v, 32), readlane_f32(v, 48)));
 }
 
 __device__ __forceinline__ int wave_sum_i32(int v) {
@@ -91,8 +81,48 @@ __device__ __forceinline__ int wave_sum_i32(int v) {
   v += dpp_i32<kDppXor2>(v);
   v += dpp_i32<kDppHalfMirror>(v);
   v += dpp_i32<kDppMirror>(v);
-  v += swz_xor16_i32(v);
-  return __builtin_amdgcn_readlane(v, 0) + __builtin_amdgcn_readlane(v, 32);
+  return (__builtin_amdgcn_readlane(v, 0) + __builtin_amdgcn_readlane(v, 16)) +
+         (__builtin_amdgcn_readlane(v, 32) + __builtin_amdgcn_readlane(v, 48));
+}
+
+// ---------------------------------------------------------------------------
+// RMSNorm reciprocal scale r = 1 / sqrt(sum_k x_k^2 / K + eps), eps = 1e-6,
+// returned in fp32 and equal to the fp32 rounding of the fp64 sequence
+// mean = ss / K, v = mean + eps, s = sqrt(v), r = 1 / s with every step
+// correctly rounded.
+//
+// The division by K is a multiplication when K is a power of two (exact).
+// 1/sqrt(v) is first evaluated as a hardware reciprocal-square-root estimate
+// refined by two Newton steps in fp64 (within a few fp64 ulps of the exact
+// value).  The fp64 sequence above is within 2^-52 (relative) of the exact
+// value too, so both round to the same fp32 number unless the exact value
+// lies within about 2^-49 of a midpoint between two fp32 numbers; when the
+// refined value is within 2^-44 of one (or fp32 r would not be a normal
+// number) the sequence itself is evaluated.  All inputs are wave-uniform, so
+// the branch does not diverge.
+// ---------------------------------------------------------------------------
+constexpr double kRmsEps = 1e-6;
+
+__device__ __forceinline__ float rms_rstd(double ss, int K) {
+  const double mean = (K & (K - 1)) == 0 ? ss * (1.0 / static_cast<double>(K)) : ss / static_cast<double>(K);
+  const double v = mean + kRmsEps;
+  const double h = 0.5 * v;
+  double y = __builtin_amdgcn_rsq(v);
+#pragma unroll
+  for (int it = 0; it < 2; ++it) {
+    const double e = __builtin_fma(-(h * y), y, 0.5);  // 1/2 - v y^2 / 2
+    y = __builtin_fma(y, e, y);
+  }
+  const float r = static_cast<float>(y);
+  const uint32_t bits = __float_as_uint(r);
+  const int ex = static_cast<int>((bits >> 23) & 0xFFu);
+  const double d = y - static_cast<double>(r);
+  // half the spacing of fp32 numbers on the side of r where y lies
+  double half = __builtin_ldexp(1.0, ex - 127 - 24);
+  if ((bits & 0x7FFFFFu) == 0 && d < 0.0) half *= 0.5;
+  const bool safe = ex > 0 && ex < 0xFE && __builtin_fabs(d) < half * (1.0 - 0x1p-20);
+  if (safe) return r;
+  return static_cast<float>(1.0 / __builtin_sqrt(v));
 }
 
 // ---------------------------------------------------------------------------
