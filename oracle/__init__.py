@@ -19,6 +19,11 @@ wrapper names the passage of the paper it follows:
   1/s_a times 1/s_w)
 * :func:`bitlinear_fwd`  -- the composition, Algorithm 1 ``forward_pass`` with
   bias 0
+* :func:`glu`, :func:`glu_fwd` -- the channel-mixer gate p = SiLU(g) (.) u of
+  Sec. "MatMul-free Channel Mixer", on its own and after the two
+  up-projections
+* :func:`glu_interleave` -- the library's storage order for the two
+  up-projection weights of one GLU (16-column blocks of gate and up in turn)
 """
 from __future__ import annotations
 
@@ -77,6 +82,7 @@ def _load():
     lib.oracle_bitlinear_fwd.argtypes = [P, P, P, ctypes.c_float, I64, I64, I64,
                                          ctypes.c_double, P, P, P, P, P]
     lib.oracle_bitlinear_fwd.restype = ctypes.c_int
+    lib.oracle_glu.argtypes = [P, P, I64, P]
     _lib = lib
     return lib
 
@@ -217,3 +223,42 @@ def bitlinear_fwd(x: np.ndarray, gamma: np.ndarray | None, t: np.ndarray,
     if st != 0:
         raise OverflowError("ternary sum outside int32")
     return {"y": y, "q": q, "a_scale": a, "acc": acc}
+
+
+def glu(g: np.ndarray, u: np.ndarray) -> np.ndarray:
+    """p = SiLU(g) * u elementwise (fp64, rounded to fp32 once)."""
+    g = _c(g, np.float32)
+    u = _c(u, np.float32)
+    if g.shape != u.shape:
+        raise ValueError("g and u differ in shape")
+    p = np.empty(g.shape, np.float32)
+    _load().oracle_glu(_p(g), _p(u), g.size, _p(p))
+    return p
+
+
+def glu_fwd(x: np.ndarray, gamma: np.ndarray | None, t_g: np.ndarray, w_scale_g: float,
+            t_u: np.ndarray, w_scale_u: float, eps: float = EPS):
+    """The channel mixer's up-projections and gate: g = BitLinear(x; t_g),
+    u = BitLinear(x; t_u), both after the same RMSNorm and activation
+    quantisation, then p = SiLU(g) * u.  Returns dict with p, g, u, acc_g, acc_u."""
+    og = bitlinear_fwd(x, gamma, t_g, w_scale_g, eps)
+    ou = bitlinear_fwd(x, gamma, t_u, w_scale_u, eps)
+    return {"p": glu(og["y"], ou["y"]), "g": og["y"], "u": ou["y"],
+            "acc_g": og["acc"], "acc_u": ou["acc"], "q": og["q"], "a_scale": og["a_scale"]}
+
+
+def glu_interleave(t_g: np.ndarray, t_u: np.ndarray) -> np.ndarray:
+    """Rows of the combined [2L][K] code matrix in the library's GLU order:
+    blocks of 16 gate rows and 16 up rows in turn (rows 32b .. 32b+15 are gate
+    rows 16b .. 16b+15, rows 32b+16 .. 32b+31 the up rows with the same
+    indices).  L must be a multiple of 16."""
+    t_g = np.asarray(t_g)
+    t_u = np.asarray(t_u)
+    L, K = t_g.shape
+    if t_u.shape != (L, K) or L % 16:
+        raise ValueError("gate and up must both be [L][K] with L a multiple of 16")
+    out = np.empty((2 * L, K), t_g.dtype)
+    for b in range(L // 16):
+        out[32 * b:32 * b + 16] = t_g[16 * b:16 * b + 16]
+        out[32 * b + 16:32 * b + 32] = t_u[16 * b:16 * b + 16]
+    return out

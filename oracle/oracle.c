@@ -274,3 +274,18 @@ int oracle_bitlinear_fwd(const float *x, const float *gamma, const int8_t *t,
     oracle_dequant(acc, a_scale, w_scale, M, N, y);
     return st;
 }
+
+/* ---------------------------------------------------------------------- */
+/* GLU channel-mixer gate (Sec. "MatMul-free Channel Mixer"): the gated   */
+/* representation is p = tau(g) (.) u, with g and u the outputs of the two */
+/* up-projections and tau the SiLU activation, tau(v) = v / (1 + e^-v).    */
+/* Evaluated in fp64 from the fp32 inputs and rounded to fp32 once.        */
+/* ---------------------------------------------------------------------- */
+void oracle_glu(const float *g, const float *u, int64_t n, float *p) {
+#pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < n; ++i) {
+        const double gv = (double)g[i];
+        const double silu = gv / (1.0 + exp(-gv));
+        p[i] = (float)(silu * (double)u[i]);
+    }
+}

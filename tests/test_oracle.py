@@ -303,3 +303,75 @@ def test_forward_negated_weights_and_zero_row():
 
 def test_oracle_threads_reported():
     assert oracle.num_threads() >= 1
+
+
+# --------------------------------------------------------------------------
+# GLU channel-mixer gate p = SiLU(g) * u (Sec. "MatMul-free Channel Mixer")
+# --------------------------------------------------------------------------
+
+def test_glu_closed_forms():
+    # sigmoid(ln 3) = 3/4 exactly, so SiLU(ln 3) = (3/4) ln 3; sigmoid(0) = 1/2.
+    # A sign slip in the exponent would give ln 3 / 4 here.
+    l3 = math.log(3.0)
+    g = np.array([l3, -l3, 0.0, 0.0], np.float32)
+    u = np.array([2.0, 2.0, 5.0, -7.0], np.float32)
+    p = oracle.glu(g, u).astype(np.float64)
+    g64 = float(np.float32(l3))
+    assert math.isclose(p[0], 2.0 * 0.75 * g64, rel_tol=2e-7)
+    assert math.isclose(p[1], 2.0 * -0.25 * g64, rel_tol=2e-7)   # SiLU(-v) = -v sigmoid(-v)
+    assert p[2] == 0.0 and p[3] == 0.0
+
+
+def test_glu_limits_and_odd_part():
+    v = np.array([40.0, 20.0, 3.5, 1.0, 0.25], np.float32)
+    one = np.ones_like(v)
+    plus = oracle.glu(v, one).astype(np.float64)
+    minus = oracle.glu(-v, one).astype(np.float64)
+    # SiLU(v) -> v for large v, SiLU(-v) -> 0 from below
+    assert plus[0] == 40.0 and abs(minus[0]) < 1e-15 and minus[0] <= 0.0
+    # odd part: SiLU(v) - SiLU(-v) = v (sigmoid(v) + sigmoid(-v) = 1)
+    np.testing.assert_allclose(plus - minus, v.astype(np.float64), rtol=3e-7)
+    # SiLU is positive and increasing for v > 0
+    assert np.all(plus > 0) and np.all(np.diff(plus[::-1]) > 0)
+
+
+def test_glu_linear_in_u_and_gate_role():
+    rng = np.random.default_rng(7)
+    g = rng.standard_normal(64).astype(np.float32)
+    u = rng.standard_normal(64).astype(np.float32)
+    p = oracle.glu(g, u)
+    assert np.array_equal(oracle.glu(g, 2 * u), 2 * p)          # exact: power-of-two scale
+    assert np.array_equal(oracle.glu(g, -u), -p)
+    assert not np.allclose(oracle.glu(u, g), p)                # the gate is the first operand
+    assert np.all(oracle.glu(g, np.zeros_like(u)) == 0)
+
+
+def test_glu_fwd_composition():
+    # identical gate and up weights: p = SiLU(y) * y with y the BitLinear output
+    rng = np.random.default_rng(3)
+    x = rng.standard_normal((5, 64)).astype(np.float32)
+    W = (rng.standard_normal((32, 64)) * 0.02).astype(np.float32)
+    t, ws = oracle.weight_quant(W)
+    out = oracle.glu_fwd(x, None, t, ws, t, ws)
+    y = oracle.bitlinear_fwd(x, None, t, ws)["y"]
+    assert np.array_equal(out["g"], y) and np.array_equal(out["u"], y)
+    y64 = y.astype(np.float64)
+    ref = y64 * y64 / (1.0 + np.exp(-y64))
+    np.testing.assert_allclose(out["p"], ref, rtol=1e-6, atol=1e-30)
+    # a zero activation row gives p = 0
+    x[2] = 0
+    assert np.all(oracle.glu_fwd(x, None, t, ws, t, ws)["p"][2] == 0)
+
+
+def test_glu_interleave_blocks():
+    t_g = np.arange(32 * 16, dtype=np.int32).reshape(32, 16) % 3 - 1
+    t_u = (np.arange(32 * 16, dtype=np.int32).reshape(32, 16) // 7) % 3 - 1
+    t = oracle.glu_interleave(t_g.astype(np.int8), t_u.astype(np.int8))
+    assert t.shape == (64, 16)
+    assert np.array_equal(t[0:16], t_g[0:16]) and np.array_equal(t[16:32], t_u[0:16])
+    assert np.array_equal(t[32:48], t_g[16:32]) and np.array_equal(t[48:64], t_u[16:32])
+    # packing the interleaved codes permutes whole columns of the separate packs
+    pg, pu, pgu = oracle.pack(t_g.astype(np.int8)), oracle.pack(t_u.astype(np.int8)), oracle.pack(t)
+    assert np.array_equal(pgu[:, 16:32], pu[:, 0:16]) and np.array_equal(pgu[:, 32:48], pg[:, 16:32])
+    with pytest.raises(ValueError):
+        oracle.glu_interleave(t_g[:24].astype(np.int8), t_u[:24].astype(np.int8))
