@@ -11,6 +11,12 @@ Workloads (shapes in workloads.py):
       of algorithmic bytes (packed weights + x + gamma + y per call).
   glu_up, glu_down, large, tiny -- prefill: a step is one forward over all M
       tokens.  value = effective TOPS, 2*M*N*K / step time.
+  glu_gate -- the GLU channel mixer's fused up-projections and gate on the
+      glu_up shape (M=8192, K=2048, L=5632): p = SiLU(g) * u in one contraction
+      over the interleaved gate|up weights.  value = effective TOPS, 2*M*2L*K.
+  channel_mixer -- the whole GLU channel mixer on that shape: glu_gate, then
+      the down-projection BitLinear of p (K=5632, N=2048, its own RMSNorm).
+      value = effective TOPS over both contractions.
 
 The JSON line carries the roofline of the dominant kernel (decode: the fused
 decode kernel, the only launch of a decode forward; prefill: the contraction),
@@ -37,6 +43,7 @@ METRIC = "prefill effective TOPS (2·M·N·K) vs int8 MFMA peak; decode HBM GB/s
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 INT8_PEAK_TOPS = 5000.0        # MI355X dense int8 MFMA, TOPS (5.0 POPS)
 DECODE = ("decode_m1", "decode_m8", "large_dec")
+GLU = ("glu_gate", "channel_mixer")
 ROTATE_BYTES = 1 << 30         # distinct packed weights per decode step
 
 
@@ -368,6 +375,87 @@ def bench_prefill(torch, mmf, w, args):
     return result
 
 
+def bench_glu(torch, mmf, name, args):
+    """glu_gate / channel_mixer on the GLU up-projection shape."""
+    import workloads
+    w = workloads.WORKLOADS["glu_up"]
+    L = w.N // 2
+    dev, x, gamma, Wp, ws = setup_common(torch, mmf, w)
+    Wgu = mmf.glu_pack(Wp[:, :L].contiguous(), Wp[:, L:].contiguous())
+    del Wp
+    w_scales = torch.cat([ws, ws])
+    log(f"[bench] {name}: M={w.M} K={w.K} L={L}")
+    p = torch.empty((w.M, L), dtype=torch.float32, device=dev)
+    wsb = torch.empty(mmf.mmf_bitlinear_workspace_bytes(w.M, w.K), dtype=torch.uint8, device=dev)
+    q = torch.empty((w.M, w.K), dtype=torch.int8, device=dev)
+    a = torch.empty((w.M,), dtype=torch.float32, device=dev)
+    rs = torch.empty((w.M,), dtype=torch.int32, device=dev)
+    mmf.mmf_act_quant(x, gamma, q, a, rs)
+    ops_glu = 2 * w.M * w.N * w.K
+    config = {"workload": name, "M": w.M, "K": w.K, "L": L, "x_dtype": w.x_dtype}
+    if name == "glu_gate":
+        def step():
+            mmf.mmf_glu_fwd_ws(x, gamma, Wgu, w_scales, p, wsb)
+        ops = ops_glu
+    else:
+        wd = workloads.WORKLOADS["glu_down"]
+        Wdp, wsd = mmf.ternarize(torch.from_numpy(workloads.make_w(wd)).to(dev))
+        gd = torch.from_numpy(workloads.make_gamma(wd)).to(dev)
+        y = torch.empty((w.M, wd.N), dtype=torch.float32, device=dev)
+        wsb2 = torch.empty(mmf.mmf_bitlinear_workspace_bytes(w.M, L), dtype=torch.uint8, device=dev)
+
+        def step():
+            mmf.mmf_glu_fwd_ws(x, gamma, Wgu, w_scales, p, wsb)
+            mmf.mmf_bitlinear_fwd_ws(p, gd, Wdp, wsd, y, wsb2)
+        ops = ops_glu + 2 * w.M * wd.N * L
+        config.update({"N_down": wd.N})
+    timer = Timer(torch)
+    ms_step = timer.time(step, args.steps, args.warmup)
+    ms_gemm = timer.time(lambda: mmf.mmf_ternary_gemm_glu(q, a, rs, Wgu, w_scales, p),
+                         args.steps, args.warmup)
+    gemm_tops = ops_glu / (ms_gemm * 1e-3) / 1e12
+    return {
+        "value": ops / (ms_step * 1e-3) / 1e12, "unit": "TOPS", "ms_per_step": ms_step,
+        "config": config,
+        "roofline": {"bound": "mfma", "kernel": "gemm_kernel with the GLU epilogue "
+                                                 "(gate|up contraction + SiLU(g) * u)",
+                     "achieved": gemm_tops, "peak": INT8_PEAK_TOPS, "unit": "TFLOP/s",
+                     "frac": gemm_tops / INT8_PEAK_TOPS, "traffic": None,
+                     "ops_per_launch": ops_glu, "avg_launch_us": ms_gemm * 1e3},
+    }, ops
+
+
+def cpu_baseline_glu(name, seconds):
+    """The oracle (two BitLinears, the gate; for channel_mixer also the down
+    projection) on a sample of token rows, in effective TOPS."""
+    import oracle
+    import workloads
+    w = workloads.WORKLOADS["glu_up"]
+    L = w.N // 2
+    _, xf = workloads.make_x(w)
+    g = workloads.make_gamma(w)
+    t, ws = oracle.weight_quant(workloads.make_w(w))
+    t_g, t_u = t[:L], t[L:]
+    down = None
+    if name == "channel_mixer":
+        wd = workloads.WORKLOADS["glu_down"]
+        td, wsd = oracle.weight_quant(workloads.make_w(wd))
+        down = (td, wsd, workloads.make_gamma(wd), wd.N)
+    rows = 4
+    while True:
+        t0 = time.perf_counter()
+        pr = oracle.glu_fwd(xf[:rows], g, t_g, ws, t_u, ws)["p"]
+        if down is not None:
+            oracle.bitlinear_fwd(pr, down[2], down[0], down[1])
+        el = time.perf_counter() - t0
+        if el >= seconds / 4 or rows >= w.M:
+            break
+        rows = min(w.M, rows * max(2, int(seconds / 4 / max(el, 1e-3))))
+    ops = 2.0 * rows * w.N * w.K + (2.0 * rows * down[3] * L if down else 0.0)
+    return {"value": ops / el / 1e12, "unit": "TOPS", "cores": oracle.num_threads(),
+            "kind": "oracle", "sample": f"{rows} of {w.M} token rows in {el:.1f} s"}
+
+
 def cpu_baseline(w, fb, seconds):
     """The oracle, as it stands, on a bounded sample of the same workload."""
     import numpy as np
@@ -414,8 +502,11 @@ def main():
     import paper_2406_02528_amd as mmf
     import workloads
     assert torch.cuda.is_available(), "bench.py needs a HIP device"
-    w = workloads.WORKLOADS[args.workload]
-    if w.name in DECODE:
+    w = None if args.workload in GLU else workloads.WORKLOADS[args.workload]
+    if w is None:
+        res, _ = bench_glu(torch, mmf, args.workload, args)
+        fb = None
+    elif w.name in DECODE:
         res, fb = bench_decode(torch, mmf, w, args)
     else:
         res = bench_prefill(torch, mmf, w, args)
@@ -430,7 +521,7 @@ def main():
     for k in ("hot_cache_call_us", "act_quant", "contraction_only", "launch_floor"):
         if k in res:
             line[k] = res[k]
-    if not args.no_secondary and w.name in DECODE:
+    if not args.no_secondary and w is not None and w.name in DECODE:
         sw = workloads.WORKLOADS["glu_up"]
         log("[bench] secondary: glu_up prefill")
         sec = bench_prefill(torch, mmf, sw, args)
@@ -444,7 +535,8 @@ def main():
         calib_copy(torch)
     if not args.no_cpu_baseline:
         log("[bench] cpu baseline (oracle)")
-        line["cpu_baseline"] = cpu_baseline(w, fb, args.cpu_seconds)
+        line["cpu_baseline"] = (cpu_baseline_glu(args.workload, args.cpu_seconds) if w is None
+                                else cpu_baseline(w, fb, args.cpu_seconds))
     print(json.dumps(line), flush=True)
 
 

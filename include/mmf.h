@@ -170,6 +170,50 @@ int mmf_ternary_gemm_i32(const int8_t *q, const uint32_t *Wpacked,
                          hipStream_t stream);
 
 /*
+ * GLU channel mixer, up-projections and gate (Sec. "MatMul-free Channel
+ * Mixer": g = x (*) W_g, u = x (*) W_u, p = SiLU(g) (.) u, SiLU(v) =
+ * v / (1 + e^-v)), fused into one contraction.
+ *
+ * Both projections see the same RMSNorm (one gamma) and the same int8
+ * activations, as the concatenated gate|up projection of the BitLinear above;
+ * each keeps its own weight scale.  For token m and channel i:
+ *   g = fp32(acc_g) * (a_scale[m] * w_scales[0])     (as y of mmf_bitlinear_fwd)
+ *   u = fp32(acc_u) * (a_scale[m] * w_scales[1])
+ * with acc_g, acc_u the exact ternary sums of the gate and up channel i.
+ *   p[m][i] = g / (1 + expf(-g)) * u                    (fp32)
+ *
+ * mmf_glu_pack interleaves the packed gate and up projections, [K/16][L]
+ * words each (as written by mmf_ternarize_weights for [L][K] latent
+ * weights), into Wgu_packed [K/16][2L]: blocks of 16 columns, gate channels
+ * 16b .. 16b + 15, then the up channels with the same indices, in turn.
+ * L must be a multiple of 16 (MMF_ERR_SHAPE otherwise).
+ *
+ * mmf_glu_fwd: x [M][K] bf16 bits (mmf_glu_fwd_f32: float32); gamma [K] or
+ * NULL; Wgu_packed [K/16][2L] from mmf_glu_pack; w_scales [2] = gate, up;
+ * p [M][L] float32 out.  Every M runs the int8 MFMA kernel.  Allocates the
+ * same stream-ordered scratch as mmf_bitlinear_fwd; mmf_glu_fwd_ws takes
+ * caller scratch of mmf_bitlinear_workspace_bytes(M, K) bytes instead.
+ */
+int mmf_glu_pack(const uint32_t *Wg_packed, const uint32_t *Wu_packed, int64_t L,
+                 int64_t K, uint32_t *Wgu_packed, hipStream_t stream);
+int mmf_glu_fwd(const uint16_t *x, const float *gamma, const uint32_t *Wgu_packed,
+                const float *w_scales, float *p, int64_t M, int64_t K, int64_t L,
+                hipStream_t stream);
+int mmf_glu_fwd_f32(const float *x, const float *gamma, const uint32_t *Wgu_packed,
+                    const float *w_scales, float *p, int64_t M, int64_t K, int64_t L,
+                    hipStream_t stream);
+int mmf_glu_fwd_ws(const void *x, int x_is_f32, const float *gamma,
+                   const uint32_t *Wgu_packed, const float *w_scales, float *p,
+                   int64_t M, int64_t K, int64_t L, void *workspace,
+                   size_t workspace_bytes, hipStream_t stream);
+/* The contraction stage of mmf_glu_fwd on its own, from quantised
+ * activations (q, a_scale, q_rowsum as written by mmf_act_quant); always the
+ * int8 MFMA kernel.  Allocates nothing. */
+int mmf_ternary_gemm_glu(const int8_t *q, const float *a_scale, const int32_t *q_rowsum,
+                         const uint32_t *Wgu_packed, const float *w_scales, float *p,
+                         int64_t M, int64_t K, int64_t L, hipStream_t stream);
+
+/*
  * Kernel selection for the contraction: MMF_PATH_AUTO (decode kernel for
  * M <= 8, MFMA kernel otherwise), MMF_PATH_GEMV or MMF_PATH_GEMM force one
  * kernel for every M (the decode kernel handles at most 8 tokens per launch

@@ -50,6 +50,12 @@ _SIGNATURES = {
     "mmf_ternary_gemm_dequant": ([_P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _P], ctypes.c_int),
     "mmf_ternary_gemm_i32": ([_P, _P, _P, _I64, _I64, _I64, _P], ctypes.c_int),
     "mmf_set_path": ([ctypes.c_int], ctypes.c_int),
+    "mmf_glu_pack": ([_P, _P, _I64, _I64, _P, _P], ctypes.c_int),
+    "mmf_glu_fwd": ([_P, _P, _P, _P, _P, _I64, _I64, _I64, _P], ctypes.c_int),
+    "mmf_glu_fwd_f32": ([_P, _P, _P, _P, _P, _I64, _I64, _I64, _P], ctypes.c_int),
+    "mmf_glu_fwd_ws": ([_P, ctypes.c_int, _P, _P, _P, _P, _I64, _I64, _I64, _P, _SZ, _P],
+                       ctypes.c_int),
+    "mmf_ternary_gemm_glu": ([_P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _P], ctypes.c_int),
 }
 for _name, (_args, _res) in _SIGNATURES.items():
     _f = getattr(_lib, _name)
@@ -213,6 +219,68 @@ def mmf_ternary_gemm_i32(q: torch.Tensor, Wpacked: torch.Tensor, acc: torch.Tens
     _check(_lib.mmf_ternary_gemm_i32(_ptr(q), _ptr(Wpacked), _ptr(acc), M, K, N, _stream(stream)))
 
 
+def mmf_glu_pack(Wg_packed: torch.Tensor, Wu_packed: torch.Tensor, Wgu_packed: torch.Tensor,
+                 stream=None) -> None:
+    """Interleave the packed gate and up projections [K/16][L] into [K/16][2L]
+    (16-column blocks of gate and up in turn); L % 16 == 0."""
+    J, L = Wg_packed.shape
+    _need(Wg_packed, "Wg_packed", torch.int32, (J, L))
+    _need(Wu_packed, "Wu_packed", torch.int32, (J, L))
+    _need(Wgu_packed, "Wgu_packed", torch.int32, (J, 2 * L))
+    _check(_lib.mmf_glu_pack(_ptr(Wg_packed), _ptr(Wu_packed), L, 16 * J, _ptr(Wgu_packed),
+                             _stream(stream)))
+
+
+def _glu_args(x, gamma, Wgu_packed, w_scales, p):
+    M, K = x.shape
+    L = Wgu_packed.shape[1] // 2
+    is_f32 = _x_kind(x)
+    _need(x, "x", x.dtype, (M, K))
+    if gamma is not None:
+        _need(gamma, "gamma", torch.float32, (K,))
+    _need(Wgu_packed, "Wgu_packed", torch.int32, (K // 16, 2 * L))
+    _need(w_scales, "w_scales", torch.float32, (2,))
+    _need(p, "p", torch.float32, (M, L))
+    return M, K, L, is_f32
+
+
+def mmf_glu_fwd(x: torch.Tensor, gamma: torch.Tensor | None, Wgu_packed: torch.Tensor,
+                w_scales: torch.Tensor, p: torch.Tensor, stream=None) -> None:
+    """GLU up-projections and gate: p f32 [M][L] = SiLU(g) * u from x bf16/f32
+    [M][K], the interleaved packed weights [K/16][2L] and w_scales [gate, up]."""
+    M, K, L, is_f32 = _glu_args(x, gamma, Wgu_packed, w_scales, p)
+    fn = _lib.mmf_glu_fwd_f32 if is_f32 else _lib.mmf_glu_fwd
+    _check(fn(_ptr(x), _ptr(gamma), _ptr(Wgu_packed), _ptr(w_scales), _ptr(p), M, K, L,
+              _stream(stream)))
+
+
+def mmf_glu_fwd_ws(x: torch.Tensor, gamma: torch.Tensor | None, Wgu_packed: torch.Tensor,
+                   w_scales: torch.Tensor, p: torch.Tensor, workspace: torch.Tensor,
+                   stream=None) -> None:
+    """mmf_glu_fwd with caller scratch (uint8, mmf_bitlinear_workspace_bytes(M, K))."""
+    M, K, L, is_f32 = _glu_args(x, gamma, Wgu_packed, w_scales, p)
+    _need(workspace, "workspace", torch.uint8, (workspace.numel(),))
+    _check(_lib.mmf_glu_fwd_ws(_ptr(x), int(is_f32), _ptr(gamma), _ptr(Wgu_packed),
+                               _ptr(w_scales), _ptr(p), M, K, L, _ptr(workspace),
+                               workspace.numel(), _stream(stream)))
+
+
+def mmf_ternary_gemm_glu(q: torch.Tensor, a_scale: torch.Tensor, q_rowsum: torch.Tensor,
+                         Wgu_packed: torch.Tensor, w_scales: torch.Tensor, p: torch.Tensor,
+                         stream=None) -> None:
+    """The GLU contraction and gate from quantised activations: p [M][L]."""
+    M, K = q.shape
+    L = Wgu_packed.shape[1] // 2
+    _need(q, "q", torch.int8, (M, K))
+    _need(a_scale, "a_scale", torch.float32, (M,))
+    _need(q_rowsum, "q_rowsum", torch.int32, (M,))
+    _need(Wgu_packed, "Wgu_packed", torch.int32, (K // 16, 2 * L))
+    _need(w_scales, "w_scales", torch.float32, (2,))
+    _need(p, "p", torch.float32, (M, L))
+    _check(_lib.mmf_ternary_gemm_glu(_ptr(q), _ptr(a_scale), _ptr(q_rowsum), _ptr(Wgu_packed),
+                                     _ptr(w_scales), _ptr(p), M, K, L, _stream(stream)))
+
+
 # ---------------------------------------------------------------------------
 # allocating conveniences (outputs allocated with torch on the inputs' device)
 # ---------------------------------------------------------------------------
@@ -232,3 +300,19 @@ def bitlinear(x: torch.Tensor, gamma: torch.Tensor | None, Wpacked: torch.Tensor
     y = torch.empty((x.shape[0], Wpacked.shape[1]), dtype=torch.float32, device=x.device)
     mmf_bitlinear_fwd(x, gamma, Wpacked, w_scale, y, stream)
     return y
+
+
+def glu_pack(Wg_packed: torch.Tensor, Wu_packed: torch.Tensor, stream=None) -> torch.Tensor:
+    """Returns the interleaved [K/16][2L] packed weights of a GLU."""
+    J, L = Wg_packed.shape
+    Wgu = torch.empty((J, 2 * L), dtype=torch.int32, device=Wg_packed.device)
+    mmf_glu_pack(Wg_packed, Wu_packed, Wgu, stream)
+    return Wgu
+
+
+def glu(x: torch.Tensor, gamma: torch.Tensor | None, Wgu_packed: torch.Tensor,
+        w_scales: torch.Tensor, stream=None) -> torch.Tensor:
+    """Returns p float32 [M][L] = SiLU(g) * u."""
+    p = torch.empty((x.shape[0], Wgu_packed.shape[1] // 2), dtype=torch.float32, device=x.device)
+    mmf_glu_fwd(x, gamma, Wgu_packed, w_scales, p, stream)
+    return p

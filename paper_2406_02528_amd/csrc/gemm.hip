@@ -251,7 +251,7 @@ __global__ __launch_bounds__((Tiling<BM, BN, WM, WN, BK, S, BX4>::kThreads)) voi
     const int row = m0 + chunk * 64 + lane;
     const uint32_t off = row < M ? 4u * static_cast<uint32_t>(row) : 0x80000000u;
     const uint64_t base = arr == 0 ? reinterpret_cast<uint64_t>(q_rowsum) : reinterpret_cast<uint64_t>(a_scale);
-    const int bytes = (arr == 0 || EP == Epilogue::kDequantF32) ? M * 4 : 0;
+    const int bytes = (arr == 0 || EP != Epilogue::kRawI32) ? M * 4 : 0;
     const v4i desc = {static_cast<int>(static_cast<uint32_t>(base)), static_cast<int>((base >> 32) & 0xFFFF),
                       bytes, kBufferFlags};
     const uint32_t dst = __builtin_amdgcn_readfirstlane(
@@ -318,14 +318,48 @@ __global__ __launch_bounds__((Tiling<BM, BN, WM, WN, BK, S, BX4>::kThreads)) voi
   // (g, l16) holds row l16 and columns 4 g .. 4 g + 3 of each 16 x 16 block ----
   const int* s_rsum = reinterpret_cast<const int*>(smem + S * T::kStageBytes);
   const float* s_scale = reinterpret_cast<const float*>(smem + S * T::kStageBytes + 4 * BM);
-  const float ws = (EP == Epilogue::kDequantF32) ? w_scale[0] : 0.0f;
+  const float ws = (EP != Epilogue::kRawI32) ? w_scale[0] : 0.0f;
+  const float ws_u = (EP == Epilogue::kGluF32) ? w_scale[1] : 0.0f;
   __syncthreads();
+  constexpr uint32_t kOut = 0x80000000u;
+  if constexpr (EP == Epilogue::kGluF32) {
+    // Blocks f = 2i (gate) and 2i + 1 (up) of a wave hold the same 16
+    // channels: lane (g, l16) has channels 4 g .. 4 g + 3 of both, so the
+    // gate p = SiLU(g) * u is formed in registers and stored 16 bytes at a
+    // time into the L = N / 2 wide output.
+    static_assert(BX4 && FN % 2 == 0, "GLU output needs whole 16-column block pairs");
+    const int L = N / 2;
+    const uint32_t out_bytes = static_cast<uint32_t>(M) * static_cast<uint32_t>(L) * 4u;
+    const __amdgpu_buffer_rsrc_t orsrc =
+        __builtin_amdgcn_make_buffer_rsrc(out, 0, static_cast<int>(out_bytes), kBufferFlags);
+#pragma unroll
+    for (int fm = 0; fm < FM; ++fm) {
+      const int lr = wm * WM + fm * 16 + l16;
+      const bool row_ok = m0 + lr < M;
+      const int rs = s_rsum[lr];
+      const float sg = s_scale[lr] * ws, su = s_scale[lr] * ws_u;
+      const uint32_t row_bytes = static_cast<uint32_t>(m0 + lr) * static_cast<uint32_t>(L) * 4u;
+#pragma unroll
+      for (int pi = 0; pi < FN / 2; ++pi) {
+        const int ch = (n0 + wn * WN) / 2 + pi * 16 + 4 * g;
+        v4i v;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float gv = static_cast<float>(acc[fm][2 * pi][r] - rs) * sg;
+          const float uv = static_cast<float>(acc[fm][2 * pi + 1][r] - rs) * su;
+          v[r] = __float_as_int(gv / (1.0f + expf(-gv)) * uv);
+        }
+        const uint32_t off = (row_ok && ch < L) ? row_bytes + 4u * static_cast<uint32_t>(ch) : kOut;
+        __builtin_amdgcn_raw_buffer_store_b128(v, orsrc, off, 0, 0);
+      }
+    }
+    return;
+  }
   // Range-checked buffer stores: rows past M fall outside the output's
   // range, columns past N are sent there explicitly; no branches.
   const uint32_t out_bytes = static_cast<uint32_t>(M) * static_cast<uint32_t>(N) * 4u;
   const __amdgpu_buffer_rsrc_t orsrc =
       __builtin_amdgcn_make_buffer_rsrc(out, 0, static_cast<int>(out_bytes), kBufferFlags);
-  constexpr uint32_t kOut = 0x80000000u;
 #pragma unroll
   for (int fm = 0; fm < FM; ++fm) {
     const int lr = wm * WM + fm * 16 + l16;
@@ -372,7 +406,15 @@ hipError_t launch_cfg(const ContractArgs& a, int64_t m_begin, int64_t m_rows, hi
                        stream, q, as, rs, a.Wpacked, a.w_scale,
                        static_cast<void*>(static_cast<float*>(a.out) + m_begin * a.N),
                        static_cast<int>(m_rows), a.K, static_cast<int>(a.N));
-  else
+  else if (a.epilogue == Epilogue::kGluF32) {
+    if constexpr (BX4)
+      hipLaunchKernelGGL((gemm_kernel<BM, BN, WM, WN, BK, S, true, Epilogue::kGluF32>), grid, block, 0, stream,
+                         q, as, rs, a.Wpacked, a.w_scale,
+                         static_cast<void*>(static_cast<float*>(a.out) + m_begin * (a.N / 2)),
+                         static_cast<int>(m_rows), a.K, static_cast<int>(a.N));
+    else
+      return hipErrorInvalidValue;
+  } else
     hipLaunchKernelGGL((gemm_kernel<BM, BN, WM, WN, BK, S, BX4, Epilogue::kRawI32>), grid, block, 0,
                        stream, q, as, rs, a.Wpacked, a.w_scale,
                        static_cast<void*>(static_cast<int32_t*>(a.out) + m_begin * a.N),

@@ -155,6 +155,50 @@ int act_quant_common(const void* x, bool x_is_f32, const float* gamma, int8_t* q
                                           static_cast<int>(K), stream));
 }
 
+// GLU (gated up-projection): x -> RMSNorm + quantisation -> the interleaved
+// gate/up contraction with the SiLU(g) * u epilogue.  Any M runs on the MFMA
+// kernel.
+int check_glu(const void* x, const float* gamma, const uint32_t* Wgu, const float* w_scales,
+              const float* p, int64_t M, int64_t K, int64_t L) {
+  if (L < 0 || L > kMaxMN / 2 || (L % 16) != 0) return MMF_ERR_SHAPE;
+  if (int st = check_shape(M, K, 2 * L)) return st;
+  if (M == 0 || L == 0) return MMF_OK;
+  if (!x || !Wgu || !w_scales || !p) return MMF_ERR_NULL;
+  if (!aligned16(x) || !aligned16(Wgu) || !aligned16(p) || (gamma && !aligned16(gamma)))
+    return MMF_ERR_ALIGN;
+  return MMF_OK;
+}
+
+int run_glu(const void* x, bool x_is_f32, const float* gamma, const uint32_t* Wgu,
+            const float* w_scales, float* p, int64_t M, int64_t K, int64_t L, char* scratch,
+            hipStream_t stream) {
+  const FwdScratch s = fwd_scratch(M, K);
+  int8_t* q = reinterpret_cast<int8_t*>(scratch + s.q_off);
+  float* a_scale = reinterpret_cast<float*>(scratch + s.a_off);
+  int32_t* rowsum = reinterpret_cast<int32_t*>(scratch + s.r_off);
+  hipError_t e = mmf::launch_act_quant(x, x_is_f32, gamma, q, a_scale, rowsum, M,
+                                       static_cast<int>(K), stream);
+  if (e != hipSuccess) return MMF_ERR_HIP;
+  mmf::ContractArgs a{q, a_scale, rowsum, Wgu, w_scales, p, M, static_cast<int>(K), 2 * L,
+                      mmf::Epilogue::kGluF32};
+  return hip_status(mmf::launch_gemm(a, stream));
+}
+
+int glu_alloc(const void* x, bool x_is_f32, const float* gamma, const uint32_t* Wgu,
+              const float* w_scales, float* p, int64_t M, int64_t K, int64_t L,
+              hipStream_t stream) {
+  if (int st = check_glu(x, gamma, Wgu, w_scales, p, M, K, L)) return st;
+  if (M == 0 || L == 0) return MMF_OK;
+  const FwdScratch s = fwd_scratch(M, K);
+  void* scratch = nullptr;
+  if (hipMallocAsync(&scratch, s.total, stream) != hipSuccess) return MMF_ERR_HIP;
+  const int st = run_glu(x, x_is_f32, gamma, Wgu, w_scales, p, M, K, L,
+                         static_cast<char*>(scratch), stream);
+  const hipError_t fe = hipFreeAsync(scratch, stream);
+  if (st != MMF_OK) return st;
+  return hip_status(fe);
+}
+
 }  // namespace
 
 extern "C" {
@@ -271,6 +315,57 @@ int mmf_ternary_gemm_i32(const int8_t* q, const uint32_t* Wpacked, int32_t* acc,
   const hipError_t fe = hipFreeAsync(rowsum, stream);
   if (e != hipSuccess) return MMF_ERR_HIP;
   return hip_status(fe);
+}
+
+int mmf_glu_pack(const uint32_t* Wg_packed, const uint32_t* Wu_packed, int64_t L, int64_t K,
+                 uint32_t* Wgu_packed, hipStream_t stream) {
+  if (L < 0 || L > kMaxMN / 2 || (L % 16) != 0) return MMF_ERR_SHAPE;
+  if (int st = check_shape(0, K, 2 * L)) return st;
+  if (L == 0) return MMF_OK;
+  if (!Wg_packed || !Wu_packed || !Wgu_packed) return MMF_ERR_NULL;
+  if (!aligned16(Wg_packed) || !aligned16(Wu_packed) || !aligned16(Wgu_packed)) return MMF_ERR_ALIGN;
+  return hip_status(mmf::launch_glu_pack(Wg_packed, Wu_packed, L, static_cast<int>(K), Wgu_packed, stream));
+}
+
+int mmf_glu_fwd(const uint16_t* x, const float* gamma, const uint32_t* Wgu_packed,
+                const float* w_scales, float* p, int64_t M, int64_t K, int64_t L,
+                hipStream_t stream) {
+  return glu_alloc(x, false, gamma, Wgu_packed, w_scales, p, M, K, L, stream);
+}
+
+int mmf_glu_fwd_f32(const float* x, const float* gamma, const uint32_t* Wgu_packed,
+                    const float* w_scales, float* p, int64_t M, int64_t K, int64_t L,
+                    hipStream_t stream) {
+  return glu_alloc(x, true, gamma, Wgu_packed, w_scales, p, M, K, L, stream);
+}
+
+int mmf_glu_fwd_ws(const void* x, int x_is_f32, const float* gamma, const uint32_t* Wgu_packed,
+                   const float* w_scales, float* p, int64_t M, int64_t K, int64_t L,
+                   void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  if (x_is_f32 != 0 && x_is_f32 != 1) return MMF_ERR_ARG;
+  if (int st = check_glu(x, gamma, Wgu_packed, w_scales, p, M, K, L)) return st;
+  if (M == 0 || L == 0) return MMF_OK;
+  if (!workspace) return MMF_ERR_NULL;
+  if ((reinterpret_cast<uintptr_t>(workspace) & (kScratchAlign - 1)) != 0 ||
+      workspace_bytes < fwd_scratch(M, K).total)
+    return MMF_ERR_WORKSPACE;
+  return run_glu(x, x_is_f32 == 1, gamma, Wgu_packed, w_scales, p, M, K, L,
+                 static_cast<char*>(workspace), stream);
+}
+
+int mmf_ternary_gemm_glu(const int8_t* q, const float* a_scale, const int32_t* q_rowsum,
+                         const uint32_t* Wgu_packed, const float* w_scales, float* p, int64_t M,
+                         int64_t K, int64_t L, hipStream_t stream) {
+  if (L < 0 || L > kMaxMN / 2 || (L % 16) != 0) return MMF_ERR_SHAPE;
+  if (int st = check_shape(M, K, 2 * L)) return st;
+  if (M == 0 || L == 0) return MMF_OK;
+  if (!q || !a_scale || !q_rowsum || !Wgu_packed || !w_scales || !p) return MMF_ERR_NULL;
+  if (!aligned16(q) || !aligned16(a_scale) || !aligned16(q_rowsum) || !aligned16(Wgu_packed) ||
+      !aligned16(p))
+    return MMF_ERR_ALIGN;
+  mmf::ContractArgs a{q, a_scale, q_rowsum, Wgu_packed, w_scales, p, M, static_cast<int>(K), 2 * L,
+                      mmf::Epilogue::kGluF32};
+  return hip_status(mmf::launch_gemm(a, stream));
 }
 
 int mmf_set_path(int path) {

@@ -21,8 +21,11 @@ int ternarize_partials_count(int64_t count);
 hipError_t launch_ternarize(const float* W, int64_t N, int K, uint32_t* Wpacked,
                             float* w_scale, double* partials, hipStream_t stream);
 
-// Output form of the contraction kernels.
-enum class Epilogue { kDequantF32, kRawI32 };
+// Output form of the contraction kernels.  kGluF32: the packed columns are
+// the two up-projections of a GLU interleaved in blocks of 16 (gate, up,
+// gate, ...), w_scale holds [gate, up], and the output is the gated
+// representation SiLU(g) * u, N / 2 columns wide.
+enum class Epilogue { kDequantF32, kRawI32, kGluF32 };
 
 struct ContractArgs {
   const int8_t* q;          // [M][K]
@@ -64,5 +67,10 @@ bool decode_fits(int64_t mt, int K, int64_t N, bool from_x, bool x_is_f32);
 hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream);
 // Prefill kernel: int8 MFMA, any M.
 hipError_t launch_gemm(const ContractArgs& a, hipStream_t stream);
+
+// Interleave the packed gate and up projections of a GLU, [K/16][L] each,
+// into [K/16][2L] blocks of 16 columns (gate, up, gate, ...); L % 16 == 0.
+hipError_t launch_glu_pack(const uint32_t* Wg, const uint32_t* Wu, int64_t L, int K, uint32_t* Wgu,
+                           hipStream_t stream);
 
 }  // namespace mmf

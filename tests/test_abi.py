@@ -142,3 +142,33 @@ def test_python_binding_rejects_cpu_tensors(mmf):
     with pytest.raises(TypeError):
         mmf.mmf_act_quant(torch.zeros(2, 16, dtype=torch.float16), None,
                           torch.zeros(2, 16, dtype=torch.int8), torch.zeros(2))
+
+
+def test_glu_argument_checks(mmf):
+    lib = _c(mmf)
+    # L must be a multiple of 16; K as for the forward
+    assert lib.mmf_glu_fwd(A, B, C, D, E, 4, 16, 24, S) == 2
+    assert lib.mmf_glu_fwd(A, B, C, D, E, 4, 24, 32, S) == 2
+    assert lib.mmf_glu_fwd(A, B, C, D, E, 4, 16, -16, S) == 2
+    assert lib.mmf_glu_pack(A, B, 24, 16, C, S) == 2
+    assert lib.mmf_glu_pack(A, B, 32, 40, C, S) == 2
+    # NULL and misaligned pointers
+    assert lib.mmf_glu_fwd(None, B, C, D, E, 4, 16, 32, S) == 1
+    assert lib.mmf_glu_fwd(A, B, C, None, E, 4, 16, 32, S) == 1
+    assert lib.mmf_glu_fwd(A, B, C, D, None, 4, 16, 32, S) == 1
+    assert lib.mmf_glu_fwd(A, B, BAD, D, E, 4, 16, 32, S) == 3
+    assert lib.mmf_glu_fwd_f32(A, B, C, D, BAD, 4, 16, 32, S) == 3
+    assert lib.mmf_glu_pack(A, None, 32, 16, C, S) == 1
+    assert lib.mmf_glu_pack(A, B, 32, 16, BAD, S) == 3
+    # workspace variant
+    need = mmf.mmf_bitlinear_workspace_bytes(4, 16)
+    assert lib.mmf_glu_fwd_ws(A, 0, B, C, D, E, 4, 16, 32, 0x100000, need - 1, S) == 4
+    assert lib.mmf_glu_fwd_ws(A, 0, B, C, D, E, 4, 16, 32, None, need, S) == 1
+    assert lib.mmf_glu_fwd_ws(A, 3, B, C, D, E, 4, 16, 32, 0x100000, need, S) == 6
+    # empty shapes are no-ops
+    assert lib.mmf_glu_fwd(None, None, None, None, None, 0, 16, 32, S) == 0
+    assert lib.mmf_glu_fwd(None, None, None, None, None, 4, 16, 0, S) == 0
+    assert lib.mmf_glu_pack(None, None, 0, 16, None, S) == 0
+    assert lib.mmf_ternary_gemm_glu(A, B, C, D, E, A, 4, 16, 24, S) == 2
+    assert lib.mmf_ternary_gemm_glu(A, B, None, D, E, A, 4, 16, 32, S) == 1
+    assert lib.mmf_ternary_gemm_glu(A, B, C, D, E, BAD, 4, 16, 32, S) == 3
