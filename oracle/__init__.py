@@ -24,6 +24,12 @@ wrapper names the passage of the paper it follows:
   up-projections
 * :func:`glu_interleave` -- the library's storage order for the two
   up-projection weights of one GLU (16-column blocks of gate and up in turn)
+* :func:`mlgru_gates`, :func:`mlgru_scan`, :func:`add_bias`,
+  :func:`mlgru_proj`, :func:`mlgru_fwd` -- the MLGRU token mixer of Sec.
+  "MatMul-free Language Model Architecture": gate activations with biases
+  and the forget-gate lower bound, the recurrence
+  h_t = f_t h_{t-1} + (1 - f_t) c_t with the output gate o' = g sigma(h), and
+  the whole mixer around its two ternary projections
 """
 from __future__ import annotations
 
@@ -83,6 +89,9 @@ def _load():
                                          ctypes.c_double, P, P, P, P, P]
     lib.oracle_bitlinear_fwd.restype = ctypes.c_int
     lib.oracle_glu.argtypes = [P, P, I64, P]
+    lib.oracle_mlgru_gates.argtypes = [P, P, P, I64, I64, P]
+    lib.oracle_mlgru_scan.argtypes = [P, P, I64, I64, I64, P, P]
+    lib.oracle_add_bias.argtypes = [P, P, I64, I64, P]
     _lib = lib
     return lib
 
@@ -262,3 +271,92 @@ def glu_interleave(t_g: np.ndarray, t_u: np.ndarray) -> np.ndarray:
         out[32 * b:32 * b + 16] = t_g[16 * b:16 * b + 16]
         out[32 * b + 16:32 * b + 32] = t_u[16 * b:16 * b + 16]
     return out
+
+
+def _opt(a, dtype):
+    return None if a is None else _c(a, dtype)
+
+
+def mlgru_gates(z: np.ndarray, bias: np.ndarray | None = None,
+                lb: np.ndarray | None = None) -> np.ndarray:
+    """Gate activations of the MLGRU.  z is [M][3d] (forget | candidate |
+    output-gate projections); returns fcg [M][3d] with f = lb + (1 - lb)
+    sigma(z_f + b_f), c = SiLU(z_c + b_c), g = z_g + b_g (fp64, rounded once)."""
+    z = _c(z, np.float32)
+    M, n3 = z.shape
+    if n3 % 3:
+        raise ValueError("z must have 3d columns")
+    d = n3 // 3
+    b = _opt(bias, np.float32)
+    low = _opt(lb, np.float32)
+    if b is not None and b.shape != (3 * d,):
+        raise ValueError("bias must be [3d]")
+    if low is not None and low.shape != (d,):
+        raise ValueError("lb must be [d]")
+    out = np.empty((M, 3 * d), np.float32)
+    _load().oracle_mlgru_gates(_p(z), None if b is None else _p(b),
+                               None if low is None else _p(low), M, d, _p(out))
+    return out
+
+
+def mlgru_scan(fcg: np.ndarray, B: int, T: int, h0: np.ndarray | None = None):
+    """The MLGRU recurrence and output gate over B sequences of T tokens
+    (rows b*T + t of fcg [B*T][3d]).  Returns (o' [B*T][d], h_last [B][d])."""
+    fcg = _c(fcg, np.float32)
+    if fcg.shape[0] != B * T or fcg.shape[1] % 3:
+        raise ValueError("fcg must be [B*T][3d]")
+    d = fcg.shape[1] // 3
+    h = _opt(h0, np.float32)
+    if h is not None and h.shape != (B, d):
+        raise ValueError("h0 must be [B][d]")
+    o = np.empty((B * T, d), np.float32)
+    hl = np.empty((B, d), np.float32)
+    _load().oracle_mlgru_scan(_p(fcg), None if h is None else _p(h), B, T, d, _p(o), _p(hl))
+    return o, hl
+
+
+def add_bias(y: np.ndarray, b: np.ndarray) -> np.ndarray:
+    """y + b per row (fp64, rounded once): the bias of Algorithm 1's forward."""
+    y = _c(y, np.float32)
+    b = _c(b, np.float32)
+    M, N = y.shape
+    if b.shape != (N,):
+        raise ValueError("bias must be [N]")
+    out = np.empty((M, N), np.float32)
+    _load().oracle_add_bias(_p(y), _p(b), M, N, _p(out))
+    return out
+
+
+def mlgru_proj(x: np.ndarray, gamma: np.ndarray | None, t_fcg: np.ndarray, w_scales,
+               bias: np.ndarray | None = None, lb: np.ndarray | None = None, eps: float = EPS):
+    """The MLGRU's input projections and gate activations: the three ternary
+    projections of the normalised, quantised x (one RMSNorm, one activation
+    quantisation; t_fcg [3d][K] holds W_f, W_c, W_g in turn, segment s scaled
+    by w_scales[s]), then :func:`mlgru_gates`.  Returns dict with fcg, z, acc,
+    q, a_scale."""
+    t_fcg = _c(t_fcg, np.int8)
+    d = t_fcg.shape[0] // 3
+    if t_fcg.shape[0] != 3 * d:
+        raise ValueError("t_fcg must have 3d rows")
+    parts = [bitlinear_fwd(x, gamma, t_fcg[s * d:(s + 1) * d], float(w_scales[s]), eps)
+             for s in range(3)]
+    z = np.concatenate([p["y"] for p in parts], axis=1)
+    acc = np.concatenate([p["acc"] for p in parts], axis=1)
+    return {"fcg": mlgru_gates(z, bias, lb), "z": z, "acc": acc,
+            "q": parts[0]["q"], "a_scale": parts[0]["a_scale"]}
+
+
+def mlgru_fwd(x: np.ndarray, B: int, T: int, gamma: np.ndarray | None, t_fcg: np.ndarray,
+              w_scales, bias: np.ndarray | None, lb: np.ndarray | None,
+              h0: np.ndarray | None, gamma_o: np.ndarray | None, t_o: np.ndarray,
+              w_scale_o: float, b_o: np.ndarray | None, eps: float = EPS):
+    """The whole MLGRU token mixer over B sequences of T tokens (x rows
+    b*T + t): projections and gates, recurrence and output gate, then the
+    output projection o = BitLinear(o'; t_o) + b_o.  Returns dict with o,
+    h_last, o_prime, fcg and the output projection's q, acc, a_scale."""
+    pr = mlgru_proj(x, gamma, t_fcg, w_scales, bias, lb, eps)
+    o_prime, h_last = mlgru_scan(pr["fcg"], B, T, h0)
+    out = bitlinear_fwd(o_prime, gamma_o, t_o, w_scale_o, eps)
+    o = out["y"] if b_o is None else add_bias(out["y"], b_o)
+    return {"o": o, "h_last": h_last, "o_prime": o_prime, "fcg": pr["fcg"],
+            "y_o": out["y"], "q_o": out["q"], "acc_o": out["acc"], "a_scale_o": out["a_scale"]}

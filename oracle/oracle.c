@@ -25,6 +25,11 @@
  *   dequantisation       -- Algorithm 1: the quantisers return the rounded value
  *                           times 1/s, so the product of two fake-quantised
  *                           operands is the integer sum times (1/s_a)(1/s_w).
+ *   GLU gate             -- Sec. "MatMul-free Channel Mixer": SiLU(g) * u.
+ *   MLGRU                -- Sec. "MatMul-free Language Model Architecture",
+ *                           MLGRU equations: forget/candidate/output gate
+ *                           activations, the recurrence over time and the
+ *                           output gate o' = g * sigma(h); bias of a layer.
  *
  * Precision.  The paper fixes none.  Where a floating-point value decides an
  * integer (the ternary code, the int8 activation) the oracle takes that
@@ -288,4 +293,76 @@ void oracle_glu(const float *g, const float *u, int64_t n, float *p) {
         const double silu = gv / (1.0 + exp(-gv));
         p[i] = (float)(silu * (double)u[i]);
     }
+}
+
+/* ---------------------------------------------------------------------- */
+/* MLGRU gate activations (Sec. "MatMul-free Language Model Architecture", */
+/* paragraph "MatMul-free Linear Gated Recurrent Unit").  z is [M][3d]: the */
+/* three ternary projections of a token side by side, forget gate columns  */
+/* [0, d), candidate [d, 2d), output gate [2d, 3d).  With the biases b     */
+/* ([3d], NULL => 0) and the forget-gate lower bound lb ([d], NULL => 0):  */
+/*   f = lb + (1 - lb) sigma(z_f + b_f)                                   */
+/*   c = SiLU(z_c + b_c) = v / (1 + e^-v)                                 */
+/*   g = z_g + b_g                                                        */
+/* The lower bound is the form of HGRN that the paper's cummax remark      */
+/* refers to (a per-layer vector in [0, 1) raising the forget gate towards */
+/* 1 in deeper layers); lb = 0 is the equations as printed.  Each value is */
+/* evaluated in fp64 from the fp32 inputs and rounded to fp32 once.        */
+/* ---------------------------------------------------------------------- */
+void oracle_mlgru_gates(const float *z, const float *bias, const float *lb,
+                        int64_t M, int64_t d, float *fcg) {
+#pragma omp parallel for schedule(static)
+    for (int64_t m = 0; m < M; ++m) {
+        const float *zr = z + m * 3 * d;
+        float *o = fcg + m * 3 * d;
+        for (int64_t i = 0; i < d; ++i) {
+            const double vf = (double)zr[i] + (bias ? (double)bias[i] : 0.0);
+            const double vc = (double)zr[d + i] + (bias ? (double)bias[d + i] : 0.0);
+            const double vg = (double)zr[2 * d + i] + (bias ? (double)bias[2 * d + i] : 0.0);
+            const double low = lb ? (double)lb[i] : 0.0;
+            o[i] = (float)(low + (1.0 - low) / (1.0 + exp(-vf)));
+            o[d + i] = (float)(vc / (1.0 + exp(-vc)));
+            o[2 * d + i] = (float)vg;
+        }
+    }
+}
+
+/* ---------------------------------------------------------------------- */
+/* MLGRU recurrence and output gate (same paragraph): for each of B        */
+/* sequences of T tokens (rows b*T + t of fcg, laid out as above)          */
+/*   h_t  = f_t (.) h_{t-1} + (1 - f_t) (.) c_t,   h_0 = h0 (NULL => 0)    */
+/*   o'_t = g_t (.) sigma(h_t)                                            */
+/* taken one step after the other in token order, the state carried in     */
+/* fp64.  o' [B*T][d] is rounded to fp32 once per value; h_last [B][d]     */
+/* (may be NULL) receives the state after the last token, rounded.        */
+/* ---------------------------------------------------------------------- */
+void oracle_mlgru_scan(const float *fcg, const float *h0, int64_t B, int64_t T,
+                       int64_t d, float *o, float *h_last) {
+#pragma omp parallel for schedule(static)
+    for (int64_t b = 0; b < B; ++b) {
+        for (int64_t i = 0; i < d; ++i) {
+            double h = h0 ? (double)h0[b * d + i] : 0.0;
+            for (int64_t t = 0; t < T; ++t) {
+                const float *row = fcg + (b * T + t) * 3 * d;
+                const double f = (double)row[i];
+                const double c = (double)row[d + i];
+                const double g = (double)row[2 * d + i];
+                h = f * h + (1.0 - f) * c;
+                o[(b * T + t) * d + i] = (float)(g / (1.0 + exp(-h)));
+            }
+            if (h_last) h_last[b * d + i] = (float)h;
+        }
+    }
+}
+
+/* ---------------------------------------------------------------------- */
+/* Bias of a dense layer (Algorithm 1, forward_pass: the ternary product   */
+/* plus b): y [M][N] fp32 outputs of the dequantised product, b [N];       */
+/* out = y + b in fp64, rounded once.                                      */
+/* ---------------------------------------------------------------------- */
+void oracle_add_bias(const float *y, const float *b, int64_t M, int64_t N, float *out) {
+#pragma omp parallel for schedule(static)
+    for (int64_t m = 0; m < M; ++m)
+        for (int64_t n = 0; n < N; ++n)
+            out[m * N + n] = (float)((double)y[m * N + n] + (double)b[n]);
 }

@@ -375,3 +375,175 @@ def test_glu_interleave_blocks():
     assert np.array_equal(pgu[:, 16:32], pu[:, 0:16]) and np.array_equal(pgu[:, 32:48], pg[:, 16:32])
     with pytest.raises(ValueError):
         oracle.glu_interleave(t_g[:24].astype(np.int8), t_u[:24].astype(np.int8))
+
+
+# --------------------------------------------------------------------------
+# MLGRU token mixer (Sec. "MatMul-free Language Model Architecture")
+# --------------------------------------------------------------------------
+
+def _fcg(f, c, g):
+    return np.concatenate([np.asarray(f, np.float32), np.asarray(c, np.float32),
+                           np.asarray(g, np.float32)], axis=-1)
+
+
+def test_mlgru_gates_closed_forms():
+    # sigmoid(ln 3) = 3/4 and sigmoid(0) = 1/2; with the lower bound 1/2 the
+    # forget gate is 1/2 + (1/2)(3/4) = 7/8.  SiLU(ln 3) = (3/4) ln 3.
+    l3 = float(np.float32(math.log(3.0)))
+    z = _fcg([[l3, 0.0, -l3]], [[l3, 0.0, -l3]], [[l3, 0.0, -2.5]])
+    out = oracle.mlgru_gates(z).astype(np.float64)[0]
+    np.testing.assert_allclose(out[0:3], [0.75, 0.5, 0.25], rtol=2e-7)
+    np.testing.assert_allclose(out[3:6], [0.75 * l3, 0.0, -0.25 * l3], rtol=2e-7)
+    assert out[6:9].tolist() == [np.float32(l3), 0.0, -2.5]     # output gate: no activation
+    lb = np.array([0.5, 0.5, 0.0], np.float32)
+    out = oracle.mlgru_gates(z, lb=lb).astype(np.float64)[0]
+    np.testing.assert_allclose(out[0:3], [0.875, 0.75, 0.25], rtol=2e-7)
+    # lb = 1 pins f to 1 whatever the projection
+    assert np.all(oracle.mlgru_gates(z, lb=np.ones(3, np.float32))[0, :3] == 1.0)
+
+
+def test_mlgru_gates_bias_and_segments():
+    rng = np.random.default_rng(11)
+    d = 8
+    # dyadic values: z + b is exact in fp32, so a bias equals a shifted input
+    z = (rng.integers(-64, 64, (4, 3 * d)) / 16).astype(np.float32)
+    b = (rng.integers(-64, 64, 3 * d) / 16).astype(np.float32)
+    assert np.array_equal(oracle.mlgru_gates(z, b), oracle.mlgru_gates(z + b))
+    # each segment depends on its own columns only
+    base = oracle.mlgru_gates(z)
+    for s in range(3):
+        z2 = z.copy()
+        z2[:, s * d:(s + 1) * d] += 1.0
+        diff = oracle.mlgru_gates(z2) != base
+        assert diff[:, s * d:(s + 1) * d].any()
+        assert not np.delete(diff, np.s_[s * d:(s + 1) * d], axis=1).any()
+    # sigmoid(-v) = 1 - sigmoid(v); SiLU(v) - SiLU(-v) = v
+    v = np.linspace(-6, 6, d).astype(np.float32)
+    zz = _fcg(v, v, v)[None]
+    zn = _fcg(-v, -v, -v)[None]
+    p, n = oracle.mlgru_gates(zz)[0].astype(np.float64), oracle.mlgru_gates(zn)[0].astype(np.float64)
+    np.testing.assert_allclose(p[:d] + n[:d], 1.0, rtol=2e-7)
+    np.testing.assert_allclose(p[d:2 * d] - n[d:2 * d], v, rtol=3e-7, atol=1e-7)
+    assert np.all((p[:d] > 0) & (p[:d] < 1))
+
+
+def test_mlgru_scan_constant_gates_closed_form():
+    # time-invariant f and c: h_t = f^t h_0 + (1 - f^t) c (geometric series)
+    T, d = 40, 5
+    f = np.array([0.5, 0.9, 0.25, 0.75, 0.0], np.float32)
+    c = np.array([1.0, -2.0, 3.0, 0.5, 4.0], np.float32)
+    h0 = np.array([[2.0, 1.0, -1.0, 0.0, 7.0]], np.float32)
+    fcg = np.tile(_fcg(f, c, np.ones(d)), (T, 1))
+    o, hl = oracle.mlgru_scan(fcg, 1, T, h0)
+    t = np.arange(1, T + 1)[:, None]
+    f64, c64 = f.astype(np.float64), c.astype(np.float64)
+    h = f64 ** t * h0.astype(np.float64) + (1 - f64 ** t) * c64
+    np.testing.assert_allclose(o, 1 / (1 + np.exp(-h)), rtol=2e-7)
+    np.testing.assert_allclose(hl[0], h[-1], rtol=2e-7)
+    # f = 0 forgets at once (h = c), f = 1 keeps h_0 forever
+    assert np.all(hl[0, 4] == 4.0)
+    fcg[:, 0] = 1.0
+    _, hl = oracle.mlgru_scan(fcg, 1, T, h0)
+    assert hl[0, 0] == 2.0
+
+
+def test_mlgru_scan_unrolled_sum():
+    # second formulation: h_t = (prod_{s<=t} f_s) h_0 + sum_s (prod_{s<r<=t} f_r)(1 - f_s) c_s
+    rng = np.random.default_rng(5)
+    B, T, d = 2, 9, 3
+    f = rng.uniform(0.05, 0.95, (B * T, d)).astype(np.float32)
+    c = rng.standard_normal((B * T, d)).astype(np.float32)
+    g = rng.standard_normal((B * T, d)).astype(np.float32)
+    h0 = rng.standard_normal((B, d)).astype(np.float32)
+    o, hl = oracle.mlgru_scan(_fcg(f, c, g), B, T, h0)
+    F, C, G = (a.astype(np.float64).reshape(B, T, d) for a in (f, c, g))
+    for b in range(B):
+        for t in range(T):
+            h = np.prod(F[b, :t + 1], axis=0) * h0[b]
+            for s in range(t + 1):
+                h = h + np.prod(F[b, s + 1:t + 1], axis=0) * (1 - F[b, s]) * C[b, s]
+            np.testing.assert_allclose(o[b * T + t], G[b, t] / (1 + np.exp(-h)), rtol=1e-6)
+        np.testing.assert_allclose(hl[b], h, rtol=1e-6)
+
+
+def test_mlgru_scan_structure():
+    rng = np.random.default_rng(9)
+    B, T, d = 3, 12, 4
+    f = rng.uniform(0.0, 1.0, (B * T, d)).astype(np.float32)
+    c = rng.standard_normal((B * T, d)).astype(np.float32)
+    g = rng.standard_normal((B * T, d)).astype(np.float32)
+    h0 = rng.standard_normal((B, d)).astype(np.float32)
+    fcg = _fcg(f, c, g)
+    o, hl = oracle.mlgru_scan(fcg, B, T, h0)
+    # sequences are independent: one call per sequence gives the same result
+    for b in range(B):
+        ob, hb = oracle.mlgru_scan(fcg[b * T:(b + 1) * T], 1, T, h0[b:b + 1])
+        assert np.array_equal(ob, o[b * T:(b + 1) * T]) and np.array_equal(hb[0], hl[b])
+    # no initial state is h_0 = 0; a zero candidate keeps the state at zero
+    o0, _ = oracle.mlgru_scan(fcg, B, T)
+    assert np.array_equal(o0, oracle.mlgru_scan(fcg, B, T, np.zeros((B, d), np.float32))[0])
+    o_z, hl_z = oracle.mlgru_scan(_fcg(f, np.zeros_like(c), g), B, T)
+    assert np.array_equal(o_z, g / 2) and np.all(hl_z == 0)     # sigma(0) = 1/2
+    # continuing from the returned state matches one long scan (up to the fp32 state)
+    t1 = 5
+    oa, ha = oracle.mlgru_scan(fcg[:t1], 1, t1, h0[:1])
+    ob, hb = oracle.mlgru_scan(fcg[t1:T], 1, T - t1, ha)
+    np.testing.assert_allclose(np.concatenate([oa, ob]), o[:T], rtol=1e-6, atol=1e-7)
+    np.testing.assert_allclose(hb[0], hl[0], rtol=1e-6, atol=1e-7)
+    # linear in (h_0, c) for fixed f: the state of a sum is the sum of states
+    c2 = rng.standard_normal((B * T, d)).astype(np.float32)
+    h2 = rng.standard_normal((B, d)).astype(np.float32)
+    big = np.full_like(g, 60.0)   # sigma(h) * 60 ~ linear readout only through h_last
+    _, s1 = oracle.mlgru_scan(_fcg(f, c, big), B, T, h0)
+    _, s2 = oracle.mlgru_scan(_fcg(f, c2, big), B, T, h2)
+    _, s12 = oracle.mlgru_scan(_fcg(f, c + c2, big), B, T, h0 + h2)
+    np.testing.assert_allclose(s12, s1.astype(np.float64) + s2, rtol=1e-5, atol=1e-6)
+
+
+def test_mlgru_fwd_zero_candidate():
+    # With W_c = 0 and no bias the candidate is SiLU(0) = 0, so from h_0 = 0
+    # the state stays 0 and o' = g sigma(0) = g / 2.  The output projection's
+    # RMSNorm removes that factor (but for eps) and absmax quantisation is
+    # scale-free, so the mixer's output is BitLinear_o(g) + b_o with the same
+    # q and integer sums, its scale moved only by eps.
+    rng = np.random.default_rng(21)
+    B, T, K = 2, 3, 32
+    x = rng.standard_normal((B * T, K)).astype(np.float32)
+    W = (rng.standard_normal((3 * K, K)) * 0.02).astype(np.float32)
+    W[K:2 * K] = 0
+    t, ws = oracle.weight_quant(W)
+    Wo = (rng.standard_normal((K, K)) * 0.02).astype(np.float32)
+    t_o, ws_o = oracle.weight_quant(Wo)
+    b_o = (rng.integers(-8, 8, K) / 4).astype(np.float32)
+    out = oracle.mlgru_fwd(x, B, T, None, t, [ws] * 3, None, None, None, None, t_o, ws_o, b_o)
+    assert np.all(out["fcg"][:, K:2 * K] == 0) and np.all(out["h_last"] == 0)
+    g = out["fcg"][:, 2 * K:]
+    assert np.array_equal(out["o_prime"], g / 2)
+    ref = oracle.bitlinear_fwd(g, None, t_o, ws_o)
+    assert np.array_equal(out["q_o"], ref["q"]) and np.array_equal(out["acc_o"], ref["acc"])
+    # only the RMSNorm's eps sees the factor 1/2: per row the output scale
+    # is 0.5 r(g/2) / r(g) = sqrt(ms + eps) / sqrt(ms + 4 eps), ms = mean(g^2)
+    ms = np.mean(g.astype(np.float64) ** 2, axis=1, keepdims=True)
+    ratio = np.sqrt(ms + oracle.EPS) / np.sqrt(ms + 4 * oracle.EPS)
+    assert ratio.min() < 1 - 1e-4   # the test shapes make the eps term visible
+    np.testing.assert_allclose(out["o"], ref["y"].astype(np.float64) * ratio + b_o, rtol=2e-6, atol=1e-7)
+
+
+def test_mlgru_proj_segment_scales():
+    # segment s is scaled by w_scales[s]: doubling the candidate's scale
+    # doubles exactly its pre-activations and leaves the other two alone
+    rng = np.random.default_rng(23)
+    K = 48
+    x = rng.standard_normal((3, K)).astype(np.float32)
+    t, ws = oracle.weight_quant((rng.standard_normal((3 * K, K)) * 0.02).astype(np.float32))
+    p1 = oracle.mlgru_proj(x, None, t, [ws, ws, ws])
+    p2 = oracle.mlgru_proj(x, None, t, [ws, 2 * ws, ws])
+    assert np.array_equal(p2["z"][:, K:2 * K], 2 * p1["z"][:, K:2 * K])
+    assert np.array_equal(np.delete(p2["z"], np.s_[K:2 * K], 1), np.delete(p1["z"], np.s_[K:2 * K], 1))
+    assert np.array_equal(p1["acc"], oracle.ternary_accumulate(p1["q"], t))
+
+
+def test_add_bias():
+    y = np.array([[1.0, -2.0, 0.5]], np.float32)
+    b = np.array([0.25, 2.0, -0.5], np.float32)
+    assert oracle.add_bias(y, b).tolist() == [[1.25, 0.0, 0.0]]
