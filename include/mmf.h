@@ -214,6 +214,80 @@ int mmf_ternary_gemm_glu(const int8_t *q, const float *a_scale, const int32_t *q
                          int64_t M, int64_t K, int64_t L, hipStream_t stream);
 
 /*
+ * Dense layer with bias (Algorithm 1, forward_pass: the ternary product plus
+ * b): y = mmf_bitlinear_fwd's output + bias[n], the add in fp32 after the
+ * dequantisation:  y[m][n] = fp32(acc) * (a_scale[m] * w_scale[0]) + bias[n].
+ * x [M][K] bf16 bits (x_is_f32 = 0) or float32 (x_is_f32 = 1); bias [N]
+ * float32; N must be a multiple of 4 (MMF_ERR_SHAPE).  Same kernels and
+ * scratch as mmf_bitlinear_fwd.
+ */
+int mmf_bitlinear_fwd_bias(const void *x, int x_is_f32, const float *gamma,
+                           const uint32_t *Wpacked, const float *w_scale, const float *bias,
+                           float *y, int64_t M, int64_t K, int64_t N, hipStream_t stream);
+
+/*
+ * MLGRU token mixer (Sec. "MatMul-free Language Model Architecture",
+ * paragraph "MatMul-free Linear Gated Recurrent Unit" and its equations),
+ * with (*) the BitLinear above:
+ *   f_t  = lb + (1 - lb) (.) sigmoid(x_t (*) W_f + b_f)    forget gate
+ *   c_t  = SiLU(x_t (*) W_c + b_c)                         candidate
+ *   h_t  = f_t (.) h_{t-1} + (1 - f_t) (.) c_t             state, h_0 given or 0
+ *   g_t  = x_t (*) W_g + b_g                               output gate
+ *   o'_t = g_t (.) sigmoid(h_t)
+ *   o_t  = o'_t (*) W_o + b_o
+ * lb [d] is the forget-gate lower bound of HGRN that the paper keeps for
+ * deeper layers (NULL: no bound, the equations as printed); biases may be
+ * NULL (zero).
+ *
+ * Layout: B sequences of T tokens, token t of sequence b in row b*T + t of
+ * x, fcg, o_prime and o; states h0, h_last [B][d] float32.  d must be a
+ * positive multiple of 16 (MMF_ERR_SHAPE).  The three input projections are
+ * one packed matrix Wfcg [K/16][3d] (columns f | c | g: mmf_ternarize_weights
+ * of the stacked [3d][K] latent weights, or three packs side by side) behind
+ * one RMSNorm gamma and one activation quantisation; w_scales [3] scales the
+ * three column blocks (three equal values when ternarised together).
+ *
+ * Workspace: every MLGRU entry point takes `workspace` of at least the bytes
+ * its _workspace_bytes function returns (256-byte aligned,
+ * MMF_ERR_WORKSPACE), or NULL, in which case it allocates that scratch
+ * stream-ordered on `stream` and frees it there.
+ */
+
+/* Input projections and gate activations: fcg [M][3d] float32 with, for
+ * column n of segment s = n / d (channel i = n % d),
+ *   z = fp32(acc) * (a_scale[m] * w_scales[s]) + bias[n]      (fp32)
+ *   f = (1 - lb[i]) / (1 + expf(-z)) + lb[i],  c = z / (1 + expf(-z)),  g = z
+ * x [M][K] bf16 bits or float32 (x_is_f32); bias [3d] or NULL; lb [d] or
+ * NULL.  M <= 8 runs the fused decode kernel, larger M the int8 MFMA kernel. */
+size_t mmf_mlgru_proj_workspace_bytes(int64_t M, int64_t K, int64_t d);
+int mmf_mlgru_proj(const void *x, int x_is_f32, const float *gamma, const uint32_t *Wfcg,
+                   const float *w_scales, const float *bias, const float *lb, float *fcg,
+                   int64_t M, int64_t K, int64_t d, void *workspace, size_t workspace_bytes,
+                   hipStream_t stream);
+
+/* Recurrence and output gate from fcg [B*T][3d]: o_prime [B*T][d] float32,
+ * the state after the last token in h_last [B][d] (NULL: not stored).  h0
+ * NULL means h_0 = 0; h_last may be the same array as h0 (the state is then
+ * updated in place), no other overlap is allowed.  In fp32, token by token
+ * within chunks of tokens, the chunks joined through their products of
+ * forget gates. */
+size_t mmf_mlgru_scan_workspace_bytes(int64_t B, int64_t T, int64_t d);
+int mmf_mlgru_scan(const float *fcg, const float *h0, float *o_prime, float *h_last,
+                   int64_t B, int64_t T, int64_t d, void *workspace, size_t workspace_bytes,
+                   hipStream_t stream);
+
+/* The whole mixer: mmf_mlgru_proj (K = d), mmf_mlgru_scan, then
+ * mmf_bitlinear_fwd_bias of o' (float32) with gamma_o, Wo [d/16][d],
+ * w_scale_o [1] and b_o [d] (NULL: zero) into o [B*T][d] float32.  The same
+ * kernels as those three calls, so the results are identical to them. */
+size_t mmf_mlgru_workspace_bytes(int64_t B, int64_t T, int64_t d);
+int mmf_mlgru_fwd(const void *x, int x_is_f32, const float *gamma, const uint32_t *Wfcg,
+                  const float *w_scales, const float *bias, const float *lb, const float *h0,
+                  float *h_last, const float *gamma_o, const uint32_t *Wo,
+                  const float *w_scale_o, const float *b_o, float *o, int64_t B, int64_t T,
+                  int64_t d, void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
  * Kernel selection for the contraction: MMF_PATH_AUTO (decode kernel for
  * M <= 8, MFMA kernel otherwise), MMF_PATH_GEMV or MMF_PATH_GEMM force one
  * kernel for every M (the decode kernel handles at most 8 tokens per launch

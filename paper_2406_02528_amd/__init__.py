@@ -8,6 +8,9 @@ module only checks tensor shapes, dtypes and devices and passes raw pointers
 and the current HIP stream through the C ABI declared in ``include/mmf.h``.
 PyTorch is used for device memory and streams only.
 
+Also the GLU channel mixer's gated up-projection and the MLGRU token mixer
+(input projections with gate activations, the recurrence, the whole mixer).
+
 Functions carry the names of the C entry points.  There is no fallback: if
 the library is not built, importing this package raises ``ImportError``.
 """
@@ -56,6 +59,16 @@ _SIGNATURES = {
     "mmf_glu_fwd_ws": ([_P, ctypes.c_int, _P, _P, _P, _P, _I64, _I64, _I64, _P, _SZ, _P],
                        ctypes.c_int),
     "mmf_ternary_gemm_glu": ([_P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _P], ctypes.c_int),
+    "mmf_bitlinear_fwd_bias": ([_P, ctypes.c_int, _P, _P, _P, _P, _P, _I64, _I64, _I64, _P],
+                               ctypes.c_int),
+    "mmf_mlgru_proj_workspace_bytes": ([_I64, _I64, _I64], _SZ),
+    "mmf_mlgru_proj": ([_P, ctypes.c_int, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _P, _SZ, _P],
+                       ctypes.c_int),
+    "mmf_mlgru_scan_workspace_bytes": ([_I64, _I64, _I64], _SZ),
+    "mmf_mlgru_scan": ([_P, _P, _P, _P, _I64, _I64, _I64, _P, _SZ, _P], ctypes.c_int),
+    "mmf_mlgru_workspace_bytes": ([_I64, _I64, _I64], _SZ),
+    "mmf_mlgru_fwd": ([_P, ctypes.c_int, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P,
+                       _I64, _I64, _I64, _P, _SZ, _P], ctypes.c_int),
 }
 for _name, (_args, _res) in _SIGNATURES.items():
     _f = getattr(_lib, _name)
@@ -281,6 +294,112 @@ def mmf_ternary_gemm_glu(q: torch.Tensor, a_scale: torch.Tensor, q_rowsum: torch
                                      _ptr(w_scales), _ptr(p), M, K, L, _stream(stream)))
 
 
+def _ws_args(workspace: torch.Tensor | None):
+    if workspace is None:
+        return _ptr(None), 0
+    _need(workspace, "workspace", torch.uint8, (workspace.numel(),))
+    return _ptr(workspace), workspace.numel()
+
+
+def mmf_bitlinear_fwd_bias(x: torch.Tensor, gamma: torch.Tensor | None, Wpacked: torch.Tensor,
+                           w_scale: torch.Tensor, bias: torch.Tensor, y: torch.Tensor,
+                           stream=None) -> None:
+    """y f32 [M][N] = BitLinear(x) + bias [N] (N % 4 == 0)."""
+    M, K = x.shape
+    N = Wpacked.shape[1]
+    is_f32 = _x_kind(x)
+    _need(x, "x", x.dtype, (M, K))
+    if gamma is not None:
+        _need(gamma, "gamma", torch.float32, (K,))
+    _need(Wpacked, "Wpacked", torch.int32, (K // 16, N))
+    _need(w_scale, "w_scale", torch.float32, (1,))
+    _need(bias, "bias", torch.float32, (N,))
+    _need(y, "y", torch.float32, (M, N))
+    _check(_lib.mmf_bitlinear_fwd_bias(_ptr(x), int(is_f32), _ptr(gamma), _ptr(Wpacked),
+                                       _ptr(w_scale), _ptr(bias), _ptr(y), M, K, N,
+                                       _stream(stream)))
+
+
+def mmf_mlgru_proj_workspace_bytes(M: int, K: int, d: int) -> int:
+    return int(_lib.mmf_mlgru_proj_workspace_bytes(M, K, d))
+
+
+def mmf_mlgru_scan_workspace_bytes(B: int, T: int, d: int) -> int:
+    return int(_lib.mmf_mlgru_scan_workspace_bytes(B, T, d))
+
+
+def mmf_mlgru_workspace_bytes(B: int, T: int, d: int) -> int:
+    return int(_lib.mmf_mlgru_workspace_bytes(B, T, d))
+
+
+def mmf_mlgru_proj(x: torch.Tensor, gamma: torch.Tensor | None, Wfcg: torch.Tensor,
+                   w_scales: torch.Tensor, bias: torch.Tensor | None, lb: torch.Tensor | None,
+                   fcg: torch.Tensor, workspace: torch.Tensor | None = None, stream=None) -> None:
+    """MLGRU input projections and gates: fcg f32 [M][3d] (f | c | g) from x
+    bf16/f32 [M][K], Wfcg [K/16][3d], w_scales [3], bias [3d] or None, lb [d]
+    or None."""
+    M, K = x.shape
+    d = Wfcg.shape[1] // 3
+    is_f32 = _x_kind(x)
+    _need(x, "x", x.dtype, (M, K))
+    if gamma is not None:
+        _need(gamma, "gamma", torch.float32, (K,))
+    _need(Wfcg, "Wfcg", torch.int32, (K // 16, 3 * d))
+    _need(w_scales, "w_scales", torch.float32, (3,))
+    if bias is not None:
+        _need(bias, "bias", torch.float32, (3 * d,))
+    if lb is not None:
+        _need(lb, "lb", torch.float32, (d,))
+    _need(fcg, "fcg", torch.float32, (M, 3 * d))
+    wp, wn = _ws_args(workspace)
+    _check(_lib.mmf_mlgru_proj(_ptr(x), int(is_f32), _ptr(gamma), _ptr(Wfcg), _ptr(w_scales),
+                               _ptr(bias), _ptr(lb), _ptr(fcg), M, K, d, wp, wn, _stream(stream)))
+
+
+def mmf_mlgru_scan(fcg: torch.Tensor, B: int, T: int, h0: torch.Tensor | None,
+                   o_prime: torch.Tensor, h_last: torch.Tensor | None,
+                   workspace: torch.Tensor | None = None, stream=None) -> None:
+    """MLGRU recurrence and output gate over B sequences of T tokens (rows
+    b*T + t): o_prime f32 [B*T][d], final state h_last [B][d] (may be h0)."""
+    d = fcg.shape[1] // 3
+    _need(fcg, "fcg", torch.float32, (B * T, 3 * d))
+    if h0 is not None:
+        _need(h0, "h0", torch.float32, (B, d))
+    _need(o_prime, "o_prime", torch.float32, (B * T, d))
+    if h_last is not None:
+        _need(h_last, "h_last", torch.float32, (B, d))
+    wp, wn = _ws_args(workspace)
+    _check(_lib.mmf_mlgru_scan(_ptr(fcg), _ptr(h0), _ptr(o_prime), _ptr(h_last), B, T, d, wp, wn,
+                               _stream(stream)))
+
+
+def mmf_mlgru_fwd(x: torch.Tensor, B: int, T: int, gamma: torch.Tensor | None,
+                  Wfcg: torch.Tensor, w_scales: torch.Tensor, bias: torch.Tensor | None,
+                  lb: torch.Tensor | None, h0: torch.Tensor | None, h_last: torch.Tensor | None,
+                  gamma_o: torch.Tensor | None, Wo: torch.Tensor, w_scale_o: torch.Tensor,
+                  b_o: torch.Tensor | None, o: torch.Tensor,
+                  workspace: torch.Tensor | None = None, stream=None) -> None:
+    """The whole MLGRU token mixer: o f32 [B*T][d] from x bf16/f32 [B*T][d]."""
+    d = Wo.shape[1]
+    is_f32 = _x_kind(x)
+    _need(x, "x", x.dtype, (B * T, d))
+    for name, t, shape in (("gamma", gamma, (d,)), ("bias", bias, (3 * d,)), ("lb", lb, (d,)),
+                           ("h0", h0, (B, d)), ("h_last", h_last, (B, d)),
+                           ("gamma_o", gamma_o, (d,)), ("b_o", b_o, (d,))):
+        if t is not None:
+            _need(t, name, torch.float32, shape)
+    _need(Wfcg, "Wfcg", torch.int32, (d // 16, 3 * d))
+    _need(w_scales, "w_scales", torch.float32, (3,))
+    _need(Wo, "Wo", torch.int32, (d // 16, d))
+    _need(w_scale_o, "w_scale_o", torch.float32, (1,))
+    _need(o, "o", torch.float32, (B * T, d))
+    wp, wn = _ws_args(workspace)
+    _check(_lib.mmf_mlgru_fwd(_ptr(x), int(is_f32), _ptr(gamma), _ptr(Wfcg), _ptr(w_scales),
+                              _ptr(bias), _ptr(lb), _ptr(h0), _ptr(h_last), _ptr(gamma_o),
+                              _ptr(Wo), _ptr(w_scale_o), _ptr(b_o), _ptr(o), B, T, d, wp, wn,
+                              _stream(stream)))
+
+
 # ---------------------------------------------------------------------------
 # allocating conveniences (outputs allocated with torch on the inputs' device)
 # ---------------------------------------------------------------------------
@@ -316,3 +435,21 @@ def glu(x: torch.Tensor, gamma: torch.Tensor | None, Wgu_packed: torch.Tensor,
     p = torch.empty((x.shape[0], Wgu_packed.shape[1] // 2), dtype=torch.float32, device=x.device)
     mmf_glu_fwd(x, gamma, Wgu_packed, w_scales, p, stream)
     return p
+
+
+def mlgru_proj(x: torch.Tensor, gamma: torch.Tensor | None, Wfcg: torch.Tensor,
+               w_scales: torch.Tensor, bias: torch.Tensor | None = None,
+               lb: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """Returns fcg float32 [M][3d]."""
+    fcg = torch.empty((x.shape[0], Wfcg.shape[1]), dtype=torch.float32, device=x.device)
+    mmf_mlgru_proj(x, gamma, Wfcg, w_scales, bias, lb, fcg, None, stream)
+    return fcg
+
+
+def mlgru_scan(fcg: torch.Tensor, B: int, T: int, h0: torch.Tensor | None = None, stream=None):
+    """Returns (o_prime float32 [B*T][d], h_last float32 [B][d])."""
+    d = fcg.shape[1] // 3
+    o = torch.empty((B * T, d), dtype=torch.float32, device=fcg.device)
+    h = torch.empty((B, d), dtype=torch.float32, device=fcg.device)
+    mmf_mlgru_scan(fcg, B, T, h0, o, h, None, stream)
+    return o, h

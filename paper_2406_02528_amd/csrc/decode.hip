@@ -317,6 +317,7 @@ struct Params {
   int64_t N;
   int K;
   int q_bytes;
+  Affine affine;
 };
 
 // The weights of a workgroup's columns are streamed in "slots": wave w owns
@@ -333,6 +334,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(const Params prm) {
   const Shared sh = carve(smem, prm.q_bytes);
   // read at entry: its latency then overlaps the rest of the kernel
   const float wscale = EP == Epilogue::kDequantF32 ? prm.w_scale[0] : 0.0f;
+  static_assert(EP != Epilogue::kAffineF32 || S != Src::kQuantised, "affine epilogue from x only");
   constexpr int C = kWave / H;  // columns per workgroup
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -365,6 +367,16 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(const Params prm) {
     qs.load(prm.q, prm.a_scale, prm.q_rowsum, K, sh);
   } else {
     rows.load(prm.x, prm.gamma, K);
+  }
+  // the factors of the column this thread writes in the affine epilogue
+  // (issued after the token rows, so a wait for those leaves them in flight)
+  ColAffine col{};
+  if constexpr (EP == Epilogue::kAffineF32) {
+    const int64_t cn = static_cast<int64_t>(blockIdx.x) * C + tid % C;
+    col = load_col_affine(prm.affine, prm.w_scale, static_cast<uint32_t>(N),
+                          cn < N ? static_cast<uint32_t>(cn) : 0u);
+  }
+  if constexpr (S != Src::kQuantised) {
     if constexpr (kWeightDelay < 0) {
       rows.begin(sh);
       __syncthreads();
@@ -466,9 +478,12 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(const Params prm) {
     }
     if (nn < N) {
       const int v = sh.red[m * kWave + cc] - rsum;
-      if constexpr (EP == Epilogue::kDequantF32)
+      if constexpr (EP == Epilogue::kDequantF32) {
         static_cast<float*>(prm.out)[m * N + nn] = static_cast<float>(v) * (sh.a_scale[m] * wscale);
-      else
+      } else if constexpr (EP == Epilogue::kAffineF32) {
+        const float z = static_cast<float>(v) * (sh.a_scale[m] * col.ws) + col.bias;
+        static_cast<float*>(prm.out)[m * N + nn] = affine_act(z, col.act, col.lb);
+      } else
         static_cast<int32_t*>(prm.out)[m * N + nn] = v;
     }
   }
@@ -481,7 +496,7 @@ hipError_t launch_one(const DecodeArgs& a, hipStream_t stream) {
   const int region = ((MT * a.K + kLdsDmaChunk - 1) / kLdsDmaChunk) * kLdsDmaChunk;
   const dim3 grid(static_cast<unsigned>((a.N + C - 1) / C));
   const Params prm{a.Wpacked, a.x, a.gamma, a.q, a.a_scale, a.q_rowsum, a.w_scale, a.out,
-                   a.N, a.K, region};
+                   a.N, a.K, region, a.affine};
   hipLaunchKernelGGL((decode_kernel<MT, H, S, VP, PF, EP>), grid, dim3(kThreads), region + kScalarBytes,
                      stream, prm);
   return hipGetLastError();
@@ -558,6 +573,11 @@ bool decode_fits(int64_t mt, int K, int64_t N, bool from_x, bool x_is_f32) {
 
 hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream) {
   const int mt = static_cast<int>(a.M);  // 1..8; the caller slices larger M
+  if (a.epilogue == Epilogue::kAffineF32) {
+    if (a.q != nullptr) return hipErrorInvalidValue;
+    if (a.x_is_f32) return dispatch_mt<Src::kF32, Epilogue::kAffineF32>(mt, a, stream);
+    return dispatch_mt<Src::kBf16, Epilogue::kAffineF32>(mt, a, stream);
+  }
   if (a.q != nullptr) {
     if (a.epilogue == Epilogue::kDequantF32)
       return dispatch_mt<Src::kQuantised, Epilogue::kDequantF32>(mt, a, stream);

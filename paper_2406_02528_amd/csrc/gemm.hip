@@ -113,7 +113,7 @@ template <int BM, int BN, int WM, int WN, int BK, int S, bool BX4, Epilogue EP>
 __global__ __launch_bounds__((Tiling<BM, BN, WM, WN, BK, S, BX4>::kThreads)) void gemm_kernel(
     const int8_t* __restrict__ q, const float* __restrict__ a_scale,
     const int32_t* __restrict__ q_rowsum, const uint32_t* __restrict__ Wp,
-    const float* __restrict__ w_scale, void* __restrict__ out, int M, int K, int N) {
+    const float* __restrict__ w_scale, void* __restrict__ out, int M, int K, int N, const Affine aff) {
   using T = Tiling<BM, BN, WM, WN, BK, S, BX4>;
   constexpr int FM = T::FM, FN = T::FN, KS = T::KS;
   // S ring slots, then the tile's per-row dequantisation factors
@@ -318,7 +318,7 @@ __global__ __launch_bounds__((Tiling<BM, BN, WM, WN, BK, S, BX4>::kThreads)) voi
   // (g, l16) holds row l16 and columns 4 g .. 4 g + 3 of each 16 x 16 block ----
   const int* s_rsum = reinterpret_cast<const int*>(smem + S * T::kStageBytes);
   const float* s_scale = reinterpret_cast<const float*>(smem + S * T::kStageBytes + 4 * BM);
-  const float ws = (EP != Epilogue::kRawI32) ? w_scale[0] : 0.0f;
+  const float ws = (EP == Epilogue::kDequantF32 || EP == Epilogue::kGluF32) ? w_scale[0] : 0.0f;
   const float ws_u = (EP == Epilogue::kGluF32) ? w_scale[1] : 0.0f;
   __syncthreads();
   constexpr uint32_t kOut = 0x80000000u;
@@ -360,6 +360,17 @@ __global__ __launch_bounds__((Tiling<BM, BN, WM, WN, BK, S, BX4>::kThreads)) voi
   const uint32_t out_bytes = static_cast<uint32_t>(M) * static_cast<uint32_t>(N) * 4u;
   const __amdgpu_buffer_rsrc_t orsrc =
       __builtin_amdgcn_make_buffer_rsrc(out, 0, static_cast<int>(out_bytes), kBufferFlags);
+  // affine epilogue: bias, lower bound, scale and activation of the lane's
+  // four columns in each 16-column block (N % 16 == 0, one segment per block)
+  ColAffine4 cf[FN];
+  if constexpr (EP == Epilogue::kAffineF32) {
+    static_assert(BX4, "affine output needs N % 4 == 0");
+#pragma unroll
+    for (int f = 0; f < FN; ++f) {
+      const int n = n0 + wn * WN + f * 16 + 4 * g;
+      cf[f] = load_col_affine4(aff, w_scale, static_cast<uint32_t>(N), n < N ? static_cast<uint32_t>(n) : 0u);
+    }
+  }
 #pragma unroll
   for (int fm = 0; fm < FM; ++fm) {
     const int lr = wm * WM + fm * 16 + l16;
@@ -374,7 +385,12 @@ __global__ __launch_bounds__((Tiling<BM, BN, WM, WN, BK, S, BX4>::kThreads)) voi
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int d = acc[fm][f][r] - rs;
-        v[r] = (EP == Epilogue::kDequantF32) ? __float_as_int(static_cast<float>(d) * sc) : d;
+        if constexpr (EP == Epilogue::kAffineF32) {
+          const float z = static_cast<float>(d) * (s_scale[lr] * cf[f].ws) + cf[f].bias[r];
+          v[r] = __float_as_int(affine_act(z, cf[f].act, cf[f].lb[r]));
+        } else {
+          v[r] = (EP == Epilogue::kDequantF32) ? __float_as_int(static_cast<float>(d) * sc) : d;
+        }
       }
       if constexpr (BX4) {
         // N % 4 == 0: the four columns are all inside or all past N
@@ -405,20 +421,28 @@ hipError_t launch_cfg(const ContractArgs& a, int64_t m_begin, int64_t m_rows, hi
     hipLaunchKernelGGL((gemm_kernel<BM, BN, WM, WN, BK, S, BX4, Epilogue::kDequantF32>), grid, block, 0,
                        stream, q, as, rs, a.Wpacked, a.w_scale,
                        static_cast<void*>(static_cast<float*>(a.out) + m_begin * a.N),
-                       static_cast<int>(m_rows), a.K, static_cast<int>(a.N));
-  else if (a.epilogue == Epilogue::kGluF32) {
+                       static_cast<int>(m_rows), a.K, static_cast<int>(a.N), a.affine);
+  else if (a.epilogue == Epilogue::kAffineF32) {
+    if constexpr (BX4)
+      hipLaunchKernelGGL((gemm_kernel<BM, BN, WM, WN, BK, S, true, Epilogue::kAffineF32>), grid, block, 0,
+                         stream, q, as, rs, a.Wpacked, a.w_scale,
+                         static_cast<void*>(static_cast<float*>(a.out) + m_begin * a.N),
+                         static_cast<int>(m_rows), a.K, static_cast<int>(a.N), a.affine);
+    else
+      return hipErrorInvalidValue;
+  } else if (a.epilogue == Epilogue::kGluF32) {
     if constexpr (BX4)
       hipLaunchKernelGGL((gemm_kernel<BM, BN, WM, WN, BK, S, true, Epilogue::kGluF32>), grid, block, 0, stream,
                          q, as, rs, a.Wpacked, a.w_scale,
                          static_cast<void*>(static_cast<float*>(a.out) + m_begin * (a.N / 2)),
-                         static_cast<int>(m_rows), a.K, static_cast<int>(a.N));
+                         static_cast<int>(m_rows), a.K, static_cast<int>(a.N), a.affine);
     else
       return hipErrorInvalidValue;
   } else
     hipLaunchKernelGGL((gemm_kernel<BM, BN, WM, WN, BK, S, BX4, Epilogue::kRawI32>), grid, block, 0,
                        stream, q, as, rs, a.Wpacked, a.w_scale,
                        static_cast<void*>(static_cast<int32_t*>(a.out) + m_begin * a.N),
-                       static_cast<int>(m_rows), a.K, static_cast<int>(a.N));
+                       static_cast<int>(m_rows), a.K, static_cast<int>(a.N), a.affine);
   return hipGetLastError();
 }
 

@@ -199,6 +199,109 @@ int glu_alloc(const void* x, bool x_is_f32, const float* gamma, const uint32_t* 
   return hip_status(fe);
 }
 
+// ---- affine forward (bias and per-segment activations after the dequant) ----
+
+// Fused decode launches when every slice of at most 8 tokens fits the fused
+// kernel, else activation quantisation into `scratch` (fwd_scratch) and the
+// MFMA kernel for every M.
+int run_affine(const void* x, bool x_is_f32, const float* gamma, const uint32_t* Wpacked,
+               const float* w_scales, const mmf::Affine& aff, float* y, int64_t M, int64_t K,
+               int64_t N, char* scratch, hipStream_t stream) {
+  if (fused_decode(M, K, N, x_is_f32)) {
+    const size_t xsz = x_is_f32 ? 4 : 2;
+    for (int64_t m0 = 0; m0 < M; m0 += kDecodeMaxTokens) {
+      const int64_t mt = M - m0 < kDecodeMaxTokens ? M - m0 : kDecodeMaxTokens;
+      mmf::DecodeArgs d{static_cast<const char*>(x) + m0 * K * xsz, x_is_f32, gamma, nullptr,
+                        nullptr, nullptr, Wpacked, w_scales, y + m0 * N, mt,
+                        static_cast<int>(K), N, mmf::Epilogue::kAffineF32, aff};
+      if (mmf::launch_decode(d, stream) != hipSuccess) return MMF_ERR_HIP;
+    }
+    return MMF_OK;
+  }
+  const FwdScratch s = fwd_scratch(M, K);
+  int8_t* q = reinterpret_cast<int8_t*>(scratch + s.q_off);
+  float* a_scale = reinterpret_cast<float*>(scratch + s.a_off);
+  int32_t* rowsum = reinterpret_cast<int32_t*>(scratch + s.r_off);
+  if (mmf::launch_act_quant(x, x_is_f32, gamma, q, a_scale, rowsum, M, static_cast<int>(K), stream) !=
+      hipSuccess)
+    return MMF_ERR_HIP;
+  mmf::ContractArgs a{q, a_scale, rowsum, Wpacked, w_scales, y, M, static_cast<int>(K), N,
+                      mmf::Epilogue::kAffineF32, aff};
+  return hip_status(mmf::launch_gemm(a, stream));
+}
+
+// Runs `run(scratch)` on the caller's workspace (checked against `need`), or
+// on stream-ordered scratch allocated here when `workspace` is NULL.
+template <class F>
+int with_workspace(void* workspace, size_t workspace_bytes, size_t need, hipStream_t stream, F&& run) {
+  if (workspace != nullptr) {
+    if ((reinterpret_cast<uintptr_t>(workspace) & (kScratchAlign - 1)) != 0 || workspace_bytes < need)
+      return MMF_ERR_WORKSPACE;
+    return run(static_cast<char*>(workspace));
+  }
+  if (need == 0) return run(nullptr);
+  void* p = nullptr;
+  if (hipMallocAsync(&p, need, stream) != hipSuccess) return MMF_ERR_HIP;
+  const int st = run(static_cast<char*>(p));
+  const hipError_t fe = hipFreeAsync(p, stream);
+  if (st != MMF_OK) return st;
+  return hip_status(fe);
+}
+
+bool aligned16_or_null(const void* p) { return p == nullptr || aligned16(p); }
+
+// ---- MLGRU ----
+constexpr uint32_t kMlgruActs = mmf::kActSigmoidLb | (mmf::kActSilu << 2) | (mmf::kActIdentity << 4);
+
+int check_mlgru_d(int64_t d) {
+  if (d <= 0 || d % 16 != 0 || d > kMaxMN / 3) return MMF_ERR_SHAPE;
+  return MMF_OK;
+}
+
+int check_mlgru_proj(const void* x, const float* gamma, const uint32_t* Wfcg, const float* w_scales,
+                     const float* bias, const float* lb, const float* fcg, int64_t M, int64_t K,
+                     int64_t d) {
+  if (int st = check_mlgru_d(d)) return st;
+  if (int st = check_shape(M, K, 3 * d)) return st;
+  if (M == 0) return MMF_OK;
+  if (!x || !Wfcg || !w_scales || !fcg) return MMF_ERR_NULL;
+  if (!aligned16(x) || !aligned16(Wfcg) || !aligned16(fcg) || !aligned16_or_null(gamma) ||
+      !aligned16_or_null(bias) || !aligned16_or_null(lb))
+    return MMF_ERR_ALIGN;
+  return MMF_OK;
+}
+
+int check_mlgru_scan(const float* fcg, const float* h0, const float* o, const float* h_last,
+                     int64_t B, int64_t T, int64_t d) {
+  if (int st = check_mlgru_d(d)) return st;
+  if (B < 0 || T < 0 || B > kMaxMN || T > kMaxMN || (T > 0 && B > kMaxMN / T)) return MMF_ERR_SHAPE;
+  if (B == 0 || T == 0) return MMF_OK;
+  if (!fcg || !o) return MMF_ERR_NULL;
+  if (!aligned16(fcg) || !aligned16(o) || !aligned16_or_null(h0) || !aligned16_or_null(h_last))
+    return MMF_ERR_ALIGN;
+  return MMF_OK;
+}
+
+size_t scan_ws_bytes(int64_t B, int64_t T, int64_t d) {
+  return round_up(static_cast<size_t>(mmf::mlgru_scan_ws_floats(B, T, d)) * 4, kScratchAlign);
+}
+
+// Scratch of the whole mixer: fcg [M][3d], o' [M][d], the quantised
+// activations of either projection, the scan's chunk summaries.
+struct MlgruScratch {
+  size_t fcg_off, op_off, q_off, scan_off, total;
+};
+MlgruScratch mlgru_scratch(int64_t B, int64_t T, int64_t d) {
+  const size_t M = static_cast<size_t>(B) * static_cast<size_t>(T);
+  MlgruScratch s;
+  s.fcg_off = 0;
+  s.op_off = round_up(M * 3 * static_cast<size_t>(d) * 4, kScratchAlign);
+  s.q_off = s.op_off + round_up(M * static_cast<size_t>(d) * 4, kScratchAlign);
+  s.scan_off = s.q_off + fwd_scratch(static_cast<int64_t>(M), d).total;
+  s.total = s.scan_off + scan_ws_bytes(B, T, d);
+  return s;
+}
+
 }  // namespace
 
 extern "C" {
@@ -366,6 +469,107 @@ int mmf_ternary_gemm_glu(const int8_t* q, const float* a_scale, const int32_t* q
   mmf::ContractArgs a{q, a_scale, q_rowsum, Wgu_packed, w_scales, p, M, static_cast<int>(K), 2 * L,
                       mmf::Epilogue::kGluF32};
   return hip_status(mmf::launch_gemm(a, stream));
+}
+
+int mmf_bitlinear_fwd_bias(const void* x, int x_is_f32, const float* gamma,
+                           const uint32_t* Wpacked, const float* w_scale, const float* bias,
+                           float* y, int64_t M, int64_t K, int64_t N, hipStream_t stream) {
+  if (x_is_f32 != 0 && x_is_f32 != 1) return MMF_ERR_ARG;
+  if (int st = check_fwd(x, gamma, Wpacked, w_scale, y, M, K, N)) return st;
+  if (N % 4 != 0) return MMF_ERR_SHAPE;
+  if (M == 0 || N == 0) return MMF_OK;
+  if (!bias) return MMF_ERR_NULL;
+  if (!aligned16(bias)) return MMF_ERR_ALIGN;
+  mmf::Affine aff;
+  aff.bias = bias;
+  aff.seg = N;
+  aff.acts = mmf::kActIdentity;
+  const size_t need = fused_decode(M, K, N, x_is_f32 == 1) ? 0 : fwd_scratch(M, K).total;
+  return with_workspace(nullptr, 0, need, stream, [&](char* scratch) {
+    return run_affine(x, x_is_f32 == 1, gamma, Wpacked, w_scale, aff, y, M, K, N, scratch, stream);
+  });
+}
+
+size_t mmf_mlgru_proj_workspace_bytes(int64_t M, int64_t K, int64_t d) {
+  if (check_mlgru_d(d) != MMF_OK || check_shape(M, K, 3 * d) != MMF_OK) return 0;
+  return fwd_scratch(M, K).total;
+}
+
+int mmf_mlgru_proj(const void* x, int x_is_f32, const float* gamma, const uint32_t* Wfcg,
+                   const float* w_scales, const float* bias, const float* lb, float* fcg,
+                   int64_t M, int64_t K, int64_t d, void* workspace, size_t workspace_bytes,
+                   hipStream_t stream) {
+  if (x_is_f32 != 0 && x_is_f32 != 1) return MMF_ERR_ARG;
+  if (int st = check_mlgru_proj(x, gamma, Wfcg, w_scales, bias, lb, fcg, M, K, d)) return st;
+  if (M == 0) return MMF_OK;
+  mmf::Affine aff;
+  aff.bias = bias;
+  aff.lb = lb;
+  aff.seg = d;
+  aff.acts = kMlgruActs;
+  return with_workspace(workspace, workspace_bytes, fwd_scratch(M, K).total, stream, [&](char* scratch) {
+    return run_affine(x, x_is_f32 == 1, gamma, Wfcg, w_scales, aff, fcg, M, K, 3 * d, scratch, stream);
+  });
+}
+
+size_t mmf_mlgru_scan_workspace_bytes(int64_t B, int64_t T, int64_t d) {
+  if (check_mlgru_d(d) != MMF_OK || B < 0 || T < 0) return 0;
+  return scan_ws_bytes(B, T, d);
+}
+
+int mmf_mlgru_scan(const float* fcg, const float* h0, float* o_prime, float* h_last, int64_t B,
+                   int64_t T, int64_t d, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  if (int st = check_mlgru_scan(fcg, h0, o_prime, h_last, B, T, d)) return st;
+  if (B == 0 || T == 0) return MMF_OK;
+  return with_workspace(workspace, workspace_bytes, scan_ws_bytes(B, T, d), stream, [&](char* scratch) {
+    return hip_status(mmf::launch_mlgru_scan(fcg, h0, o_prime, h_last, B, T, d,
+                                             reinterpret_cast<float*>(scratch), stream));
+  });
+}
+
+size_t mmf_mlgru_workspace_bytes(int64_t B, int64_t T, int64_t d) {
+  if (check_mlgru_d(d) != MMF_OK || B < 0 || T < 0 || (T > 0 && B > kMaxMN / T)) return 0;
+  return mlgru_scratch(B, T, d).total;
+}
+
+int mmf_mlgru_fwd(const void* x, int x_is_f32, const float* gamma, const uint32_t* Wfcg,
+                  const float* w_scales, const float* bias, const float* lb, const float* h0,
+                  float* h_last, const float* gamma_o, const uint32_t* Wo, const float* w_scale_o,
+                  const float* b_o, float* o, int64_t B, int64_t T, int64_t d, void* workspace,
+                  size_t workspace_bytes, hipStream_t stream) {
+  if (x_is_f32 != 0 && x_is_f32 != 1) return MMF_ERR_ARG;
+  if (int st = check_mlgru_d(d)) return st;
+  if (d > kMaxK) return MMF_ERR_SHAPE;
+  if (B < 0 || T < 0 || B > kMaxMN || T > kMaxMN || (T > 0 && B > kMaxMN / T)) return MMF_ERR_SHAPE;
+  const int64_t M = B * T;
+  if (M == 0) return MMF_OK;
+  if (!x || !Wfcg || !w_scales || !Wo || !w_scale_o || !o) return MMF_ERR_NULL;
+  if (!aligned16(x) || !aligned16(Wfcg) || !aligned16(Wo) || !aligned16(o) ||
+      !aligned16_or_null(gamma) || !aligned16_or_null(bias) || !aligned16_or_null(lb) ||
+      !aligned16_or_null(h0) || !aligned16_or_null(h_last) || !aligned16_or_null(gamma_o) ||
+      !aligned16_or_null(b_o))
+    return MMF_ERR_ALIGN;
+  const MlgruScratch s = mlgru_scratch(B, T, d);
+  return with_workspace(workspace, workspace_bytes, s.total, stream, [&](char* scratch) {
+    float* fcg = reinterpret_cast<float*>(scratch + s.fcg_off);
+    float* op = reinterpret_cast<float*>(scratch + s.op_off);
+    mmf::Affine in;
+    in.bias = bias;
+    in.lb = lb;
+    in.seg = d;
+    in.acts = kMlgruActs;
+    int st = run_affine(x, x_is_f32 == 1, gamma, Wfcg, w_scales, in, fcg, M, d, 3 * d,
+                        scratch + s.q_off, stream);
+    if (st != MMF_OK) return st;
+    if (mmf::launch_mlgru_scan(fcg, h0, op, h_last, B, T, d, reinterpret_cast<float*>(scratch + s.scan_off),
+                               stream) != hipSuccess)
+      return MMF_ERR_HIP;
+    mmf::Affine out;
+    out.bias = b_o;
+    out.seg = d;
+    out.acts = mmf::kActIdentity;
+    return run_affine(op, true, gamma_o, Wo, w_scale_o, out, o, M, d, d, scratch + s.q_off, stream);
+  });
 }
 
 int mmf_set_path(int path) {

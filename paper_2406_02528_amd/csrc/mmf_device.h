@@ -1,8 +1,11 @@
 // Device helpers shared by the gfx950 kernels: wave64 reductions through DPP
-// and ds_swizzle, and the 2-bit code unpacking of the packed weight format.
+// and readlane, the RMSNorm root, the 2-bit code unpacking of the packed
+// weight format and the affine (bias + activation) epilogue.
 #pragma once
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+
+#include "mmf_launch.h"
 
 namespace mmf {
 
@@ -143,6 +146,72 @@ __device__ __forceinline__ int dot4(uint32_t a, uint32_t b, int c) {
 
 __device__ __forceinline__ float bf16_to_f32(uint16_t b) {
   return __uint_as_float(static_cast<uint32_t>(b) << 16);
+}
+
+// ---------------------------------------------------------------------------
+// Affine epilogue.  z = (float)acc * (a_scale * w_scale[s]) + bias[n] in
+// fp32, one rounding per operation, then the activation of segment s:
+// identity, lb + (1 - lb) / (1 + e^-z) (sigmoid with a lower bound) or
+// z / (1 + e^-z) (SiLU).  The column factors go through buffer resources of
+// size 0 when an array is absent, which read as 0 with no memory access.
+// ---------------------------------------------------------------------------
+constexpr int kBufferWord3 = 0x00020000;  // gfx9 buffer descriptor word 3
+
+__device__ __forceinline__ float affine_act(float z, uint32_t act, float lb) {
+  if (act == kActIdentity) return z;
+  const float den = 1.0f + expf(-z);
+  if (act == kActSilu) return z / den;
+  return (1.0f - lb) / den + lb;
+}
+
+struct ColAffine {
+  float ws, bias, lb;
+  uint32_t act;
+};
+
+// Factors of column n (< N, a multiple of seg) of an affine epilogue.
+__device__ __forceinline__ ColAffine load_col_affine(const Affine& a, const float* w_scale,
+                                                     uint32_t N, uint32_t n) {
+  const uint32_t seg = static_cast<uint32_t>(a.seg);
+  const uint32_t s = n / seg;
+  const __amdgpu_buffer_rsrc_t ws_r = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<float*>(w_scale), 0, static_cast<int>((N / seg) * 4u), kBufferWord3);
+  const __amdgpu_buffer_rsrc_t b_r = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<float*>(a.bias), 0, a.bias != nullptr ? static_cast<int>(N * 4u) : 0, kBufferWord3);
+  const __amdgpu_buffer_rsrc_t l_r = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<float*>(a.lb), 0, a.lb != nullptr ? static_cast<int>(seg * 4u) : 0, kBufferWord3);
+  ColAffine c;
+  c.ws = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(ws_r, 4u * s, 0, 0));
+  c.bias = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(b_r, 4u * n, 0, 0));
+  c.lb = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(l_r, 4u * (n - s * seg), 0, 0));
+  c.act = (a.acts >> (2u * s)) & 3u;
+  return c;
+}
+
+// Four consecutive columns n .. n + 3 (n % 4 == 0, seg % 16 == 0: one segment).
+typedef float v4f __attribute__((ext_vector_type(4)));
+struct ColAffine4 {
+  float ws;
+  v4f bias, lb;
+  uint32_t act;
+};
+
+__device__ __forceinline__ ColAffine4 load_col_affine4(const Affine& a, const float* w_scale,
+                                                       uint32_t N, uint32_t n) {
+  const uint32_t seg = static_cast<uint32_t>(a.seg);
+  const uint32_t s = n / seg;
+  const __amdgpu_buffer_rsrc_t ws_r = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<float*>(w_scale), 0, static_cast<int>((N / seg) * 4u), kBufferWord3);
+  const __amdgpu_buffer_rsrc_t b_r = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<float*>(a.bias), 0, a.bias != nullptr ? static_cast<int>(N * 4u) : 0, kBufferWord3);
+  const __amdgpu_buffer_rsrc_t l_r = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<float*>(a.lb), 0, a.lb != nullptr ? static_cast<int>(seg * 4u) : 0, kBufferWord3);
+  ColAffine4 c;
+  c.ws = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(ws_r, 4u * s, 0, 0));
+  c.bias = __builtin_bit_cast(v4f, __builtin_amdgcn_raw_buffer_load_b128(b_r, 4u * n, 0, 0));
+  c.lb = __builtin_bit_cast(v4f, __builtin_amdgcn_raw_buffer_load_b128(l_r, 4u * (n - s * seg), 0, 0));
+  c.act = (a.acts >> (2u * s)) & 3u;
+  return c;
 }
 
 }  // namespace mmf

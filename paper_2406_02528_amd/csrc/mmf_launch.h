@@ -25,7 +25,22 @@ hipError_t launch_ternarize(const float* W, int64_t N, int K, uint32_t* Wpacked,
 // the two up-projections of a GLU interleaved in blocks of 16 (gate, up,
 // gate, ...), w_scale holds [gate, up], and the output is the gated
 // representation SiLU(g) * u, N / 2 columns wide.
-enum class Epilogue { kDequantF32, kRawI32, kGluF32 };
+enum class Epilogue { kDequantF32, kRawI32, kGluF32, kAffineF32 };
+
+// kAffineF32: y = act_s(acc * a_scale * w_scale[s] + bias[n]) with the columns
+// in segments of `seg` (s = n / seg, seg % 16 == 0) and one activation per
+// segment, 2 bits each in `acts` (segment s at bits 2s, 2s + 1):
+//   kActIdentity  y = z
+//   kActSigmoidLb y = lb + (1 - lb) sigmoid(z), lb = lb[n % seg] (0 if null)
+//   kActSilu      y = z sigmoid(z)
+// bias may be null (no bias).  At most 16 segments.
+constexpr uint32_t kActIdentity = 0, kActSigmoidLb = 1, kActSilu = 2;
+struct Affine {
+  const float* bias = nullptr;  // [N]
+  const float* lb = nullptr;    // [seg]
+  int64_t seg = 0;
+  uint32_t acts = 0;
+};
 
 struct ContractArgs {
   const int8_t* q;          // [M][K]
@@ -38,6 +53,7 @@ struct ContractArgs {
   int K;
   int64_t N;
   Epilogue epilogue;
+  Affine affine{};          // kAffineF32 only; w_scale then holds N / seg values
 };
 
 // Decode contraction with q read from global memory (scalar loads); any K,
@@ -62,6 +78,7 @@ struct DecodeArgs {
   int K;
   int64_t N;
   Epilogue epilogue;
+  Affine affine{};          // kAffineF32 only
 };
 bool decode_fits(int64_t mt, int K, int64_t N, bool from_x, bool x_is_f32);
 hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream);
@@ -70,6 +87,17 @@ hipError_t launch_gemm(const ContractArgs& a, hipStream_t stream);
 
 // Interleave the packed gate and up projections of a GLU, [K/16][L] each,
 // into [K/16][2L] blocks of 16 columns (gate, up, gate, ...); L % 16 == 0.
+// MLGRU recurrence over B sequences of T tokens, fcg [B*T][3d] (forget gate,
+// candidate, output gate), d % 4 == 0:
+//   h_t = f_t h_{t-1} + (1 - f_t) c_t,  o'_t = g_t sigmoid(h_t).
+// The sequence is cut into chunks of `chunk` tokens; with more than one
+// chunk `ws` holds mlgru_scan_ws_floats(B, T, d) floats (chunk summaries and
+// carries), else it is unused.  h0 may be null (h_0 = 0) and may alias h_last.
+int64_t mlgru_chunk_len(int64_t B, int64_t T, int64_t d);
+int64_t mlgru_scan_ws_floats(int64_t B, int64_t T, int64_t d);
+hipError_t launch_mlgru_scan(const float* fcg, const float* h0, float* o, float* h_last, int64_t B,
+                             int64_t T, int64_t d, float* ws, hipStream_t stream);
+
 hipError_t launch_glu_pack(const uint32_t* Wg, const uint32_t* Wu, int64_t L, int K, uint32_t* Wgu,
                            hipStream_t stream);
 

@@ -172,3 +172,64 @@ def test_glu_argument_checks(mmf):
     assert lib.mmf_ternary_gemm_glu(A, B, C, D, E, A, 4, 16, 24, S) == 2
     assert lib.mmf_ternary_gemm_glu(A, B, None, D, E, A, 4, 16, 32, S) == 1
     assert lib.mmf_ternary_gemm_glu(A, B, C, D, E, BAD, 4, 16, 32, S) == 3
+
+
+def test_bias_argument_checks(mmf):
+    lib = _c(mmf)
+    assert lib.mmf_bitlinear_fwd_bias(A, 0, B, C, D, E, A, 4, 16, 6, S) == 2    # N % 4
+    assert lib.mmf_bitlinear_fwd_bias(A, 0, B, C, D, None, A, 4, 16, 8, S) == 1
+    assert lib.mmf_bitlinear_fwd_bias(A, 0, B, C, D, BAD, A, 4, 16, 8, S) == 3
+    assert lib.mmf_bitlinear_fwd_bias(A, 2, B, C, D, E, A, 4, 16, 8, S) == 6
+    assert lib.mmf_bitlinear_fwd_bias(A, 0, B, C, D, E, A, 4, 24, 8, S) == 2
+    assert lib.mmf_bitlinear_fwd_bias(None, 0, None, None, None, None, None, 0, 16, 8, S) == 0
+
+
+def test_mlgru_argument_checks(mmf):
+    lib = _c(mmf)
+    W = 0x100000   # aligned stand-in workspace
+    # projection: d a positive multiple of 16, K as for the forward
+    for d in (0, -16, 24):
+        assert lib.mmf_mlgru_proj(A, 0, B, C, D, E, A, B, 4, 16, d, None, 0, S) == 2
+    assert lib.mmf_mlgru_proj(A, 0, B, C, D, E, A, B, 4, 24, 16, None, 0, S) == 2
+    assert lib.mmf_mlgru_proj(None, 0, B, C, D, E, A, B, 4, 16, 16, None, 0, S) == 1
+    assert lib.mmf_mlgru_proj(A, 0, B, None, D, E, A, B, 4, 16, 16, None, 0, S) == 1
+    assert lib.mmf_mlgru_proj(A, 0, B, C, None, E, A, B, 4, 16, 16, None, 0, S) == 1
+    assert lib.mmf_mlgru_proj(A, 0, B, C, D, E, A, None, 4, 16, 16, None, 0, S) == 1
+    assert lib.mmf_mlgru_proj(A, 0, B, C, D, BAD, A, B, 4, 16, 16, None, 0, S) == 3
+    assert lib.mmf_mlgru_proj(A, 0, B, C, D, E, BAD, B, 4, 16, 16, None, 0, S) == 3
+    assert lib.mmf_mlgru_proj(A, 5, B, C, D, E, A, B, 4, 16, 16, None, 0, S) == 6
+    need = mmf.mmf_mlgru_proj_workspace_bytes(4, 16, 16)
+    assert need > 0 and need % 256 == 0
+    assert lib.mmf_mlgru_proj(A, 0, B, C, D, E, A, B, 4, 16, 16, W, need - 1, S) == 4
+    assert lib.mmf_mlgru_proj(A, 0, B, C, D, E, A, B, 4, 16, 16, W + 16, need, S) == 4
+    assert lib.mmf_mlgru_proj(None, 0, None, None, None, None, None, None, 0, 16, 16, None, 0, S) == 0
+    # recurrence
+    assert lib.mmf_mlgru_scan(A, B, C, D, 2, 3, 24, None, 0, S) == 2
+    assert lib.mmf_mlgru_scan(A, B, C, D, -1, 3, 16, None, 0, S) == 2
+    assert lib.mmf_mlgru_scan(A, B, C, D, 2 ** 20, 2 ** 12, 16, None, 0, S) == 2   # B*T > 2^31-1
+    assert lib.mmf_mlgru_scan(None, B, C, D, 2, 3, 16, None, 0, S) == 1
+    assert lib.mmf_mlgru_scan(A, B, None, D, 2, 3, 16, None, 0, S) == 1
+    assert lib.mmf_mlgru_scan(A, BAD, C, D, 2, 3, 16, None, 0, S) == 3
+    assert lib.mmf_mlgru_scan(A, B, C, BAD, 2, 3, 16, None, 0, S) == 3
+    assert lib.mmf_mlgru_scan(None, None, None, None, 0, 3, 16, None, 0, S) == 0
+    assert lib.mmf_mlgru_scan(None, None, None, None, 2, 0, 16, None, 0, S) == 0
+    # a short sequence is one chunk and needs no workspace; a long one does
+    assert mmf.mmf_mlgru_scan_workspace_bytes(1, 1, 2048) == 0
+    assert mmf.mmf_mlgru_scan_workspace_bytes(4, 16, 64) == 0
+    need = mmf.mmf_mlgru_scan_workspace_bytes(1, 2048, 2048)
+    assert need >= 3 * 2048 * 4 * 2 and need % 256 == 0
+    assert lib.mmf_mlgru_scan(A, B, C, D, 1, 2048, 2048, W, need - 1, S) == 4
+    # whole mixer
+    assert lib.mmf_mlgru_fwd(A, 0, B, C, D, E, A, B, C, D, E, A, B, C, 1, 2, 24, None, 0, S) == 2
+    assert lib.mmf_mlgru_fwd(A, 0, B, C, D, E, A, B, C, D, None, A, B, C, 1, 2, 32, None, 0, S) == 1
+    assert lib.mmf_mlgru_fwd(A, 0, B, C, D, E, A, B, C, D, E, None, B, C, 1, 2, 32, None, 0, S) == 1
+    assert lib.mmf_mlgru_fwd(A, 0, B, C, D, E, A, B, C, D, E, A, B, None, 1, 2, 32, None, 0, S) == 1
+    assert lib.mmf_mlgru_fwd(A, 0, B, C, D, E, A, BAD, C, D, E, A, B, C, 1, 2, 32, None, 0, S) == 3
+    assert lib.mmf_mlgru_fwd(A, 0, B, C, D, E, A, B, C, D, E, A, BAD, C, 1, 2, 32, None, 0, S) == 3
+    assert lib.mmf_mlgru_fwd(A, 9, B, C, D, E, A, B, C, D, E, A, B, C, 1, 2, 32, None, 0, S) == 6
+    need = mmf.mmf_mlgru_workspace_bytes(1, 2, 32)
+    assert need >= 2 * 32 * 16 and need % 256 == 0
+    assert lib.mmf_mlgru_fwd(A, 0, B, C, D, E, A, B, C, D, E, A, B, C, 1, 2, 32, W, need - 1, S) == 4
+    assert lib.mmf_mlgru_fwd(None, 0, None, None, None, None, None, None, None, None, None, None,
+                             None, None, 0, 2, 32, None, 0, S) == 0
+    assert mmf.mmf_mlgru_workspace_bytes(1, 2048, 2048) >= 2048 * 2048 * 16

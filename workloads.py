@@ -17,6 +17,14 @@ the MLGRU gate projections f, c, g concatenated along the output dimension):
   large       M=16384, K=5120, N=27648    prefill at d = 5120 (GLU gate|up)
   large_dec   M=1,     K=5120, N=15360    decode at d = 5120 (f|c|g)
 
+MLGRU token-mixer workloads (``MLGRU_WORKLOADS``) at d = 2048: one decode
+step (B=1 sequence, T=1 token) and the prefill of one 2048-token sequence
+(the paper's inference setting, batch 1, sequence length 2048).  Their input
+projection f|c|g is the ``decode`` workload's [6144][2048] weight; the output
+projection W_o is [2048][2048] N(0, 0.02); biases U(-0.5, 0.5); the
+forget-gate lower bound U(0, 0.95) per channel (a deep layer's); the
+initial state N(0, 1) x 0.5 (a running sequence).
+
 Latent weights are N(0, 0.02) float32 of shape [N][K] (out x in).  RMSNorm
 scales are U(0.5, 1.5) except for ``tiny`` (all ones).  The seed of workload i
 and stream j is 240602528 + 10 i + j with j = 0 for x, 1 for W, 2 for gamma and
@@ -57,6 +65,71 @@ WORKLOADS = {
     "large": Workload("large", 5, 16384, 5120, 27648, "bf16", "normal", "uniform"),
     "large_dec": Workload("large_dec", 5, 1, 5120, 15360, "bf16", "normal", "uniform"),
 }
+
+
+@dataclass(frozen=True)
+class MlgruWorkload:
+    name: str
+    index: int          # seed index
+    B: int              # sequences
+    T: int              # tokens per sequence
+    d: int              # model width
+
+    @property
+    def M(self) -> int:
+        return self.B * self.T
+
+    @property
+    def ops(self) -> int:
+        """Effective dense ops of the two projections, 2 M (3d + d) d."""
+        return 2 * self.M * 4 * self.d * self.d
+
+
+MLGRU_WORKLOADS = {
+    "mlgru_decode": MlgruWorkload("mlgru_decode", 6, 1, 1, 2048),
+    "mlgru_prefill": MlgruWorkload("mlgru_prefill", 6, 1, 2048, 2048),
+}
+
+# seed streams of the MLGRU workloads beyond x (0), W_fcg (1), gamma (2)
+_MLGRU_STREAMS = {"w_o": 4, "gamma_o": 5, "bias": 6, "b_o": 7, "lb": 8, "h0": 9}
+
+
+def make_mlgru(w: MlgruWorkload) -> dict:
+    """Inputs of one MLGRU workload: x (bf16 bits and float32 values, [M][d]),
+    gamma [d], W_fcg [3d][d] (the decode workload's weights at d = 2048),
+    W_o [d][d], gamma_o [d], bias [3d], b_o [d], lb [d], h0 [B][d]."""
+    base = Workload(w.name, w.index, w.M, w.d, 3 * w.d, "bf16", "normal", "uniform")
+    x_bits, x_f32 = make_x(base)
+    gamma = make_gamma(base)
+    if w.d == WORKLOADS["decode_m1"].K:
+        W_fcg = make_w(WORKLOADS["decode_m1"])
+    else:
+        W_fcg = make_w(base)
+
+    def rng(name):
+        return np.random.default_rng(seed(w.index, _MLGRU_STREAMS[name]))
+
+    d = w.d
+    return {
+        "x_bits": x_bits, "x_f32": x_f32, "gamma": gamma, "W_fcg": W_fcg,
+        "W_o": (rng("w_o").standard_normal((d, d), dtype=np.float32) * np.float32(0.02)).astype(np.float32),
+        "gamma_o": rng("gamma_o").uniform(0.5, 1.5, d).astype(np.float32),
+        "bias": rng("bias").uniform(-0.5, 0.5, 3 * d).astype(np.float32),
+        "b_o": rng("b_o").uniform(-0.5, 0.5, d).astype(np.float32),
+        "lb": rng("lb").uniform(0.0, 0.95, d).astype(np.float32),
+        "h0": (rng("h0").standard_normal((w.B, d), dtype=np.float32) * np.float32(0.5)).astype(np.float32),
+    }
+
+
+def random_gates(rs: np.random.Generator, M: int, d: int, lb_max: float = 0.99):
+    """Random MLGRU gate rows [M][3d] for recurrence tests: forget gates
+    uniform in [low, 1) with a per-channel floor low ~ U(0, lb_max) (long and
+    short memories side by side), candidates and output gates N(0, 1)."""
+    low = rs.uniform(0.0, lb_max, d)
+    f = rs.uniform(low, 1.0, (M, d))
+    c = rs.standard_normal((M, d))
+    g = rs.standard_normal((M, d))
+    return np.concatenate([f, c, g], axis=1).astype(np.float32)
 
 
 def seed(index: int, stream: int) -> int:
