@@ -17,6 +17,13 @@ Workloads (shapes in workloads.py):
   channel_mixer -- the whole GLU channel mixer on that shape: glu_gate, then
       the down-projection BitLinear of p (K=5632, N=2048, its own RMSNorm).
       value = effective TOPS over both contractions.
+  mlgru_decode -- one token step of the MLGRU token mixer at d = 2048 (input
+      projections f|c|g with their gates, the recurrence, the output
+      projection with bias), state updated in place, for each of R distinct
+      weight sets totalling >= 1 GiB, from one HIP graph.  value = HBM GB/s of
+      algorithmic bytes per step.
+  mlgru_prefill -- the MLGRU token mixer over one 2048-token sequence at
+      d = 2048.  value = effective TOPS, 2*M*(3d + d)*d.
 
 The JSON line carries the roofline of the dominant kernel (decode: the fused
 decode kernel, the only launch of a decode forward; prefill: the contraction),
@@ -44,6 +51,7 @@ HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 INT8_PEAK_TOPS = 5000.0        # MI355X dense int8 MFMA, TOPS (5.0 POPS)
 DECODE = ("decode_m1", "decode_m8", "large_dec")
 GLU = ("glu_gate", "channel_mixer")
+MLGRU = ("mlgru_decode", "mlgru_prefill")
 ROTATE_BYTES = 1 << 30         # distinct packed weights per decode step
 
 
@@ -425,6 +433,190 @@ def bench_glu(torch, mmf, name, args):
     }, ops
 
 
+def mlgru_bytes(B, T, d):
+    """Algorithmic bytes of one MLGRU mixer call: (projection, recurrence,
+    output projection).  Projection: x (bf16), gamma, packed f|c|g weights,
+    w_scales, biases, lower bound, fcg written.  Recurrence: fcg read, state
+    read and written, o' written.  Output projection: o' read, gamma_o,
+    packed W_o, w_scale, b_o, o written."""
+    M = B * T
+    proj = M * d * 2 + 4 * d + (d // 16) * 3 * d * 4 + 12 + 4 * 3 * d + 4 * d + 4 * M * 3 * d
+    scan = 4 * M * 3 * d + 2 * 4 * B * d + 4 * M * d
+    oproj = 4 * M * d + 4 * d + (d // 16) * d * 4 + 4 + 4 * d + 4 * M * d
+    return proj, scan, oproj
+
+
+def mlgru_setup(torch, mmf, w, copies=1):
+    """Device inputs of an MLGRU workload; `copies` distinct weight sets (the
+    first the seeded one, the others drawn on the device)."""
+    import numpy as np
+    import workloads
+    dev = torch.device("cuda:0")
+    inp = workloads.make_mlgru(w)
+    T_ = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    x = torch.from_numpy(inp["x_bits"].view(np.int16)).to(dev).view(torch.bfloat16)
+    sets = []
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(240602528)
+    for i in range(copies):
+        if i == 0:
+            Wf, Wo = T_(inp["W_fcg"]), T_(inp["W_o"])
+        else:
+            Wf = torch.randn((3 * w.d, w.d), generator=gen, device=dev) * 0.02
+            Wo = torch.randn((w.d, w.d), generator=gen, device=dev) * 0.02
+        Wfp, wsf = mmf.ternarize(Wf)
+        Wop, wso = mmf.ternarize(Wo)
+        sets.append((Wfp, torch.cat([wsf, wsf, wsf]), Wop, wso))
+        del Wf, Wo
+    return {"dev": dev, "x": x, "gamma": T_(inp["gamma"]), "gamma_o": T_(inp["gamma_o"]),
+            "bias": T_(inp["bias"]), "b_o": T_(inp["b_o"]), "lb": T_(inp["lb"]),
+            "h": T_(inp["h0"]), "sets": sets}
+
+
+def bench_mlgru(torch, mmf, name, args):
+    import workloads
+    w = workloads.MLGRU_WORKLOADS[name]
+    M, d = w.M, w.d
+    pb, sb, ob = mlgru_bytes(w.B, w.T, d)
+    timer = Timer(torch)
+    if name == "mlgru_decode":
+        R = max(1, math.ceil(ROTATE_BYTES / ((d // 16) * 4 * d * 4)))
+        log(f"[bench] {name}: B={w.B} T={w.T} d={d}, {R} weight sets")
+        st = mlgru_setup(torch, mmf, w, R)
+    else:
+        R = 1
+        log(f"[bench] {name}: B={w.B} T={w.T} d={d}")
+        st = mlgru_setup(torch, mmf, w, 1)
+    dev, x, h = st["dev"], st["x"], st["h"]
+    o = torch.empty((M, d), dtype=torch.float32, device=dev)
+    wsb = torch.empty(mmf.mmf_mlgru_workspace_bytes(w.B, w.T, d), dtype=torch.uint8, device=dev)
+    fcg = torch.empty((M, 3 * d), dtype=torch.float32, device=dev)
+    op = torch.empty((M, d), dtype=torch.float32, device=dev)
+    h_out = torch.empty_like(h)
+    pws = torch.empty(mmf.mmf_mlgru_proj_workspace_bytes(M, d, d), dtype=torch.uint8, device=dev)
+    sws = torch.empty(max(1, mmf.mmf_mlgru_scan_workspace_bytes(w.B, w.T, d)), dtype=torch.uint8,
+                      device=dev)
+    sws_arg = sws if mmf.mmf_mlgru_scan_workspace_bytes(w.B, w.T, d) else None
+
+    def mixer(i):
+        Wfp, wsf, Wop, wso = st["sets"][i]
+        mmf.mmf_mlgru_fwd(x, w.B, w.T, st["gamma"], Wfp, wsf, st["bias"], st["lb"], h, h,
+                          st["gamma_o"], Wop, wso, st["b_o"], o, wsb)
+
+    def proj(i):
+        Wfp, wsf, _, _ = st["sets"][i]
+        mmf.mmf_mlgru_proj(x, st["gamma"], Wfp, wsf, st["bias"], st["lb"], fcg, pws)
+
+    def scan(i):
+        mmf.mmf_mlgru_scan(fcg, w.B, w.T, h, op, h_out, sws_arg)
+
+    def oproj(i):
+        _, _, Wop, wso = st["sets"][i]
+        mmf.mmf_bitlinear_fwd_bias(op, st["gamma_o"], Wop, wso, st["b_o"], o)
+
+    proj(0)
+    scan(0)
+    torch.cuda.synchronize()
+    stages = {}
+    if name == "mlgru_decode":
+        graphs = {}
+        for key, fn in (("mixer", mixer), ("proj", proj), ("scan", scan), ("oproj", oproj)):
+            for i in range(R):
+                fn(i)
+            torch.cuda.synchronize()
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                for i in range(R):
+                    fn(i)
+            graphs[key] = g
+        log("[bench] timing the mixer graph")
+        ms_step = timer.time(graphs["mixer"].replay, args.steps, args.warmup)
+        for key in ("proj", "scan", "oproj"):
+            stages[key] = timer.time(graphs[key].replay, args.steps, args.warmup) * 1e3 / R
+        step_bytes = pb + sb + ob
+        value = R * step_bytes / (ms_step * 1e-3) / 1e9
+        us_proj = stages["proj"]
+        achieved = pb / (us_proj * 1e-6) / 1e9
+        roof = {"bound": "hbm", "kernel": "decode_kernel with the MLGRU gate epilogue "
+                                          "(f|c|g projection + bias + sigmoid/SiLU)",
+                "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                "bytes_per_launch": pb, "avg_launch_us": us_proj}
+        res = {"value": value, "unit": "GB/s", "ms_per_step": ms_step}
+        extra = {"token_steps_per_graph": R, "us_per_token_step": ms_step * 1e3 / R,
+                 "bytes_per_token_step": step_bytes}
+    else:
+        q = torch.empty((M, d), dtype=torch.int8, device=dev)
+        a = torch.empty((M,), dtype=torch.float32, device=dev)
+        rsum = torch.empty((M,), dtype=torch.int32, device=dev)
+        mmf.mmf_act_quant(x, st["gamma"], q, a, rsum)
+        Wfp, wsf, _, _ = st["sets"][0]
+        ms_step = timer.time(lambda: mixer(0), args.steps, args.warmup)
+        ms_gemm = timer.time(lambda: mmf.mmf_mlgru_proj_q(q, a, rsum, Wfp, wsf, st["bias"],
+                                                          st["lb"], fcg), args.steps, args.warmup)
+        for key, fn in (("proj", proj), ("scan", scan), ("oproj", oproj)):
+            stages[key] = timer.time(lambda: fn(0), args.steps, args.warmup) * 1e3
+        ops_proj = 2 * M * 3 * d * d
+        gemm_tops = ops_proj / (ms_gemm * 1e-3) / 1e12
+        res = {"value": w.ops / (ms_step * 1e-3) / 1e12, "unit": "TOPS", "ms_per_step": ms_step}
+        roof = {"bound": "mfma", "kernel": "gemm_kernel with the MLGRU gate epilogue "
+                                           "(f|c|g contraction + bias + sigmoid/SiLU)",
+                "achieved": gemm_tops, "peak": INT8_PEAK_TOPS, "unit": "TFLOP/s",
+                "frac": gemm_tops / INT8_PEAK_TOPS, "traffic": None,
+                "ops_per_launch": ops_proj, "avg_launch_us": ms_gemm * 1e3}
+        extra = {"tokens_per_s": M / (ms_step * 1e-3)}
+    res["config"] = {"workload": name, "B": w.B, "T": w.T, "d": d, "x_dtype": "bf16", **extra}
+    res["roofline"] = roof
+    res["stages"] = {
+        "proj_us": stages["proj"], "scan_us": stages["scan"], "oproj_us": stages["oproj"],
+        "scan_bytes": sb, "scan_GB/s": sb / (stages["scan"] * 1e-6) / 1e9,
+        "scan_frac_hbm": sb / (stages["scan"] * 1e-6) / 1e9 / HBM_PEAK_GBS,
+        "note": "per call, each stage timed alone (decode: inside a graph of R calls)"}
+    return res, (pb + sb + ob)
+
+
+def cpu_baseline_mlgru(name, step_bytes, seconds):
+    """The oracle's whole mixer: decode, repeated token steps of the same
+    workload (GB/s with the GPU's byte count); prefill, a prefix of the
+    sequence grown until it fills a quarter of the budget (effective TOPS)."""
+    import oracle
+    import workloads
+    w = workloads.MLGRU_WORKLOADS[name]
+    inp = workloads.make_mlgru(w)
+    t, ws = oracle.weight_quant(inp["W_fcg"])
+    t_o, ws_o = oracle.weight_quant(inp["W_o"])
+
+    def run(T):
+        return oracle.mlgru_fwd(inp["x_f32"][:w.B * T], w.B, T, inp["gamma"], t, [ws] * 3,
+                                inp["bias"], inp["lb"], inp["h0"], inp["gamma_o"], t_o, ws_o,
+                                inp["b_o"])
+
+    if name == "mlgru_decode":
+        calls = 0
+        t0 = time.perf_counter()
+        while True:
+            run(1)
+            calls += 1
+            el = time.perf_counter() - t0
+            if el >= seconds:
+                break
+        return {"value": calls * step_bytes / el / 1e9, "unit": "GB/s", "cores": oracle.num_threads(),
+                "kind": "oracle",
+                "sample": f"{calls} token steps (B={w.B}, d={w.d}) in {el:.1f} s; bytes counted as "
+                          "for the GPU"}
+    T = 8
+    while True:
+        t0 = time.perf_counter()
+        run(T)
+        el = time.perf_counter() - t0
+        if el >= seconds / 4 or T >= w.T:
+            break
+        T = min(w.T, T * max(2, int(seconds / 4 / max(el, 1e-3))))
+    return {"value": 2.0 * w.B * T * 4 * w.d * w.d / el / 1e12, "unit": "TOPS",
+            "cores": oracle.num_threads(), "kind": "oracle",
+            "sample": f"the first {T} of {w.T} tokens (B={w.B}, d={w.d}) in {el:.1f} s"}
+
+
 def cpu_baseline_glu(name, seconds):
     """The oracle (two BitLinears, the gate; for channel_mixer also the down
     projection) on a sample of token rows, in effective TOPS."""
@@ -502,8 +694,10 @@ def main():
     import paper_2406_02528_amd as mmf
     import workloads
     assert torch.cuda.is_available(), "bench.py needs a HIP device"
-    w = None if args.workload in GLU else workloads.WORKLOADS[args.workload]
-    if w is None:
+    w = None if args.workload in GLU + MLGRU else workloads.WORKLOADS[args.workload]
+    if args.workload in MLGRU:
+        res, fb = bench_mlgru(torch, mmf, args.workload, args)
+    elif w is None:
         res, _ = bench_glu(torch, mmf, args.workload, args)
         fb = None
     elif w.name in DECODE:
@@ -518,7 +712,7 @@ def main():
         "data": "synthetic (seeded; shapes of the paper's model widths)",
         "config": res["config"], "roofline": res["roofline"],
     }
-    for k in ("hot_cache_call_us", "act_quant", "contraction_only", "launch_floor"):
+    for k in ("hot_cache_call_us", "act_quant", "contraction_only", "launch_floor", "stages"):
         if k in res:
             line[k] = res[k]
     if not args.no_secondary and w is not None and w.name in DECODE:
@@ -535,8 +729,12 @@ def main():
         calib_copy(torch)
     if not args.no_cpu_baseline:
         log("[bench] cpu baseline (oracle)")
-        line["cpu_baseline"] = (cpu_baseline_glu(args.workload, args.cpu_seconds) if w is None
-                                else cpu_baseline(w, fb, args.cpu_seconds))
+        if args.workload in MLGRU:
+            line["cpu_baseline"] = cpu_baseline_mlgru(args.workload, fb, args.cpu_seconds)
+        elif w is None:
+            line["cpu_baseline"] = cpu_baseline_glu(args.workload, args.cpu_seconds)
+        else:
+            line["cpu_baseline"] = cpu_baseline(w, fb, args.cpu_seconds)
     print(json.dumps(line), flush=True)
 
 

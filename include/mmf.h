@@ -180,7 +180,10 @@ int mmf_ternary_gemm_i32(const int8_t *q, const uint32_t *Wpacked,
  *   g = fp32(acc_g) * (a_scale[m] * w_scales[0])     (as y of mmf_bitlinear_fwd)
  *   u = fp32(acc_u) * (a_scale[m] * w_scales[1])
  * with acc_g, acc_u the exact ternary sums of the gate and up channel i.
- *   p[m][i] = g / (1 + expf(-g)) * u                    (fp32)
+ *   p[m][i] = (g * s) * u,  s = 1 / (1 + e^-g)           (fp32)
+ * with s from the hardware base-2 exponential and reciprocal, e^-g taken as
+ * 2^(-g log2 e) (1 ulp each; the rounded argument adds about |g| u of
+ * relative error for large |g|, u = 2^-24).
  *
  * mmf_glu_pack interleaves the packed gate and up projections, [K/16][L]
  * words each (as written by mmf_ternarize_weights for [L][K] latent
@@ -256,7 +259,9 @@ int mmf_bitlinear_fwd_bias(const void *x, int x_is_f32, const float *gamma,
 /* Input projections and gate activations: fcg [M][3d] float32 with, for
  * column n of segment s = n / d (channel i = n % d),
  *   z = fp32(acc) * (a_scale[m] * w_scales[s]) + bias[n]      (fp32)
- *   f = (1 - lb[i]) / (1 + expf(-z)) + lb[i],  c = z / (1 + expf(-z)),  g = z
+ *   f = (1 - lb[i]) * s + lb[i],  c = z * s,  g = z,   s = 1 / (1 + e^-z)
+ * with s evaluated as for the GLU gate (hardware exp2 and reciprocal). The
+ * recurrence's output gate o' = g * s(h) uses the same s.
  * x [M][K] bf16 bits or float32 (x_is_f32); bias [3d] or NULL; lb [d] or
  * NULL.  M <= 8 runs the fused decode kernel, larger M the int8 MFMA kernel. */
 size_t mmf_mlgru_proj_workspace_bytes(int64_t M, int64_t K, int64_t d);
@@ -264,6 +269,14 @@ int mmf_mlgru_proj(const void *x, int x_is_f32, const float *gamma, const uint32
                    const float *w_scales, const float *bias, const float *lb, float *fcg,
                    int64_t M, int64_t K, int64_t d, void *workspace, size_t workspace_bytes,
                    hipStream_t stream);
+
+/* The contraction stage of mmf_mlgru_proj on its own, from quantised
+ * activations (q, a_scale, q_rowsum as written by mmf_act_quant); always the
+ * int8 MFMA kernel.  Allocates nothing. */
+int mmf_mlgru_proj_q(const int8_t *q, const float *a_scale, const int32_t *q_rowsum,
+                     const uint32_t *Wfcg, const float *w_scales, const float *bias,
+                     const float *lb, float *fcg, int64_t M, int64_t K, int64_t d,
+                     hipStream_t stream);
 
 /* Recurrence and output gate from fcg [B*T][3d]: o_prime [B*T][d] float32,
  * the state after the last token in h_last [B][d] (NULL: not stored).  h0

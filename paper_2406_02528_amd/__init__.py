@@ -64,6 +64,7 @@ _SIGNATURES = {
     "mmf_mlgru_proj_workspace_bytes": ([_I64, _I64, _I64], _SZ),
     "mmf_mlgru_proj": ([_P, ctypes.c_int, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _P, _SZ, _P],
                        ctypes.c_int),
+    "mmf_mlgru_proj_q": ([_P, _P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _P], ctypes.c_int),
     "mmf_mlgru_scan_workspace_bytes": ([_I64, _I64, _I64], _SZ),
     "mmf_mlgru_scan": ([_P, _P, _P, _P, _I64, _I64, _I64, _P, _SZ, _P], ctypes.c_int),
     "mmf_mlgru_workspace_bytes": ([_I64, _I64, _I64], _SZ),
@@ -354,6 +355,27 @@ def mmf_mlgru_proj(x: torch.Tensor, gamma: torch.Tensor | None, Wfcg: torch.Tens
     wp, wn = _ws_args(workspace)
     _check(_lib.mmf_mlgru_proj(_ptr(x), int(is_f32), _ptr(gamma), _ptr(Wfcg), _ptr(w_scales),
                                _ptr(bias), _ptr(lb), _ptr(fcg), M, K, d, wp, wn, _stream(stream)))
+
+
+def mmf_mlgru_proj_q(q: torch.Tensor, a_scale: torch.Tensor, q_rowsum: torch.Tensor,
+                     Wfcg: torch.Tensor, w_scales: torch.Tensor, bias: torch.Tensor | None,
+                     lb: torch.Tensor | None, fcg: torch.Tensor, stream=None) -> None:
+    """The MLGRU projection's contraction and gates from quantised activations."""
+    M, K = q.shape
+    d = Wfcg.shape[1] // 3
+    _need(q, "q", torch.int8, (M, K))
+    _need(a_scale, "a_scale", torch.float32, (M,))
+    _need(q_rowsum, "q_rowsum", torch.int32, (M,))
+    _need(Wfcg, "Wfcg", torch.int32, (K // 16, 3 * d))
+    _need(w_scales, "w_scales", torch.float32, (3,))
+    if bias is not None:
+        _need(bias, "bias", torch.float32, (3 * d,))
+    if lb is not None:
+        _need(lb, "lb", torch.float32, (d,))
+    _need(fcg, "fcg", torch.float32, (M, 3 * d))
+    _check(_lib.mmf_mlgru_proj_q(_ptr(q), _ptr(a_scale), _ptr(q_rowsum), _ptr(Wfcg),
+                                 _ptr(w_scales), _ptr(bias), _ptr(lb), _ptr(fcg), M, K, d,
+                                 _stream(stream)))
 
 
 def mmf_mlgru_scan(fcg: torch.Tensor, B: int, T: int, h0: torch.Tensor | None,

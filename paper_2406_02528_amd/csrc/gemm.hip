@@ -347,7 +347,7 @@ __global__ __launch_bounds__((Tiling<BM, BN, WM, WN, BK, S, BX4>::kThreads)) voi
         for (int r = 0; r < 4; ++r) {
           const float gv = static_cast<float>(acc[fm][2 * pi][r] - rs) * sg;
           const float uv = static_cast<float>(acc[fm][2 * pi + 1][r] - rs) * su;
-          v[r] = __float_as_int(gv / (1.0f + expf(-gv)) * uv);
+          v[r] = __float_as_int(gv * sigmoid_hw(gv) * uv);
         }
         const uint32_t off = (row_ok && ch < L) ? row_bytes + 4u * static_cast<uint32_t>(ch) : kOut;
         __builtin_amdgcn_raw_buffer_store_b128(v, orsrc, off, 0, 0);

@@ -8,8 +8,8 @@
 // The recurrence is linear in h, so a chunk of L tokens maps the state that
 // enters it to A h + B, with A the product of its forget gates and B the
 // state it ends in from h = 0.  Long sequences therefore run as three
-// launches: (1) A and B of every chunk and channel; (2) for every channel, a
-// pass over the chunks in order that gives the state entering each one;
+// launches: (1) A and B of every chunk and channel; (2) for every channel,
+// the state entering each chunk, composed over the chunks in order;
 // (3) every chunk again from its entering state, writing o' and, in the last
 // chunk, the final state.  A sequence of at most L tokens is one launch of
 // (3) from h_0.  All work is streaming: one thread holds four adjacent
@@ -23,7 +23,7 @@ namespace {
 
 constexpr int kBlock = 256;
 constexpr int kUnroll = 8;       // tokens whose loads are in flight together
-constexpr int kCarryUnroll = 16; // chunk summaries in flight in the carry pass
+constexpr int kCarryCh = 32;     // channels per workgroup of the carry pass
 constexpr int64_t kMinChunk = 16;
 constexpr int64_t kMaxChunks = 128;
 
@@ -32,7 +32,7 @@ __device__ __forceinline__ void st4(float* p, float4 v) { *reinterpret_cast<floa
 
 // one step of the recurrence on one channel
 __device__ __forceinline__ float mlgru_step(float h, float f, float c) { return f * h + (1.0f - f) * c; }
-__device__ __forceinline__ float out_gate(float g, float h) { return g / (1.0f + expf(-h)); }
+__device__ __forceinline__ float out_gate(float g, float h) { return g * sigmoid_hw(h); }
 
 struct ChunkIdx {
   int64_t b, k, i;  // sequence, chunk, first channel (multiple of 4)
@@ -78,32 +78,70 @@ __global__ __launch_bounds__(kBlock) void mlgru_chunk_kernel(const float* __rest
   st4(Bs + o, h);
 }
 
-// (2) state entering each chunk: h <- A_k h + B_k in chunk order, one
-// thread per channel; the summaries of the next chunks are loaded together.
+// (2) state entering each chunk: h <- A_k h + B_k in chunk order.  A
+// workgroup owns kCarryCh channels of one sequence.  Its threads first copy
+// the summaries of every chunk into LDS (all loads issued before any store),
+// then each of kSegs groups composes a run of consecutive chunks into one
+// map h -> a h + b, one group joins the kSegs maps in order, and each group
+// walks its run again from the state entering it, writing the carries: the
+// chain of dependent steps is 2 nchunk / kSegs + kSegs long, not nchunk.
 __global__ __launch_bounds__(kBlock) void mlgru_carry_kernel(const float* __restrict__ A,
                                                              const float* __restrict__ Bs,
                                                              const float* __restrict__ h0, int64_t nchunk,
-                                                             int64_t d, int64_t total, float* __restrict__ carry) {
-  const int64_t idx = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
-  if (idx >= total) return;
-  const int64_t b = idx / d, i = idx % d;
-  float h = h0 != nullptr ? h0[idx] : 0.0f;
-  const int64_t base = b * nchunk * d + i;
-  for (int64_t k0 = 0; k0 < nchunk; k0 += kCarryUnroll) {
-    float av[kCarryUnroll], bv[kCarryUnroll];
+                                                             int64_t d, float* __restrict__ carry) {
+  constexpr int kSegs = kBlock / kCarryCh;
+  constexpr int kPerThread = kMaxChunks * kCarryCh / kBlock;
+  __shared__ float sa[kMaxChunks][kCarryCh];
+  __shared__ float sb[kMaxChunks][kCarryCh];
+  __shared__ float seg_a[kSegs][kCarryCh], seg_b[kSegs][kCarryCh], seg_h[kSegs][kCarryCh];
+  const int64_t nblk = (d + kCarryCh - 1) / kCarryCh;
+  const int64_t b = blockIdx.x / nblk;
+  const int64_t c0 = (blockIdx.x % nblk) * kCarryCh;
+  const int nch = static_cast<int>(nchunk);
+  const int64_t base = b * nchunk * d + c0;
+  const int c = threadIdx.x % kCarryCh, sg = threadIdx.x / kCarryCh;
+  const bool col_ok = c0 + c < d;
+  {
+    float ra[kPerThread], rb[kPerThread];
 #pragma unroll
-    for (int u = 0; u < kCarryUnroll; ++u) {
-      const int64_t k = k0 + u < nchunk ? k0 + u : nchunk - 1;
-      av[u] = A[base + k * d];
-      bv[u] = Bs[base + k * d];
+    for (int u = 0; u < kPerThread; ++u) {
+      const int k = sg + kSegs * u;  // element threadIdx.x + kBlock u
+      const bool ok = col_ok && k < nch;
+      ra[u] = ok ? A[base + k * d + c] : 1.0f;
+      rb[u] = ok ? Bs[base + k * d + c] : 0.0f;
     }
 #pragma unroll
-    for (int u = 0; u < kCarryUnroll; ++u) {
-      if (k0 + u < nchunk) {
-        carry[base + (k0 + u) * d] = h;
-        h = av[u] * h + bv[u];
-      }
+    for (int u = 0; u < kPerThread; ++u) {
+      sa[sg + kSegs * u][c] = ra[u];
+      sb[sg + kSegs * u][c] = rb[u];
     }
+  }
+  __syncthreads();
+  const int per = (nch + kSegs - 1) / kSegs;
+  const int k0 = sg * per < nch ? sg * per : nch;
+  const int k1 = k0 + per < nch ? k0 + per : nch;
+  float ca = 1.0f, cb = 0.0f;  // composed map of the run [k0, k1)
+  for (int k = k0; k < k1; ++k) {
+    ca = sa[k][c] * ca;
+    cb = sa[k][c] * cb + sb[k][c];
+  }
+  seg_a[sg][c] = ca;
+  seg_b[sg][c] = cb;
+  __syncthreads();
+  if (sg == 0) {
+    float h = (h0 != nullptr && col_ok) ? h0[b * d + c0 + c] : 0.0f;
+#pragma unroll
+    for (int s = 0; s < kSegs; ++s) {
+      seg_h[s][c] = h;
+      h = seg_a[s][c] * h + seg_b[s][c];
+    }
+  }
+  __syncthreads();
+  if (!col_ok) return;
+  float h = seg_h[sg][c];
+  for (int k = k0; k < k1; ++k) {
+    carry[base + k * d + c] = h;
+    h = sa[k][c] * h + sb[k][c];
   }
 }
 
@@ -186,8 +224,8 @@ hipError_t launch_mlgru_scan(const float* fcg, const float* h0, float* o, float*
     carry = ws + 2 * B * nchunk * d;
     hipLaunchKernelGGL(mlgru_chunk_kernel, dim3(blocks_for(total)), dim3(kBlock), 0, stream, fcg, T, d, L,
                        nchunk, total, A, Bs);
-    hipLaunchKernelGGL(mlgru_carry_kernel, dim3(blocks_for(B * d)), dim3(kBlock), 0, stream, A, Bs, h0, nchunk,
-                       d, B * d, carry);
+    hipLaunchKernelGGL(mlgru_carry_kernel, dim3(static_cast<unsigned>(B * ((d + kCarryCh - 1) / kCarryCh))),
+                       dim3(kBlock), 0, stream, A, Bs, h0, nchunk, d, carry);
   }
   hipLaunchKernelGGL(mlgru_apply_kernel, dim3(blocks_for(total)), dim3(kBlock), 0, stream, fcg, carry, h0, T, d,
                      L, nchunk, total, o, h_last);

@@ -512,6 +512,27 @@ int mmf_mlgru_proj(const void* x, int x_is_f32, const float* gamma, const uint32
   });
 }
 
+int mmf_mlgru_proj_q(const int8_t* q, const float* a_scale, const int32_t* q_rowsum,
+                     const uint32_t* Wfcg, const float* w_scales, const float* bias,
+                     const float* lb, float* fcg, int64_t M, int64_t K, int64_t d,
+                     hipStream_t stream) {
+  if (int st = check_mlgru_d(d)) return st;
+  if (int st = check_shape(M, K, 3 * d)) return st;
+  if (M == 0) return MMF_OK;
+  if (!q || !a_scale || !q_rowsum || !Wfcg || !w_scales || !fcg) return MMF_ERR_NULL;
+  if (!aligned16(q) || !aligned16(a_scale) || !aligned16(q_rowsum) || !aligned16(Wfcg) ||
+      !aligned16(fcg) || !aligned16_or_null(bias) || !aligned16_or_null(lb))
+    return MMF_ERR_ALIGN;
+  mmf::Affine aff;
+  aff.bias = bias;
+  aff.lb = lb;
+  aff.seg = d;
+  aff.acts = kMlgruActs;
+  mmf::ContractArgs a{q, a_scale, q_rowsum, Wfcg, w_scales, fcg, M, static_cast<int>(K), 3 * d,
+                      mmf::Epilogue::kAffineF32, aff};
+  return hip_status(mmf::launch_gemm(a, stream));
+}
+
 size_t mmf_mlgru_scan_workspace_bytes(int64_t B, int64_t T, int64_t d) {
   if (check_mlgru_d(d) != MMF_OK || B < 0 || T < 0) return 0;
   return scan_ws_bytes(B, T, d);

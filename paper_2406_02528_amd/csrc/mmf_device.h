@@ -149,19 +149,31 @@ __device__ __forceinline__ float bf16_to_f32(uint16_t b) {
 }
 
 // ---------------------------------------------------------------------------
+// Logistic sigmoid 1 / (1 + e^-v) from the hardware base-2 exponential and
+// reciprocal (v_exp_f32, v_rcp_f32, 1 ulp each): e^-v = 2^(-v log2 e) with
+// the argument rounded once in fp32, so the result carries a relative error
+// of about (1 - sigmoid) (|v| + 2) u + 3u (u = 2^-24).  Saturates cleanly:
+// 2^x overflows to inf for v << 0 (sigmoid 0) and underflows to 0 for
+// v >> 0 (sigmoid 1).
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float sigmoid_hw(float v) {
+  return __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(v * -1.44269504088896341f));
+}
+
+// ---------------------------------------------------------------------------
 // Affine epilogue.  z = (float)acc * (a_scale * w_scale[s]) + bias[n] in
 // fp32, one rounding per operation, then the activation of segment s:
-// identity, lb + (1 - lb) / (1 + e^-z) (sigmoid with a lower bound) or
-// z / (1 + e^-z) (SiLU).  The column factors go through buffer resources of
+// identity, (1 - lb) sigmoid(z) + lb (sigmoid with a lower bound) or
+// z sigmoid(z) (SiLU).  The column factors go through buffer resources of
 // size 0 when an array is absent, which read as 0 with no memory access.
 // ---------------------------------------------------------------------------
 constexpr int kBufferWord3 = 0x00020000;  // gfx9 buffer descriptor word 3
 
 __device__ __forceinline__ float affine_act(float z, uint32_t act, float lb) {
   if (act == kActIdentity) return z;
-  const float den = 1.0f + expf(-z);
-  if (act == kActSilu) return z / den;
-  return (1.0f - lb) / den + lb;
+  const float s = sigmoid_hw(z);
+  if (act == kActSilu) return z * s;
+  return (1.0f - lb) * s + lb;
 }
 
 struct ColAffine {

@@ -203,6 +203,10 @@ def test_mlgru_argument_checks(mmf):
     assert lib.mmf_mlgru_proj(A, 0, B, C, D, E, A, B, 4, 16, 16, W, need - 1, S) == 4
     assert lib.mmf_mlgru_proj(A, 0, B, C, D, E, A, B, 4, 16, 16, W + 16, need, S) == 4
     assert lib.mmf_mlgru_proj(None, 0, None, None, None, None, None, None, 0, 16, 16, None, 0, S) == 0
+    assert lib.mmf_mlgru_proj_q(A, B, C, D, E, A, B, C, 4, 16, 24, S) == 2
+    assert lib.mmf_mlgru_proj_q(A, B, None, D, E, A, B, C, 4, 16, 16, S) == 1
+    assert lib.mmf_mlgru_proj_q(A, B, C, D, E, BAD, B, C, 4, 16, 16, S) == 3
+    assert lib.mmf_mlgru_proj_q(None, None, None, None, None, None, None, None, 0, 16, 16, S) == 0
     # recurrence
     assert lib.mmf_mlgru_scan(A, B, C, D, 2, 3, 24, None, 0, S) == 2
     assert lib.mmf_mlgru_scan(A, B, C, D, -1, 3, 16, None, 0, S) == 2
