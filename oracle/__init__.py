@@ -30,6 +30,10 @@ wrapper names the passage of the paper it follows:
   and the forget-gate lower bound, the recurrence
   h_t = f_t h_{t-1} + (1 - f_t) c_t with the output gate o' = g sigma(h), and
   the whole mixer around its two ternary projections
+* :func:`bitlinear_train_fwd`, :func:`bitlinear_bwd` -- Algorithm 1's training
+  forward (the latent weights quantised on every call, rstd kept) and its
+  backward_pass / rms_norm_bwd with the straight-through estimator of Sec.
+  "Surrogate Gradient"
 """
 from __future__ import annotations
 
@@ -92,6 +96,8 @@ def _load():
     lib.oracle_mlgru_gates.argtypes = [P, P, P, I64, I64, P]
     lib.oracle_mlgru_scan.argtypes = [P, P, I64, I64, I64, P, P]
     lib.oracle_add_bias.argtypes = [P, P, I64, I64, P]
+    lib.oracle_bitlinear_bwd.argtypes = [P, P, P, P, P, P, P, ctypes.c_float, I64, I64, I64,
+                                         P, P, P, P, P, P]
     _lib = lib
     return lib
 
@@ -360,3 +366,48 @@ def mlgru_fwd(x: np.ndarray, B: int, T: int, gamma: np.ndarray | None, t_fcg: np
     o = out["y"] if b_o is None else add_bias(out["y"], b_o)
     return {"o": o, "h_last": h_last, "o_prime": o_prime, "fcg": pr["fcg"],
             "y_o": out["y"], "q_o": out["q"], "acc_o": out["acc"], "a_scale_o": out["a_scale"]}
+
+
+def bitlinear_train_fwd(x: np.ndarray, gamma: np.ndarray | None, W: np.ndarray,
+                        bias: np.ndarray | None = None, eps: float = EPS):
+    """Algorithm 1's forward_pass with the latent weights W [N][K]:
+    weight_quant, RMSNorm (rstd kept for the backward), activation_quant,
+    the ternary product, the bias.  Returns dict with y, t, w_scale, q,
+    a_scale, rstd, acc."""
+    t, ws = weight_quant(W)
+    out = bitlinear_fwd(x, gamma, t, ws, eps)
+    _, r = rms_norm(x, gamma, eps)
+    y = out["y"] if bias is None else add_bias(out["y"], bias)
+    return {"y": y, "t": t, "w_scale": ws, "q": out["q"], "a_scale": out["a_scale"],
+            "rstd": r, "acc": out["acc"]}
+
+
+def bitlinear_bwd(dO: np.ndarray, x: np.ndarray, gamma: np.ndarray | None, rstd: np.ndarray,
+                  q: np.ndarray, a_scale: np.ndarray, t: np.ndarray, w_scale: float):
+    """Backward of the BitLinear (Algorithm 1 backward_pass, rms_norm_bwd in the
+    RMSNorm reading, straight-through quantisers).  dO [M][N] (values of the
+    bf16 gradient), x [M][K], rstd [M] the forward's, q/a_scale the forward's
+    int8 activations, t [N][K] the forward's ternary codes.  Returns dict with
+    dx [M][K], dW [N][K], db [N], dgamma [K] (None without gamma), dY [M][K]
+    (fp64), yq [M][K] (the bf16-stored dequantised activations)."""
+    dO = _c(dO, np.float32)
+    x = _c(x, np.float32)
+    M, K = x.shape
+    N = dO.shape[1]
+    g = None if gamma is None else _c(gamma, np.float32)
+    r = _c(rstd, np.float32)
+    q = _c(q, np.int8)
+    a = _c(a_scale, np.float32)
+    t = _c(t, np.int8)
+    if dO.shape != (M, N) or t.shape != (N, K) or q.shape != (M, K):
+        raise ValueError("shape mismatch")
+    dY = np.empty((M, K), np.float64)
+    yq = np.empty((M, K), np.float32)
+    dx = np.empty((M, K), np.float32)
+    dW = np.empty((N, K), np.float32)
+    db = np.empty(N, np.float32)
+    dg = np.empty(K, np.float32) if g is not None else None
+    _load().oracle_bitlinear_bwd(_p(dO), _p(x), None if g is None else _p(g), _p(r), _p(q), _p(a),
+                                 _p(t), ctypes.c_float(w_scale), M, K, N, _p(dY), _p(yq), _p(dx),
+                                 _p(dW), _p(db), None if dg is None else _p(dg))
+    return {"dx": dx, "dW": dW, "db": db, "dgamma": dg, "dY": dY, "yq": yq}

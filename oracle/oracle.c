@@ -30,6 +30,9 @@
  *                           MLGRU equations: forget/candidate/output gate
  *                           activations, the recurrence over time and the
  *                           output gate o' = g * sigma(h); bias of a layer.
+ *   backward             -- Algorithm 1, backward_pass and rms_norm_bwd, with
+ *                           the straight-through estimator of Sec.
+ *                           "Surrogate Gradient".
  *
  * Precision.  The paper fixes none.  Where a floating-point value decides an
  * integer (the ternary code, the int8 activation) the oracle takes that
@@ -365,4 +368,84 @@ void oracle_add_bias(const float *y, const float *b, int64_t M, int64_t N, float
     for (int64_t m = 0; m < M; ++m)
         for (int64_t n = 0; n < N; ++n)
             out[m * N + n] = (float)((double)y[m * N + n] + (double)b[n]);
+}
+
+/* ---------------------------------------------------------------------- */
+/* bfloat16 storage of a float: round to nearest, ties to even, on the     */
+/* top 16 bits (the 16-bit activations the training path stores).         */
+/* ---------------------------------------------------------------------- */
+static float round_to_bf16(float v) {
+    uint32_t b;
+    memcpy(&b, &v, 4);
+    const uint32_t lsb = (b >> 16) & 1u;
+    b = (b + 0x7FFFu + lsb) & 0xFFFF0000u;
+    float out;
+    memcpy(&out, &b, 4);
+    return out;
+}
+
+/* ---------------------------------------------------------------------- */
+/* Backward of the BitLinear (Algorithm 1, backward_pass and rms_norm_bwd; */
+/* Sec. "Surrogate Gradient": the straight-through estimator passes the    */
+/* gradient through both quantisers unchanged).  In the RMSNorm reading    */
+/* (no mean subtracted, so the mean term of rms_norm_bwd vanishes) with    */
+/* the learned scale applied after the normalisation, y = (x r) gamma:     */
+/*   dY  = dO x Wt^T            Wt = t * w_scale, the forward's weights    */
+/*   g   = gamma (.) dY,  s = sum_k g_k x_k                                */
+/*   dX  = r g - (r^3 / K) x s                                             */
+/*   dW  = dO^T x Yq            Yq = q * a_scale stored as bfloat16        */
+/*   db  = sum over tokens of dO;  dgamma = sum over tokens of dY x r      */
+/* dO [M][N] holds the values of the bf16 output gradient; r [M] is the    */
+/* forward's fp32 rstd.  Sums in fp64, each output rounded to fp32 once;   */
+/* Yq is rounded to bf16 from the fp32 product q * a_scale, as stored.     */
+/* Scratch: dY double[M*K], yq float[M*K] supplied by the caller.          */
+/* ---------------------------------------------------------------------- */
+void oracle_bitlinear_bwd(const float *dO, const float *x, const float *gamma,
+                          const float *r, const int8_t *q, const float *a_scale,
+                          const int8_t *t, float w_scale, int64_t M, int64_t K,
+                          int64_t N, double *dY, float *yq, float *dx, float *dW,
+                          float *db, float *dgamma) {
+#pragma omp parallel for schedule(static)
+    for (int64_t m = 0; m < M; ++m) {
+        for (int64_t k = 0; k < K; ++k) {
+            double acc = 0.0;
+            for (int64_t n = 0; n < N; ++n)
+                acc += (double)dO[m * N + n] * (double)t[n * K + k];
+            dY[m * K + k] = acc * (double)w_scale;
+        }
+        const double rm = (double)r[m];
+        double s = 0.0;
+        for (int64_t k = 0; k < K; ++k) {
+            const double gk = gamma ? (double)gamma[k] : 1.0;
+            s += gk * dY[m * K + k] * (double)x[m * K + k];
+        }
+        for (int64_t k = 0; k < K; ++k) {
+            const double gk = gamma ? (double)gamma[k] : 1.0;
+            dx[m * K + k] = (float)(rm * gk * dY[m * K + k] -
+                                    rm * rm * rm / (double)K * (double)x[m * K + k] * s);
+            yq[m * K + k] = round_to_bf16((float)q[m * K + k] * a_scale[m]);
+        }
+    }
+#pragma omp parallel for schedule(static)
+    for (int64_t n = 0; n < N; ++n) {
+        for (int64_t k = 0; k < K; ++k) {
+            double acc = 0.0;
+            for (int64_t m = 0; m < M; ++m) acc += (double)dO[m * N + n] * (double)yq[m * K + k];
+            dW[n * K + k] = (float)acc;
+        }
+        if (db) {
+            double acc = 0.0;
+            for (int64_t m = 0; m < M; ++m) acc += (double)dO[m * N + n];
+            db[n] = (float)acc;
+        }
+    }
+    if (dgamma) {
+#pragma omp parallel for schedule(static)
+        for (int64_t k = 0; k < K; ++k) {
+            double acc = 0.0;
+            for (int64_t m = 0; m < M; ++m)
+                acc += dY[m * K + k] * (double)x[m * K + k] * (double)r[m];
+            dgamma[k] = (float)acc;
+        }
+    }
 }

@@ -547,3 +547,110 @@ def test_add_bias():
     y = np.array([[1.0, -2.0, 0.5]], np.float32)
     b = np.array([0.25, 2.0, -0.5], np.float32)
     assert oracle.add_bias(y, b).tolist() == [[1.25, 0.0, 0.0]]
+
+
+# --------------------------------------------------------------------------
+# training forward and backward (Algorithm 1, backward_pass / rms_norm_bwd;
+# straight-through quantisers, Sec. "Surrogate Gradient")
+# --------------------------------------------------------------------------
+
+def _ste_case(seed, M=3, K=24, N=10, with_gamma=True):
+    rs = np.random.default_rng(seed)
+    x = rs.standard_normal((M, K)).astype(np.float32)
+    gamma = rs.uniform(0.5, 1.5, K).astype(np.float32) if with_gamma else None
+    W = (rs.standard_normal((N, K)) * 0.02).astype(np.float32)
+    f = oracle.bitlinear_train_fwd(x, gamma, W)
+    dO = rs.standard_normal((M, N)).astype(np.float32)
+    b = oracle.bitlinear_bwd(dO, x, gamma, f["rstd"], f["q"], f["a_scale"], f["t"], f["w_scale"])
+    return x, gamma, W, f, dO, b
+
+
+def _surrogate(x, gamma, Wt, dO):
+    """The loss the straight-through estimator differentiates: the forward with
+    both quantisers replaced by the identity, sum(dO * ((x r gamma) Wt^T)),
+    in fp64 with the exact rstd."""
+    x = x.astype(np.float64)
+    r = 1.0 / np.sqrt(np.mean(x * x, axis=1, keepdims=True) + oracle.EPS)
+    y = x * r * (1.0 if gamma is None else gamma.astype(np.float64))
+    return float(np.sum(dO.astype(np.float64) * (y @ Wt.T)))
+
+
+@pytest.mark.parametrize("with_gamma", [True, False])
+def test_bwd_dx_is_the_ste_gradient(with_gamma):
+    # central differences of the surrogate loss against dx
+    x, gamma, W, f, dO, b = _ste_case(31, with_gamma=with_gamma)
+    Wt = f["t"].astype(np.float64) * float(f["w_scale"])
+    h = 1e-4
+    num = np.empty(x.shape)
+    for m in range(x.shape[0]):
+        for k in range(x.shape[1]):
+            xp, xm = x.astype(np.float64), x.astype(np.float64)
+            xp = xp.copy(); xm = xm.copy()
+            xp[m, k] += h
+            xm[m, k] -= h
+            num[m, k] = (_surrogate(xp, gamma, Wt, dO) - _surrogate(xm, gamma, Wt, dO)) / (2 * h)
+    np.testing.assert_allclose(b["dx"], num, rtol=2e-6, atol=2e-7 * np.abs(num).max())
+
+
+def test_bwd_dgamma_is_the_ste_gradient():
+    x, gamma, W, f, dO, b = _ste_case(32)
+    Wt = f["t"].astype(np.float64) * float(f["w_scale"])
+    h = 1e-4
+    num = np.empty(gamma.shape)
+    for k in range(gamma.size):
+        gp, gm = gamma.astype(np.float64).copy(), gamma.astype(np.float64).copy()
+        gp[k] += h
+        gm[k] -= h
+        num[k] = (_surrogate(x, gp, Wt, dO) - _surrogate(x, gm, Wt, dO)) / (2 * h)
+    np.testing.assert_allclose(b["dgamma"], num, rtol=2e-6, atol=2e-7 * np.abs(num).max())
+
+
+def test_bwd_dw_db_and_stored_activations():
+    import torch
+    x, gamma, W, f, dO, b = _ste_case(33, M=5, K=32, N=12)
+    # Yq: q * a_scale in fp32, stored as bfloat16 (torch's round-to-nearest-even)
+    yq = (torch.from_numpy(f["q"].astype(np.float32) * f["a_scale"][:, None])
+          .to(torch.bfloat16).to(torch.float32).numpy())
+    assert np.array_equal(b["yq"], yq)
+    # the loss is linear in the forward's weights Wt: its gradient is dO^T Yq
+    np.testing.assert_allclose(b["dW"], dO.astype(np.float64).T @ yq.astype(np.float64), rtol=1e-6, atol=1e-7)
+    np.testing.assert_allclose(b["db"], dO.astype(np.float64).sum(axis=0), rtol=1e-6, atol=1e-7)
+
+
+def test_bwd_invariant_pins_eps():
+    # sum_k x_k dx_k = eps r^3 s exactly (s = sum_k gamma_k dY_k x_k): the
+    # normalisation's gradient is orthogonal to x up to the eps term
+    x, gamma, W, f, dO, b = _ste_case(34, M=4, K=48, N=8)
+    r = f["rstd"].astype(np.float64)
+    s = np.sum(gamma.astype(np.float64) * b["dY"] * x, axis=1)
+    lhs = np.sum(x.astype(np.float64) * b["dx"], axis=1)
+    scale = np.abs(r * s) * 1e-6 + 1e-12
+    assert np.all(np.abs(lhs - oracle.EPS * r ** 3 * s) <= scale)
+    # zero output gradient: zero everywhere
+    z = oracle.bitlinear_bwd(np.zeros_like(dO), x, gamma, f["rstd"], f["q"], f["a_scale"], f["t"], f["w_scale"])
+    assert not z["dx"].any() and not z["dW"].any() and not z["db"].any() and not z["dgamma"].any()
+
+
+def test_train_fwd_rstd_and_bias():
+    rs = np.random.default_rng(35)
+    x = rs.standard_normal((4, 64)).astype(np.float32)
+    W = (rs.standard_normal((16, 64)) * 0.02).astype(np.float32)
+    b = (rs.integers(-8, 8, 16) / 8).astype(np.float32)
+    f = oracle.bitlinear_train_fwd(x, None, W, b)
+    r = 1.0 / np.sqrt(np.mean(x.astype(np.float64) ** 2, axis=1) + 1e-6)
+    np.testing.assert_allclose(f["rstd"], r, rtol=1e-7)
+    f0 = oracle.bitlinear_train_fwd(x, None, W)
+    np.testing.assert_allclose(f["y"], f0["y"].astype(np.float64) + b, rtol=1e-7, atol=1e-7)
+
+
+def test_bwd_bf16_storage_rounds_ties_to_even():
+    # q * a_scale = +-(1 + 2^-8) lies halfway between the bf16 values 1
+    # (mantissa even) and 1 + 2^-7 (odd): ties to even give 1
+    a = np.array([1 + 2.0 ** -8, 1 + 2.0 ** -7 + 2.0 ** -8], np.float32)
+    q = np.array([[1, -1], [1, -1]], np.int8)
+    K, N = 2, 1
+    b = oracle.bitlinear_bwd(np.zeros((2, N), np.float32), np.ones((2, K), np.float32), None,
+                             np.ones(2, np.float32), q, a, np.zeros((N, K), np.int8), 1.0)
+    assert b["yq"][0].tolist() == [1.0, -1.0]
+    # 1 + 3 * 2^-8 = 1 + 1.5 * 2^-7: between mantissas 1 (odd) and 2 (even)
+    assert b["yq"][1].tolist() == [1.015625, -1.015625]
