@@ -301,6 +301,52 @@ int mmf_mlgru_fwd(const void *x, int x_is_f32, const float *gamma, const uint32_
                   int64_t d, void *workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * Training forward (Algorithm 1, forward_pass: the latent weights are
+ * quantised on every call; the RMSNorm statistic r is kept for the
+ * backward).  From latent float32 weights W [N][K]:
+ *   Wpacked [K/16][N], w_scale [1]   as mmf_ternarize_weights(W)
+ *   q [M][K], a_scale [M], rstd [M]  as mmf_act_quant(x), rstd[m] =
+ *                                    1/sqrt(mean_k x^2 + 1e-6) (float32)
+ *   y [M][N]                         as mmf_bitlinear_fwd(_bias) with them
+ * (bias [N] or NULL; with a bias N must be a multiple of 4).  rstd may be
+ * NULL.  Every M runs the int8 MFMA kernel; K/16 * N * 4 must stay below
+ * 2^31 and N at most 2^24 (MMF_ERR_SHAPE).  Wpacked, w_scale, q, a_scale
+ * and rstd are what mmf_bitlinear_bwd takes.  Workspace as for the MLGRU
+ * entry points (NULL: allocated stream-ordered).
+ */
+size_t mmf_bitlinear_train_workspace_bytes(int64_t M, int64_t K, int64_t N);
+int mmf_bitlinear_train_fwd(const void *x, int x_is_f32, const float *gamma, const float *W,
+                            const float *bias, float *y, uint32_t *Wpacked, float *w_scale,
+                            int8_t *q, float *a_scale, float *rstd, int64_t M, int64_t K,
+                            int64_t N, void *workspace, size_t workspace_bytes,
+                            hipStream_t stream);
+
+/*
+ * Backward of the BitLinear (Algorithm 1, backward_pass and rms_norm_bwd;
+ * the straight-through estimator of Sec. "Surrogate Gradient" passes the
+ * gradient through both quantisers unchanged), in the RMSNorm reading
+ * (no mean subtracted) with y = (x r) gamma:
+ *   dY = dO Wt^T,  Wt = t * w_scale (the ternary weights the forward used)
+ *   dx = r g - (r^3 / K) x s,  g = gamma (.) dY,  s = sum_k g_k x_k
+ *   dW = dO^T Yq,  Yq = q * a_scale stored as bfloat16 (the gradient of the
+ *        latent weights through the straight-through weight quantiser)
+ *   db = sum over tokens of dO;  dgamma = sum over tokens of dY (.) x r
+ * dO [M][N] bfloat16 bits; x [M][K] bf16 bits or float32 (x_is_f32); gamma
+ * [K] or NULL (ones); rstd, q, a_scale, Wpacked, w_scale from
+ * mmf_bitlinear_train_fwd.  Outputs float32: dx [M][K], dW [N][K], db [N]
+ * (NULL: not computed), dgamma [K] (NULL: not computed).  The two products
+ * are bf16 GEMMs with fp32 accumulation on the matrix cores (rocBLAS); s, db
+ * and dgamma are summed in fp64.  M at most 65535 * 64 (MMF_ERR_SHAPE).
+ * M == 0 or N == 0 is a no-op.  Workspace as above.
+ */
+size_t mmf_bitlinear_bwd_workspace_bytes(int64_t M, int64_t K, int64_t N);
+int mmf_bitlinear_bwd(const uint16_t *dO, const void *x, int x_is_f32, const float *gamma,
+                      const float *rstd, const int8_t *q, const float *a_scale,
+                      const uint32_t *Wpacked, const float *w_scale, float *dx, float *dW,
+                      float *db, float *dgamma, int64_t M, int64_t K, int64_t N,
+                      void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
  * Kernel selection for the contraction: MMF_PATH_AUTO (decode kernel for
  * M <= 8, MFMA kernel otherwise), MMF_PATH_GEMV or MMF_PATH_GEMM force one
  * kernel for every M (the decode kernel handles at most 8 tokens per launch

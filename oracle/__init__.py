@@ -388,8 +388,8 @@ def bitlinear_bwd(dO: np.ndarray, x: np.ndarray, gamma: np.ndarray | None, rstd:
     RMSNorm reading, straight-through quantisers).  dO [M][N] (values of the
     bf16 gradient), x [M][K], rstd [M] the forward's, q/a_scale the forward's
     int8 activations, t [N][K] the forward's ternary codes.  Returns dict with
-    dx [M][K], dW [N][K], db [N], dgamma [K] (None without gamma), dY [M][K]
-    (fp64), yq [M][K] (the bf16-stored dequantised activations)."""
+    dx [M][K], dW [N][K], db [N], dgamma [K] (at gamma = 1 without gamma),
+    dY [M][K] (fp64), yq [M][K] (the bf16-stored dequantised activations)."""
     dO = _c(dO, np.float32)
     x = _c(x, np.float32)
     M, K = x.shape
@@ -406,8 +406,8 @@ def bitlinear_bwd(dO: np.ndarray, x: np.ndarray, gamma: np.ndarray | None, rstd:
     dx = np.empty((M, K), np.float32)
     dW = np.empty((N, K), np.float32)
     db = np.empty(N, np.float32)
-    dg = np.empty(K, np.float32) if g is not None else None
+    dg = np.empty(K, np.float32)
     _load().oracle_bitlinear_bwd(_p(dO), _p(x), None if g is None else _p(g), _p(r), _p(q), _p(a),
                                  _p(t), ctypes.c_float(w_scale), M, K, N, _p(dY), _p(yq), _p(dx),
-                                 _p(dW), _p(db), None if dg is None else _p(dg))
+                                 _p(dW), _p(db), _p(dg))
     return {"dx": dx, "dW": dW, "db": db, "dgamma": dg, "dY": dY, "yq": yq}

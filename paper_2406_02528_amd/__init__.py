@@ -8,8 +8,9 @@ module only checks tensor shapes, dtypes and devices and passes raw pointers
 and the current HIP stream through the C ABI declared in ``include/mmf.h``.
 PyTorch is used for device memory and streams only.
 
-Also the GLU channel mixer's gated up-projection and the MLGRU token mixer
-(input projections with gate activations, the recurrence, the whole mixer).
+Also the GLU channel mixer's gated up-projection, the MLGRU token mixer
+(input projections with gate activations, the recurrence, the whole mixer),
+and the training forward and backward of the layer.
 
 Functions carry the names of the C entry points.  There is no fallback: if
 the library is not built, importing this package raises ``ImportError``.
@@ -68,6 +69,12 @@ _SIGNATURES = {
     "mmf_mlgru_scan_workspace_bytes": ([_I64, _I64, _I64], _SZ),
     "mmf_mlgru_scan": ([_P, _P, _P, _P, _I64, _I64, _I64, _P, _SZ, _P], ctypes.c_int),
     "mmf_mlgru_workspace_bytes": ([_I64, _I64, _I64], _SZ),
+    "mmf_bitlinear_train_workspace_bytes": ([_I64, _I64, _I64], _SZ),
+    "mmf_bitlinear_train_fwd": ([_P, ctypes.c_int, _P, _P, _P, _P, _P, _P, _P, _P, _P, _I64, _I64,
+                                 _I64, _P, _SZ, _P], ctypes.c_int),
+    "mmf_bitlinear_bwd_workspace_bytes": ([_I64, _I64, _I64], _SZ),
+    "mmf_bitlinear_bwd": ([_P, _P, ctypes.c_int, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _I64, _I64,
+                           _I64, _P, _SZ, _P], ctypes.c_int),
     "mmf_mlgru_fwd": ([_P, ctypes.c_int, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P,
                        _I64, _I64, _I64, _P, _SZ, _P], ctypes.c_int),
 }
@@ -420,6 +427,74 @@ def mmf_mlgru_fwd(x: torch.Tensor, B: int, T: int, gamma: torch.Tensor | None,
                               _ptr(bias), _ptr(lb), _ptr(h0), _ptr(h_last), _ptr(gamma_o),
                               _ptr(Wo), _ptr(w_scale_o), _ptr(b_o), _ptr(o), B, T, d, wp, wn,
                               _stream(stream)))
+
+
+def mmf_bitlinear_train_workspace_bytes(M: int, K: int, N: int) -> int:
+    return int(_lib.mmf_bitlinear_train_workspace_bytes(M, K, N))
+
+
+def mmf_bitlinear_bwd_workspace_bytes(M: int, K: int, N: int) -> int:
+    return int(_lib.mmf_bitlinear_bwd_workspace_bytes(M, K, N))
+
+
+def mmf_bitlinear_train_fwd(x: torch.Tensor, gamma: torch.Tensor | None, W: torch.Tensor,
+                            bias: torch.Tensor | None, y: torch.Tensor, Wpacked: torch.Tensor,
+                            w_scale: torch.Tensor, q: torch.Tensor, a_scale: torch.Tensor,
+                            rstd: torch.Tensor | None, workspace: torch.Tensor | None = None,
+                            stream=None) -> None:
+    """Training forward from latent float32 weights W [N][K]: y [M][N] and the
+    state the backward needs (Wpacked, w_scale, q, a_scale, rstd)."""
+    M, K = x.shape
+    N = W.shape[0]
+    is_f32 = _x_kind(x)
+    _need(x, "x", x.dtype, (M, K))
+    if gamma is not None:
+        _need(gamma, "gamma", torch.float32, (K,))
+    _need(W, "W", torch.float32, (N, K))
+    if bias is not None:
+        _need(bias, "bias", torch.float32, (N,))
+    _need(y, "y", torch.float32, (M, N))
+    _need(Wpacked, "Wpacked", torch.int32, (K // 16, N))
+    _need(w_scale, "w_scale", torch.float32, (1,))
+    _need(q, "q", torch.int8, (M, K))
+    _need(a_scale, "a_scale", torch.float32, (M,))
+    if rstd is not None:
+        _need(rstd, "rstd", torch.float32, (M,))
+    wp, wn = _ws_args(workspace)
+    _check(_lib.mmf_bitlinear_train_fwd(_ptr(x), int(is_f32), _ptr(gamma), _ptr(W), _ptr(bias), _ptr(y),
+                                        _ptr(Wpacked), _ptr(w_scale), _ptr(q), _ptr(a_scale), _ptr(rstd),
+                                        M, K, N, wp, wn, _stream(stream)))
+
+
+def mmf_bitlinear_bwd(dO: torch.Tensor, x: torch.Tensor, gamma: torch.Tensor | None,
+                      rstd: torch.Tensor, q: torch.Tensor, a_scale: torch.Tensor,
+                      Wpacked: torch.Tensor, w_scale: torch.Tensor, dx: torch.Tensor,
+                      dW: torch.Tensor, db: torch.Tensor | None, dgamma: torch.Tensor | None,
+                      workspace: torch.Tensor | None = None, stream=None) -> None:
+    """Backward: dx [M][K], dW [N][K], db [N], dgamma [K] (float32) from dO
+    bf16 [M][N] and the training forward's saved state."""
+    M, K = x.shape
+    N = dO.shape[1]
+    is_f32 = _x_kind(x)
+    _need(dO, "dO", torch.bfloat16, (M, N))
+    _need(x, "x", x.dtype, (M, K))
+    if gamma is not None:
+        _need(gamma, "gamma", torch.float32, (K,))
+    _need(rstd, "rstd", torch.float32, (M,))
+    _need(q, "q", torch.int8, (M, K))
+    _need(a_scale, "a_scale", torch.float32, (M,))
+    _need(Wpacked, "Wpacked", torch.int32, (K // 16, N))
+    _need(w_scale, "w_scale", torch.float32, (1,))
+    _need(dx, "dx", torch.float32, (M, K))
+    _need(dW, "dW", torch.float32, (N, K))
+    if db is not None:
+        _need(db, "db", torch.float32, (N,))
+    if dgamma is not None:
+        _need(dgamma, "dgamma", torch.float32, (K,))
+    wp, wn = _ws_args(workspace)
+    _check(_lib.mmf_bitlinear_bwd(_ptr(dO), _ptr(x), int(is_f32), _ptr(gamma), _ptr(rstd), _ptr(q),
+                                  _ptr(a_scale), _ptr(Wpacked), _ptr(w_scale), _ptr(dx), _ptr(dW),
+                                  _ptr(db), _ptr(dgamma), M, K, N, wp, wn, _stream(stream)))
 
 
 # ---------------------------------------------------------------------------

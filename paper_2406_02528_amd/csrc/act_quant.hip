@@ -1,6 +1,6 @@
 // Fused RMSNorm + per-token absmax int8 quantisation (Algorithm 1,
 // rms_norm_fwd + activation_quant; RMSNorm with the mean of squares and
-// eps = 1e-6, learned scale gamma).  One wave64 per token row; the row is read
+// eps = 1e-6, learned scale gamma), optionally keeping rstd for the backward.  One wave64 per token row; the row is read
 // from HBM once and kept in registers while the two row statistics (sum of
 // squares, then absmax of the normalised values) are reduced across the wave.
 #include "mmf_device.h"
@@ -63,7 +63,7 @@ template <typename XT, int VPL>
 __global__ __launch_bounds__(256) void act_quant_kernel(
     const XT* __restrict__ x, const float* __restrict__ gamma,
     int8_t* __restrict__ q, float* __restrict__ a_scale,
-    int32_t* __restrict__ q_rowsum, int64_t M, int K) {
+    int32_t* __restrict__ q_rowsum, float* __restrict__ rstd, int64_t M, int K) {
   using V = Vec<XT>;
   constexpr int E = V::kElems;
   const int lane = threadIdx.x & 63;
@@ -132,6 +132,7 @@ __global__ __launch_bounds__(256) void act_quant_kernel(
     if (lane == 0) {
       a_scale[row] = amax / 127.0f;
       if (q_rowsum != nullptr) q_rowsum[row] = rs;
+      if (rstd != nullptr) rstd[row] = r;
     }
   } else {
     // pass 1: sum of squares
@@ -177,13 +178,14 @@ __global__ __launch_bounds__(256) void act_quant_kernel(
     if (lane == 0) {
       a_scale[row] = amax / 127.0f;
       if (q_rowsum != nullptr) q_rowsum[row] = rs;
+      if (rstd != nullptr) rstd[row] = r;
     }
   }
 }
 
 template <typename XT>
 hipError_t launch_typed(const XT* x, const float* gamma, int8_t* q, float* a_scale,
-                        int32_t* q_rowsum, int64_t M, int K, hipStream_t stream) {
+                        int32_t* q_rowsum, float* rstd, int64_t M, int K, hipStream_t stream) {
   constexpr int E = Vec<XT>::kElems;
   const int nvec = K / E;
   const int vpl = (nvec + kWave - 1) / kWave;
@@ -191,7 +193,7 @@ hipError_t launch_typed(const XT* x, const float* gamma, int8_t* q, float* a_sca
   const dim3 block(kWave * kRowsPerBlock);
 #define MMF_AQ_LAUNCH(V)                                                          \
   hipLaunchKernelGGL((act_quant_kernel<XT, V>), grid, block, 0, stream, x, gamma, \
-                     q, a_scale, q_rowsum, M, K)
+                     q, a_scale, q_rowsum, rstd, M, K)
   if (vpl <= 1) MMF_AQ_LAUNCH(1);
   else if (vpl <= 2) MMF_AQ_LAUNCH(2);
   else if (vpl <= 4) MMF_AQ_LAUNCH(4);
@@ -206,11 +208,11 @@ hipError_t launch_typed(const XT* x, const float* gamma, int8_t* q, float* a_sca
 
 hipError_t launch_act_quant(const void* x, bool x_is_f32, const float* gamma, int8_t* q,
                             float* a_scale, int32_t* q_rowsum, int64_t M, int K,
-                            hipStream_t stream) {
+                            hipStream_t stream, float* rstd) {
   if (M == 0) return hipSuccess;
   if (x_is_f32)
-    return launch_typed(static_cast<const float*>(x), gamma, q, a_scale, q_rowsum, M, K, stream);
-  return launch_typed(static_cast<const uint16_t*>(x), gamma, q, a_scale, q_rowsum, M, K, stream);
+    return launch_typed(static_cast<const float*>(x), gamma, q, a_scale, q_rowsum, rstd, M, K, stream);
+  return launch_typed(static_cast<const uint16_t*>(x), gamma, q, a_scale, q_rowsum, rstd, M, K, stream);
 }
 
 }  // namespace mmf

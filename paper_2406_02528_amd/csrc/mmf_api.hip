@@ -302,6 +302,41 @@ MlgruScratch mlgru_scratch(int64_t B, int64_t T, int64_t d) {
   return s;
 }
 
+// ---- training forward and backward ----
+
+// A launch of the MFMA kernel needs packed weights and rows of output within
+// 32-bit offsets.
+bool gemm_shape_ok(int64_t K, int64_t N) {
+  return (K / 16) * N * 4 < (int64_t(1) << 31) && N <= (int64_t(1) << 24);
+}
+
+struct TrainScratch {
+  size_t part_off, rs_off, total;
+};
+TrainScratch train_scratch(int64_t M, int64_t K, int64_t N) {
+  TrainScratch s;
+  s.part_off = 0;
+  s.rs_off = round_up(sizeof(double) * static_cast<size_t>(mmf::ternarize_partials_count(N * K)), kScratchAlign);
+  s.total = s.rs_off + round_up(static_cast<size_t>(M) * 4, kScratchAlign);
+  return s;
+}
+
+struct BwdScratch {
+  size_t t_off, yq_off, dy_off, part_off, total;
+};
+BwdScratch bwd_scratch(int64_t M, int64_t K, int64_t N) {
+  BwdScratch s;
+  s.t_off = 0;
+  s.yq_off = round_up(static_cast<size_t>(K) * static_cast<size_t>(N) * 2, kScratchAlign);
+  s.dy_off = s.yq_off + round_up(static_cast<size_t>(M) * static_cast<size_t>(K) * 2, kScratchAlign);
+  s.part_off = s.dy_off + round_up(static_cast<size_t>(M) * static_cast<size_t>(K) * 4, kScratchAlign);
+  const int64_t cols = N > K ? N : K;
+  s.total = s.part_off + round_up(sizeof(double) * static_cast<size_t>(mmf::col_sum_partials(M) * cols),
+                                  kScratchAlign);
+  return s;
+}
+constexpr int64_t kMaxBwdRows = int64_t(65535) * 64;  // column sums: 64 rows per partial
+
 }  // namespace
 
 extern "C" {
@@ -590,6 +625,83 @@ int mmf_mlgru_fwd(const void* x, int x_is_f32, const float* gamma, const uint32_
     out.seg = d;
     out.acts = mmf::kActIdentity;
     return run_affine(op, true, gamma_o, Wo, w_scale_o, out, o, M, d, d, scratch + s.q_off, stream);
+  });
+}
+
+size_t mmf_bitlinear_train_workspace_bytes(int64_t M, int64_t K, int64_t N) {
+  if (check_shape(M, K, N) != MMF_OK) return 0;
+  return train_scratch(M, K, N).total;
+}
+
+int mmf_bitlinear_train_fwd(const void* x, int x_is_f32, const float* gamma, const float* W,
+                            const float* bias, float* y, uint32_t* Wpacked, float* w_scale, int8_t* q,
+                            float* a_scale, float* rstd, int64_t M, int64_t K, int64_t N, void* workspace,
+                            size_t workspace_bytes, hipStream_t stream) {
+  if (x_is_f32 != 0 && x_is_f32 != 1) return MMF_ERR_ARG;
+  if (int st = check_shape(M, K, N)) return st;
+  if (!gemm_shape_ok(K, N) || (bias && N % 4 != 0)) return MMF_ERR_SHAPE;
+  if (M == 0 || N == 0) return MMF_OK;
+  if (!x || !W || !y || !Wpacked || !w_scale || !q || !a_scale) return MMF_ERR_NULL;
+  if (!aligned16(x) || !aligned16(W) || !aligned16(y) || !aligned16(Wpacked) || !aligned16(q) ||
+      !aligned16(a_scale) || !aligned16_or_null(gamma) || !aligned16_or_null(bias) || !aligned16_or_null(rstd))
+    return MMF_ERR_ALIGN;
+  const TrainScratch s = train_scratch(M, K, N);
+  return with_workspace(workspace, workspace_bytes, s.total, stream, [&](char* scratch) {
+    int32_t* rowsum = reinterpret_cast<int32_t*>(scratch + s.rs_off);
+    if (mmf::launch_ternarize(W, N, static_cast<int>(K), Wpacked, w_scale,
+                              reinterpret_cast<double*>(scratch + s.part_off), stream) != hipSuccess)
+      return MMF_ERR_HIP;
+    if (mmf::launch_act_quant(x, x_is_f32 == 1, gamma, q, a_scale, rowsum, M, static_cast<int>(K), stream,
+                              rstd) != hipSuccess)
+      return MMF_ERR_HIP;
+    mmf::Affine aff;
+    aff.bias = bias;
+    aff.seg = N;
+    aff.acts = mmf::kActIdentity;
+    mmf::ContractArgs a{q, a_scale, rowsum, Wpacked, w_scale, y, M, static_cast<int>(K), N,
+                        bias ? mmf::Epilogue::kAffineF32 : mmf::Epilogue::kDequantF32, aff};
+    return hip_status(mmf::launch_gemm(a, stream));
+  });
+}
+
+size_t mmf_bitlinear_bwd_workspace_bytes(int64_t M, int64_t K, int64_t N) {
+  if (check_shape(M, K, N) != MMF_OK) return 0;
+  return bwd_scratch(M, K, N).total;
+}
+
+int mmf_bitlinear_bwd(const uint16_t* dO, const void* x, int x_is_f32, const float* gamma,
+                      const float* rstd, const int8_t* q, const float* a_scale, const uint32_t* Wpacked,
+                      const float* w_scale, float* dx, float* dW, float* db, float* dgamma, int64_t M,
+                      int64_t K, int64_t N, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  if (x_is_f32 != 0 && x_is_f32 != 1) return MMF_ERR_ARG;
+  if (int st = check_shape(M, K, N)) return st;
+  if (M > kMaxBwdRows) return MMF_ERR_SHAPE;
+  if (M == 0 || N == 0) return MMF_OK;
+  if (!dO || !x || !rstd || !q || !a_scale || !Wpacked || !w_scale || !dx || !dW) return MMF_ERR_NULL;
+  if (!aligned16(dO) || !aligned16(x) || !aligned16(rstd) || !aligned16(q) || !aligned16(a_scale) ||
+      !aligned16(Wpacked) || !aligned16(dx) || !aligned16(dW) || !aligned16_or_null(gamma) ||
+      !aligned16_or_null(db) || !aligned16_or_null(dgamma))
+    return MMF_ERR_ALIGN;
+  const BwdScratch s = bwd_scratch(M, K, N);
+  return with_workspace(workspace, workspace_bytes, s.total, stream, [&](char* scratch) {
+    uint16_t* T = reinterpret_cast<uint16_t*>(scratch + s.t_off);
+    uint16_t* yq = reinterpret_cast<uint16_t*>(scratch + s.yq_off);
+    float* dYs = reinterpret_cast<float*>(scratch + s.dy_off);
+    double* parts = reinterpret_cast<double*>(scratch + s.part_off);
+    const int Ki = static_cast<int>(K);
+    // dY (before the weight scale) = dO T^T with T the forward's codes as bf16
+    if (mmf::launch_expand_ternary(Wpacked, Ki, N, T, stream) != hipSuccess) return MMF_ERR_HIP;
+    if (mmf::gemm_bf16(false, true, M, K, N, dO, N, T, N, dYs, K, stream) != hipSuccess) return MMF_ERR_HIP;
+    if (mmf::launch_rms_norm_bwd(dYs, w_scale, x, x_is_f32 == 1, gamma, rstd, M, Ki, dx, stream) != hipSuccess)
+      return MMF_ERR_HIP;
+    // dW = dO^T Yq
+    if (mmf::launch_dequant_bf16(q, a_scale, M, Ki, yq, stream) != hipSuccess) return MMF_ERR_HIP;
+    if (mmf::gemm_bf16(true, false, N, K, M, dO, N, yq, K, dW, K, stream) != hipSuccess) return MMF_ERR_HIP;
+    if (db && mmf::launch_col_sum_bf16(dO, M, N, parts, db, stream) != hipSuccess) return MMF_ERR_HIP;
+    if (dgamma && mmf::launch_dgamma(dYs, w_scale, x, x_is_f32 == 1, rstd, M, Ki, parts, dgamma, stream) !=
+                      hipSuccess)
+      return MMF_ERR_HIP;
+    return MMF_OK;
   });
 }
 

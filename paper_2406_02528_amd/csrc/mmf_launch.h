@@ -6,10 +6,11 @@
 
 namespace mmf {
 
-// RMSNorm + absmax int8 quantisation of M rows of K features (K % 16 == 0).
+// RMSNorm + absmax int8 quantisation of M rows of K features (K % 16 == 0);
+// rstd (optional) receives each row's 1/sqrt(mean x^2 + eps).
 hipError_t launch_act_quant(const void* x, bool x_is_f32, const float* gamma, int8_t* q,
                             float* a_scale, int32_t* q_rowsum, int64_t M, int K,
-                            hipStream_t stream);
+                            hipStream_t stream, float* rstd = nullptr);
 
 // q_rowsum[m] = sum_k q[m][k].
 hipError_t launch_row_sum(const int8_t* q, int32_t* q_rowsum, int64_t M, int K,
@@ -97,6 +98,33 @@ int64_t mlgru_chunk_len(int64_t B, int64_t T, int64_t d);
 int64_t mlgru_scan_ws_floats(int64_t B, int64_t T, int64_t d);
 hipError_t launch_mlgru_scan(const float* fcg, const float* h0, float* o, float* h_last, int64_t B,
                              int64_t T, int64_t d, float* ws, hipStream_t stream);
+
+// ---- backward (bwd.hip) ----
+// T [K][N] bf16 = the ternary codes of Wpacked [K/16][N] as -1, 0, +1.
+hipError_t launch_expand_ternary(const uint32_t* Wpacked, int K, int64_t N, uint16_t* T,
+                                 hipStream_t stream);
+// yq [M][K] bf16 = q * a_scale[m] (fp32 product, rounded to nearest even).
+hipError_t launch_dequant_bf16(const int8_t* q, const float* a_scale, int64_t M, int K, uint16_t* yq,
+                               hipStream_t stream);
+// RMSNorm backward per row: dY = w_scale * dYs, g = gamma dY,
+// s = sum g x (fp64), dx = r g - (r^3 s / K) x.
+hipError_t launch_rms_norm_bwd(const float* dYs, const float* w_scale, const void* x, bool x_is_f32,
+                               const float* gamma, const float* rstd, int64_t M, int K, float* dx,
+                               hipStream_t stream);
+// Column sums over M rows, in fp64, in a fixed order: db[n] = sum_m dO[m][n]
+// (dO bf16 [M][N]) and dgamma[k] = sum_m (w_scale dYs[m][k]) x[m][k] r[m].
+// `partials` holds col_sum_partials(M) * cols doubles.
+int64_t col_sum_partials(int64_t M);
+hipError_t launch_col_sum_bf16(const uint16_t* dO, int64_t M, int64_t N, double* partials, float* db,
+                               hipStream_t stream);
+hipError_t launch_dgamma(const float* dYs, const float* w_scale, const void* x, bool x_is_f32,
+                         const float* rstd, int64_t M, int K, double* partials, float* dgamma,
+                         hipStream_t stream);
+// Dense bf16 x bf16 -> fp32 products on the matrix cores through rocBLAS,
+// row-major operands:  C[Mr][Nc] = A[Mr][Kc] * B[Kc][Nc] (transB: B given as
+// [Nc][Kc]); (transA: A given as [Kc][Mr]).
+hipError_t gemm_bf16(bool transA, bool transB, int64_t Mr, int64_t Nc, int64_t Kc, const uint16_t* A,
+                     int64_t lda, const uint16_t* B, int64_t ldb, float* C, int64_t ldc, hipStream_t stream);
 
 hipError_t launch_glu_pack(const uint32_t* Wg, const uint32_t* Wu, int64_t L, int K, uint32_t* Wgu,
                            hipStream_t stream);

@@ -237,3 +237,35 @@ def test_mlgru_argument_checks(mmf):
     assert lib.mmf_mlgru_fwd(None, 0, None, None, None, None, None, None, None, None, None, None,
                              None, None, 0, 2, 32, None, 0, S) == 0
     assert mmf.mmf_mlgru_workspace_bytes(1, 2048, 2048) >= 2048 * 2048 * 16
+
+
+def test_train_and_bwd_argument_checks(mmf):
+    lib = _c(mmf)
+    W = 0x100000
+    # training forward: shape, GEMM limits, bias needs N % 4 == 0
+    assert lib.mmf_bitlinear_train_fwd(A, 0, B, C, D, E, A, B, C, D, E, 4, 24, 8, None, 0, S) == 2
+    assert lib.mmf_bitlinear_train_fwd(A, 0, B, C, D, E, A, B, C, D, E, 4, 16, 2 ** 24 + 4, None, 0, S) == 2
+    assert lib.mmf_bitlinear_train_fwd(A, 0, B, C, D, E, A, B, C, D, E, 4, 16, 6, None, 0, S) == 2
+    assert lib.mmf_bitlinear_train_fwd(A, 0, B, None, None, E, A, B, C, D, E, 4, 16, 6, None, 0, S) == 1
+    assert lib.mmf_bitlinear_train_fwd(A, 0, B, None, None, E, A, B, C, D, E, 4, 16, 8, None, 0, S) == 1
+    assert lib.mmf_bitlinear_train_fwd(A, 0, B, C, None, E, A, B, None, D, E, 4, 16, 8, None, 0, S) == 1
+    assert lib.mmf_bitlinear_train_fwd(A, 0, B, C, None, E, A, B, C, D, BAD, 4, 16, 8, None, 0, S) == 3
+    assert lib.mmf_bitlinear_train_fwd(A, 7, B, C, None, E, A, B, C, D, E, 4, 16, 8, None, 0, S) == 6
+    need = mmf.mmf_bitlinear_train_workspace_bytes(4, 16, 8)
+    assert need > 0 and need % 256 == 0
+    assert lib.mmf_bitlinear_train_fwd(A, 0, B, C, None, E, A, B, C, D, E, 4, 16, 8, W, need - 1, S) == 4
+    assert lib.mmf_bitlinear_train_fwd(None, 0, None, None, None, None, None, None, None, None, None,
+                                       0, 16, 8, None, 0, S) == 0
+    # backward
+    assert lib.mmf_bitlinear_bwd(A, B, 0, C, D, E, A, B, C, D, E, A, B, 4, 24, 8, None, 0, S) == 2
+    assert lib.mmf_bitlinear_bwd(A, B, 0, C, D, E, A, B, C, D, E, A, B, 65535 * 64 + 1, 16, 8, None, 0, S) == 2
+    assert lib.mmf_bitlinear_bwd(None, B, 0, C, D, E, A, B, C, D, E, A, B, 4, 16, 8, None, 0, S) == 1
+    assert lib.mmf_bitlinear_bwd(A, B, 0, C, None, E, A, B, C, D, E, A, B, 4, 16, 8, None, 0, S) == 1
+    assert lib.mmf_bitlinear_bwd(A, B, 0, C, D, E, A, B, C, D, None, A, B, 4, 16, 8, None, 0, S) == 1
+    assert lib.mmf_bitlinear_bwd(A, B, 0, C, D, E, A, B, C, D, E, BAD, B, 4, 16, 8, None, 0, S) == 3
+    assert lib.mmf_bitlinear_bwd(A, B, 2, C, D, E, A, B, C, D, E, A, B, 4, 16, 8, None, 0, S) == 6
+    need = mmf.mmf_bitlinear_bwd_workspace_bytes(4, 16, 8)
+    assert need >= 16 * 8 * 2 + 4 * 16 * 6 and need % 256 == 0
+    assert lib.mmf_bitlinear_bwd(A, B, 0, C, D, E, A, B, C, D, E, A, B, 4, 16, 8, W, need - 1, S) == 4
+    assert lib.mmf_bitlinear_bwd(None, None, 0, None, None, None, None, None, None, None, None, None,
+                                 None, 0, 16, 8, None, 0, S) == 0

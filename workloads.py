@@ -25,6 +25,11 @@ projection W_o is [2048][2048] N(0, 0.02); biases U(-0.5, 0.5); the
 forget-gate lower bound U(0, 0.95) per channel (a deep layer's); the
 initial state N(0, 1) x 0.5 (a running sequence).
 
+Training workloads (``TRAIN_WORKLOADS``): the paper's training-efficiency
+setting (input size and sequence length 1024; 16 sequences, M = 16384,
+K = N = 1024) and the 1.3B model's GLU up-projection over 8192 tokens, each
+with a bf16 output gradient dO ~ N(0, 1) [M][N].
+
 Latent weights are N(0, 0.02) float32 of shape [N][K] (out x in).  RMSNorm
 scales are U(0.5, 1.5) except for ``tiny`` (all ones).  The seed of workload i
 and stream j is 240602528 + 10 i + j with j = 0 for x, 1 for W, 2 for gamma and
@@ -119,6 +124,42 @@ def make_mlgru(w: MlgruWorkload) -> dict:
         "lb": rng("lb").uniform(0.0, 0.95, d).astype(np.float32),
         "h0": (rng("h0").standard_normal((w.B, d), dtype=np.float32) * np.float32(0.5)).astype(np.float32),
     }
+
+
+@dataclass(frozen=True)
+class TrainWorkload:
+    name: str
+    index: int          # seed index
+    M: int
+    K: int
+    N: int
+
+    @property
+    def ops(self) -> int:
+        """Effective dense ops of one training step: the forward's contraction
+        and the backward's two, 3 x 2 M N K."""
+        return 6 * self.M * self.N * self.K
+
+
+TRAIN_WORKLOADS = {
+    # the paper's training-efficiency setting: input size and sequence length
+    # 1024 (tokens of 16 sequences flattened into the batch)
+    "train_d1024": TrainWorkload("train_d1024", 7, 16 * 1024, 1024, 1024),
+    # the 1.3B model's GLU up-projection (gate|up) over 8192 tokens
+    "train_glu_up": TrainWorkload("train_glu_up", 8, 8192, 2048, 11264),
+}
+
+
+def make_train(w: TrainWorkload) -> dict:
+    """Inputs of a training workload: x (bf16 bits and float32 values [M][K],
+    N(0, 1)), gamma [K] U(0.5, 1.5), latent W [N][K] N(0, 0.02), output
+    gradient dO (bf16 bits [M][N], N(0, 1)); seed streams 0, 2, 1 and 4."""
+    base = Workload(w.name, w.index, w.M, w.K, w.N, "bf16", "normal", "uniform")
+    x_bits, x_f32 = make_x(base)
+    rng = np.random.default_rng(seed(w.index, 4))
+    dO = rng.standard_normal((w.M, w.N), dtype=np.float32)
+    return {"x_bits": x_bits, "x_f32": x_f32, "gamma": make_gamma(base), "W": make_w(base),
+            "dO_bits": f32_to_bf16_bits(dO)}
 
 
 def random_gates(rs: np.random.Generator, M: int, d: int, lb_max: float = 0.99):
