@@ -24,6 +24,11 @@ Workloads (shapes in workloads.py):
       algorithmic bytes per step.
   mlgru_prefill -- the MLGRU token mixer over one 2048-token sequence at
       d = 2048.  value = effective TOPS, 2*M*(3d + d)*d.
+  train_d1024, train_glu_up -- one training step of the layer: the training
+      forward (latent weights ternarised, rstd kept) and the backward (dx, dW,
+      db, dgamma) on the paper's training setting (input size and sequence
+      length 1024, 16 sequences) or the 1.3B model's GLU up-projection.
+      value = effective TOPS, 3 x 2*M*N*K per step.
 
 The JSON line carries the roofline of the dominant kernel (decode: the fused
 decode kernel, the only launch of a decode forward; prefill: the contraction),
@@ -52,6 +57,8 @@ INT8_PEAK_TOPS = 5000.0        # MI355X dense int8 MFMA, TOPS (5.0 POPS)
 DECODE = ("decode_m1", "decode_m8", "large_dec")
 GLU = ("glu_gate", "channel_mixer")
 MLGRU = ("mlgru_decode", "mlgru_prefill")
+TRAIN = ("train_d1024", "train_glu_up")
+BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 ROTATE_BYTES = 1 << 30         # distinct packed weights per decode step
 
 
@@ -617,6 +624,86 @@ def cpu_baseline_mlgru(name, step_bytes, seconds):
             "sample": f"the first {T} of {w.T} tokens (B={w.B}, d={w.d}) in {el:.1f} s"}
 
 
+def bench_train(torch, mmf, name, args):
+    import numpy as np
+    import workloads
+    w = workloads.TRAIN_WORKLOADS[name]
+    M, K, N = w.M, w.K, w.N
+    log(f"[bench] {name}: M={M} K={K} N={N}")
+    inp = workloads.make_train(w)
+    dev = torch.device("cuda:0")
+    T_ = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    x = torch.from_numpy(inp["x_bits"].view(np.int16)).to(dev).view(torch.bfloat16)
+    dO = torch.from_numpy(inp["dO_bits"].view(np.int16)).to(dev).view(torch.bfloat16)
+    gamma, W = T_(inp["gamma"]), T_(inp["W"])
+    del inp
+    y = torch.empty((M, N), dtype=torch.float32, device=dev)
+    Wp = torch.empty((K // 16, N), dtype=torch.int32, device=dev)
+    ws = torch.empty((1,), dtype=torch.float32, device=dev)
+    q = torch.empty((M, K), dtype=torch.int8, device=dev)
+    a = torch.empty((M,), dtype=torch.float32, device=dev)
+    r = torch.empty((M,), dtype=torch.float32, device=dev)
+    dx = torch.empty((M, K), dtype=torch.float32, device=dev)
+    dW = torch.empty((N, K), dtype=torch.float32, device=dev)
+    db = torch.empty((N,), dtype=torch.float32, device=dev)
+    dg = torch.empty((K,), dtype=torch.float32, device=dev)
+    wsf = torch.empty(mmf.mmf_bitlinear_train_workspace_bytes(M, K, N), dtype=torch.uint8, device=dev)
+    wsb = torch.empty(mmf.mmf_bitlinear_bwd_workspace_bytes(M, K, N), dtype=torch.uint8, device=dev)
+
+    def fwd():
+        mmf.mmf_bitlinear_train_fwd(x, gamma, W, None, y, Wp, ws, q, a, r, wsf)
+
+    def bwd():
+        mmf.mmf_bitlinear_bwd(dO, x, gamma, r, q, a, Wp, ws, dx, dW, db, dg, wsb)
+
+    def step():
+        fwd()
+        bwd()
+
+    timer = Timer(torch)
+    ms_step = timer.time(step, args.steps, args.warmup)
+    ms_fwd = timer.time(fwd, args.steps, args.warmup)
+    ms_bwd = timer.time(bwd, args.steps, args.warmup)
+    mnk2 = 2.0 * M * N * K
+    bwd_tflops = 2 * mnk2 / (ms_bwd * 1e-3) / 1e12
+    return {
+        "value": w.ops / (ms_step * 1e-3) / 1e12, "unit": "TOPS", "ms_per_step": ms_step,
+        "config": {"workload": name, "M": M, "K": K, "N": N, "x_dtype": "bf16", "dO_dtype": "bf16",
+                   "fwd_us": ms_fwd * 1e3, "bwd_us": ms_bwd * 1e3},
+        "roofline": {"bound": "mfma", "kernel": "backward: the dY and dW bf16 GEMMs (rocBLAS, fp32 "
+                                                "accumulation) with their operand preparation, "
+                                                "RMSNorm backward and column sums, timed as one call",
+                     "achieved": bwd_tflops, "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": bwd_tflops / BF16_PEAK_TFLOPS, "traffic": None,
+                     "flops_per_launch": 2 * mnk2, "avg_launch_us": ms_bwd * 1e3},
+        "forward": {"avg_call_us": ms_fwd * 1e3, "int8_TOPS": mnk2 / (ms_fwd * 1e-3) / 1e12,
+                    "note": "ternarisation of the latent weights + act-quant + int8 MFMA contraction"},
+    }
+
+
+def cpu_baseline_train(name, seconds):
+    """The oracle's training forward and backward on a sample of token rows
+    over all K and N, in effective TOPS (3 x 2 rows N K)."""
+    import oracle
+    import workloads
+    w = workloads.TRAIN_WORKLOADS[name]
+    inp = workloads.make_train(w)
+    dO = workloads.bf16_bits_to_f32(inp["dO_bits"])
+    rows = 4
+    while True:
+        t0 = time.perf_counter()
+        f = oracle.bitlinear_train_fwd(inp["x_f32"][:rows], inp["gamma"], inp["W"])
+        oracle.bitlinear_bwd(dO[:rows], inp["x_f32"][:rows], inp["gamma"], f["rstd"], f["q"],
+                             f["a_scale"], f["t"], f["w_scale"])
+        el = time.perf_counter() - t0
+        if el >= seconds / 4 or rows >= w.M:
+            break
+        rows = min(w.M, rows * max(2, int(seconds / 4 / max(el, 1e-3))))
+    return {"value": 6.0 * rows * w.N * w.K / el / 1e12, "unit": "TOPS", "cores": oracle.num_threads(),
+            "kind": "oracle", "sample": f"{rows} of {w.M} token rows (K={w.K}, N={w.N}), forward and "
+                                        f"backward, in {el:.1f} s"}
+
+
 def cpu_baseline_glu(name, seconds):
     """The oracle (two BitLinears, the gate; for channel_mixer also the down
     projection) on a sample of token rows, in effective TOPS."""
@@ -694,9 +781,11 @@ def main():
     import paper_2406_02528_amd as mmf
     import workloads
     assert torch.cuda.is_available(), "bench.py needs a HIP device"
-    w = None if args.workload in GLU + MLGRU else workloads.WORKLOADS[args.workload]
+    w = None if args.workload in GLU + MLGRU + TRAIN else workloads.WORKLOADS[args.workload]
     if args.workload in MLGRU:
         res, fb = bench_mlgru(torch, mmf, args.workload, args)
+    elif args.workload in TRAIN:
+        res, fb = bench_train(torch, mmf, args.workload, args), None
     elif w is None:
         res, _ = bench_glu(torch, mmf, args.workload, args)
         fb = None
@@ -712,7 +801,7 @@ def main():
         "data": "synthetic (seeded; shapes of the paper's model widths)",
         "config": res["config"], "roofline": res["roofline"],
     }
-    for k in ("hot_cache_call_us", "act_quant", "contraction_only", "launch_floor", "stages"):
+    for k in ("hot_cache_call_us", "act_quant", "contraction_only", "launch_floor", "stages", "forward"):
         if k in res:
             line[k] = res[k]
     if not args.no_secondary and w is not None and w.name in DECODE:
@@ -731,6 +820,8 @@ def main():
         log("[bench] cpu baseline (oracle)")
         if args.workload in MLGRU:
             line["cpu_baseline"] = cpu_baseline_mlgru(args.workload, fb, args.cpu_seconds)
+        elif args.workload in TRAIN:
+            line["cpu_baseline"] = cpu_baseline_train(args.workload, args.cpu_seconds)
         elif w is None:
             line["cpu_baseline"] = cpu_baseline_glu(args.workload, args.cpu_seconds)
         else:

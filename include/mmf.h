@@ -336,8 +336,9 @@ int mmf_bitlinear_train_fwd(const void *x, int x_is_f32, const float *gamma, con
  * mmf_bitlinear_train_fwd.  Outputs float32: dx [M][K], dW [N][K], db [N]
  * (NULL: not computed), dgamma [K] (NULL: not computed).  The two products
  * are bf16 GEMMs with fp32 accumulation on the matrix cores (rocBLAS); s, db
- * and dgamma are summed in fp64.  M at most 65535 * 64 (MMF_ERR_SHAPE).
- * M == 0 or N == 0 is a no-op.  Workspace as above.
+ * and dgamma are summed in fp64; when the dW product is long and narrow
+ * (few output tiles) its contraction over tokens is split into up to 8
+ * parts, added in fp64.  M == 0 or N == 0 is a no-op.  Workspace as above.
  */
 size_t mmf_bitlinear_bwd_workspace_bytes(int64_t M, int64_t K, int64_t N);
 int mmf_bitlinear_bwd(const uint16_t *dO, const void *x, int x_is_f32, const float *gamma,

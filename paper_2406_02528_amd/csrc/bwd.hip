@@ -14,6 +14,7 @@
 #include <rocblas/rocblas.h>
 
 #include <mutex>
+#include <type_traits>
 
 #include "mmf_device.h"
 #include "mmf_launch.h"
@@ -23,7 +24,6 @@ namespace {
 
 constexpr int kBlock = 256;
 constexpr int kRowsPerBlock = kBlock / kWave;  // one wave per row
-constexpr int64_t kChunkRows = 64;            // rows per partial of a column sum
 constexpr uint16_t kBf16One = 0x3F80, kBf16MinusOne = 0xBF80;
 
 unsigned blocks_for(int64_t threads) { return static_cast<unsigned>((threads + kBlock - 1) / kBlock); }
@@ -87,8 +87,10 @@ __device__ __forceinline__ void load_x4(const float* x, float* f) {
 }
 
 // One wave per row: s = sum_k g_k x_k in fp64 over the row, then
-// dx = r g - coef x with coef = r^3 s / K (rounded from fp64 once).
-template <typename XT>
+// dx = r g - coef x with coef = r^3 s / K (rounded from fp64 once).  VPL > 0:
+// the lane keeps its VPL groups of 4 (g and x) in registers between the two
+// passes (rows of K <= 256 VPL); VPL == 0 re-reads the row.
+template <typename XT, int VPL>
 __global__ __launch_bounds__(kBlock) void rms_norm_bwd_kernel(const float* __restrict__ dYs,
                                                               const float* __restrict__ w_scale,
                                                               const XT* __restrict__ x,
@@ -102,94 +104,186 @@ __global__ __launch_bounds__(kBlock) void rms_norm_bwd_kernel(const float* __res
   const float r = rstd[row];
   const float* dr = dYs + row * K;
   const XT* xr = x + row * K;
-  double s = 0.0;
-  for (int k = 4 * lane; k < K; k += 4 * kWave) {
+  auto load_gx = [&](int k, float* g, float* xf) {
     const float4 d = *reinterpret_cast<const float4*>(dr + k);
     const float dv[4] = {d.x, d.y, d.z, d.w};
-    float xf[4];
     load_x4(xr + k, xf);
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const float dy = w * dv[e];
-      const float g = gamma != nullptr ? gamma[k + e] * dy : dy;
-      s += static_cast<double>(g) * static_cast<double>(xf[e]);
+      g[e] = gamma != nullptr ? gamma[k + e] * dy : dy;
     }
-  }
-  s = wave_sum_f64(s);
-  const double rd = static_cast<double>(r);
-  const float coef = static_cast<float>(rd * rd * rd * s / static_cast<double>(K));
-  for (int k = 4 * lane; k < K; k += 4 * kWave) {
-    const float4 d = *reinterpret_cast<const float4*>(dr + k);
-    const float dv[4] = {d.x, d.y, d.z, d.w};
-    float xf[4];
-    load_x4(xr + k, xf);
+  };
+  auto store_dx = [&](int k, const float* g, const float* xf, float coef) {
     float o[4];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const float dy = w * dv[e];
-      const float g = gamma != nullptr ? gamma[k + e] * dy : dy;
-      o[e] = r * g - coef * xf[e];
-    }
+    for (int e = 0; e < 4; ++e) o[e] = r * g[e] - coef * xf[e];
     *reinterpret_cast<float4*>(dx + row * K + k) = make_float4(o[0], o[1], o[2], o[3]);
+  };
+  double s = 0.0;
+  if constexpr (VPL > 0) {
+    float g[VPL][4], xf[VPL][4];
+#pragma unroll
+    for (int i = 0; i < VPL; ++i) {
+      const int k = 4 * (lane + kWave * i);
+      if (k < K) {
+        load_gx(k, g[i], xf[i]);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) s += static_cast<double>(g[i][e]) * static_cast<double>(xf[i][e]);
+      }
+    }
+    s = wave_sum_f64(s);
+    const double rd = static_cast<double>(r);
+    const float coef = static_cast<float>(rd * rd * rd * s / static_cast<double>(K));
+#pragma unroll
+    for (int i = 0; i < VPL; ++i) {
+      const int k = 4 * (lane + kWave * i);
+      if (k < K) store_dx(k, g[i], xf[i], coef);
+    }
+  } else {
+    for (int k = 4 * lane; k < K; k += 4 * kWave) {
+      float g[4], xf[4];
+      load_gx(k, g, xf);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) s += static_cast<double>(g[e]) * static_cast<double>(xf[e]);
+    }
+    s = wave_sum_f64(s);
+    const double rd = static_cast<double>(r);
+    const float coef = static_cast<float>(rd * rd * rd * s / static_cast<double>(K));
+    for (int k = 4 * lane; k < K; k += 4 * kWave) {
+      float g[4], xf[4];
+      load_gx(k, g, xf);
+      store_dx(k, g, xf, coef);
+    }
   }
 }
 
-// Column sums: partial p of column c is the fp64 sum over rows
-// [p kChunkRows, (p+1) kChunkRows); the final pass adds the partials in order.
+// Column sums: partial p of a column is the fp64 sum over the rows
+// [p R, (p+1) R), R = max(ceil(M / kMaxParts), kMinRowsPerPart); a final
+// pass adds the partials.  Every sum runs in a fixed order, so the results
+// are reproducible; 16-byte loads where a row's group of 8 is aligned.
+constexpr int64_t kMaxParts = 64;
+constexpr int64_t kMinRowsPerPart = 256;
+
 struct SumBf16 {
   const uint16_t* a;
   int64_t cols;
-  __device__ double operator()(int64_t m, int64_t c) const {
-    return static_cast<double>(__uint_as_float(static_cast<uint32_t>(a[m * cols + c]) << 16));
+  __device__ void add8(int64_t m, int64_t c0, double* acc) const {
+    const uint16_t* p = a + m * cols + c0;
+    if ((cols & 7) == 0) {
+      const uint4 v = *reinterpret_cast<const uint4*>(p);
+      const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        acc[2 * i] += static_cast<double>(__uint_as_float(w[i] << 16));
+        acc[2 * i + 1] += static_cast<double>(__uint_as_float(w[i] & 0xFFFF0000u));
+      }
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        if (c0 + e < cols) acc[e] += static_cast<double>(__uint_as_float(static_cast<uint32_t>(p[e]) << 16));
+    }
   }
 };
 template <typename XT>
-struct SumDgamma {
+struct SumDgamma {  // cols = K, a multiple of 16
   const float* dYs;
   const float* w_scale;
   const XT* x;
   const float* rstd;
   int64_t cols;
-  __device__ double operator()(int64_t m, int64_t c) const {
-    float xv;
-    if constexpr (sizeof(XT) == 2)
-      xv = __uint_as_float(static_cast<uint32_t>(x[m * cols + c]) << 16);
-    else
-      xv = x[m * cols + c];
-    const float dy = w_scale[0] * dYs[m * cols + c];
-    return static_cast<double>(dy) * static_cast<double>(xv) * static_cast<double>(rstd[m]);
+  __device__ void add8(int64_t m, int64_t c0, double* acc) const {
+    const float w = w_scale[0];
+    const double r = static_cast<double>(rstd[m]);
+    const float4 d0 = *reinterpret_cast<const float4*>(dYs + m * cols + c0);
+    const float4 d1 = *reinterpret_cast<const float4*>(dYs + m * cols + c0 + 4);
+    const float dv[8] = {d0.x, d0.y, d0.z, d0.w, d1.x, d1.y, d1.z, d1.w};
+    float xv[8];
+    load_x4(x + m * cols + c0, xv);
+    load_x4(x + m * cols + c0 + 4, xv + 4);
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+      acc[e] += static_cast<double>(w * dv[e]) * static_cast<double>(xv[e]) * r;
   }
 };
 
+// Partial pass: a workgroup owns 64 columns (8 groups of 8) and the rows
+// [p R, (p+1) R); thread (row lane rl, group cg) adds rows m0 + rl + 32 i,
+// so a wave reads 8 rows of 64 contiguous columns at a time; the 32 row
+// lanes are then added in LDS in a fixed order.
+constexpr int kColGroups = 8, kRowLanes = kBlock / kColGroups;  // 8 x 32
+
 template <typename F>
-__global__ __launch_bounds__(kBlock) void col_partial_kernel(F f, int64_t M, int64_t cols, double* partials) {
-  const int64_t c = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
-  if (c >= cols) return;
+__global__ __launch_bounds__(kBlock) void col_partial_kernel(F f, int64_t M, int64_t cols, int64_t rows_per_part,
+                                                             double* partials) {
+  __shared__ double red[kRowLanes][kColGroups * 8 + 1];
+  const int cg = threadIdx.x % kColGroups, rl = threadIdx.x / kColGroups;
+  const int64_t c0 = static_cast<int64_t>(blockIdx.x) * (kColGroups * 8) + 8 * cg;
   const int64_t p = blockIdx.y;
-  const int64_t m0 = p * kChunkRows;
-  const int64_t m1 = m0 + kChunkRows < M ? m0 + kChunkRows : M;
-  double acc = 0.0;
-  for (int64_t m = m0; m < m1; ++m) acc += f(m, c);
-  partials[p * cols + c] = acc;
+  const int64_t m0 = p * rows_per_part;
+  const int64_t m1 = m0 + rows_per_part < M ? m0 + rows_per_part : M;
+  double acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  if (c0 < cols) {
+#pragma unroll 2
+    for (int64_t m = m0 + rl; m < m1; m += kRowLanes) f.add8(m, c0, acc);
+  }
+#pragma unroll
+  for (int e = 0; e < 8; ++e) red[rl][8 * cg + e] = acc[e];
+  __syncthreads();
+  if (threadIdx.x < kColGroups * 8) {
+    const int c = threadIdx.x;
+    double s = 0.0;
+    for (int l = 0; l < kRowLanes; ++l) s += red[l][c];
+    const int64_t col = static_cast<int64_t>(blockIdx.x) * (kColGroups * 8) + c;
+    if (col < cols) partials[p * cols + col] = s;
+  }
 }
 
+// Final pass: 32 columns per workgroup, 8 lanes per column over the partials,
+// then the lanes in a fixed order.
 __global__ __launch_bounds__(kBlock) void col_final_kernel(const double* partials, int64_t nparts, int64_t cols,
                                                            float* out) {
-  const int64_t c = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
-  if (c >= cols) return;
+  constexpr int kCols = 32, kLanes = kBlock / kCols;
+  __shared__ double red[kLanes][kCols];
+  const int c = threadIdx.x % kCols, l = threadIdx.x / kCols;
+  const int64_t col = static_cast<int64_t>(blockIdx.x) * kCols + c;
   double acc = 0.0;
-  for (int64_t p = 0; p < nparts; ++p) acc += partials[p * cols + c];
-  out[c] = static_cast<float>(acc);
+  if (col < cols)
+    for (int64_t p = l; p < nparts; p += kLanes) acc += partials[p * cols + col];
+  red[l][c] = acc;
+  __syncthreads();
+  if (l == 0 && col < cols) {
+    double s = 0.0;
+    for (int i = 0; i < kLanes; ++i) s += red[i][c];
+    out[col] = static_cast<float>(s);
+  }
+}
+
+int64_t rows_per_part(int64_t M) {
+  int64_t R = (M + kMaxParts - 1) / kMaxParts;
+  return R < kMinRowsPerPart ? kMinRowsPerPart : R;
 }
 
 template <typename F>
 hipError_t col_sum(F f, int64_t M, int64_t cols, double* partials, float* out, hipStream_t stream) {
-  const int64_t nparts = col_sum_partials(M);
-  if (nparts > 65535) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(col_partial_kernel<F>, dim3(blocks_for(cols), static_cast<unsigned>(nparts)), dim3(kBlock), 0,
-                     stream, f, M, cols, partials);
-  hipLaunchKernelGGL(col_final_kernel, dim3(blocks_for(cols)), dim3(kBlock), 0, stream, partials, nparts, cols, out);
+  const int64_t R = rows_per_part(M);
+  const int64_t nparts = (M + R - 1) / R;
+  hipLaunchKernelGGL(col_partial_kernel<F>,
+                     dim3(static_cast<unsigned>((cols + kColGroups * 8 - 1) / (kColGroups * 8)),
+                          static_cast<unsigned>(nparts)),
+                     dim3(kBlock), 0, stream, f, M, cols, R, partials);
+  hipLaunchKernelGGL(col_final_kernel, dim3(static_cast<unsigned>((cols + 31) / 32)), dim3(kBlock), 0, stream,
+                     partials, nparts, cols, out);
   return hipGetLastError();
+}
+
+// Sum of S partial products [S][n] into out [n], in order, in fp64.
+__global__ __launch_bounds__(kBlock) void sum_parts_kernel(const float* parts, int64_t S, int64_t n, float* out) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+  if (i >= n) return;
+  double acc = 0.0;
+  for (int64_t s = 0; s < S; ++s) acc += static_cast<double>(parts[s * n + i]);
+  out[i] = static_cast<float>(acc);
 }
 
 // One rocBLAS handle per device, created on first use; the stream is set
@@ -225,16 +319,32 @@ hipError_t launch_rms_norm_bwd(const float* dYs, const float* w_scale, const voi
                                hipStream_t stream) {
   if (M == 0) return hipSuccess;
   const dim3 grid(static_cast<unsigned>((M + kRowsPerBlock - 1) / kRowsPerBlock));
+  const int vpl = (K + 4 * kWave - 1) / (4 * kWave);
+  auto go = [&](auto xt, auto v) {
+    using XT = decltype(xt);
+    constexpr int V = decltype(v)::value;
+    hipLaunchKernelGGL((rms_norm_bwd_kernel<XT, V>), grid, dim3(kBlock), 0, stream, dYs, w_scale,
+                       static_cast<const XT*>(x), gamma, rstd, M, K, dx);
+  };
+  auto by_vpl = [&](auto xt) {
+    if (vpl <= 1) go(xt, std::integral_constant<int, 1>{});
+    else if (vpl <= 2) go(xt, std::integral_constant<int, 2>{});
+    else if (vpl <= 4) go(xt, std::integral_constant<int, 4>{});
+    else if (vpl <= 8) go(xt, std::integral_constant<int, 8>{});
+    else go(xt, std::integral_constant<int, 0>{});
+  };
   if (x_is_f32)
-    hipLaunchKernelGGL(rms_norm_bwd_kernel<float>, grid, dim3(kBlock), 0, stream, dYs, w_scale,
-                       static_cast<const float*>(x), gamma, rstd, M, K, dx);
+    by_vpl(float{});
   else
-    hipLaunchKernelGGL(rms_norm_bwd_kernel<uint16_t>, grid, dim3(kBlock), 0, stream, dYs, w_scale,
-                       static_cast<const uint16_t*>(x), gamma, rstd, M, K, dx);
+    by_vpl(uint16_t{});
   return hipGetLastError();
 }
 
-int64_t col_sum_partials(int64_t M) { return M > 0 ? (M + kChunkRows - 1) / kChunkRows : 1; }
+int64_t col_sum_partials(int64_t M) {
+  if (M <= 0) return 1;
+  const int64_t R = rows_per_part(M);
+  return (M + R - 1) / R;
+}
 
 hipError_t launch_col_sum_bf16(const uint16_t* dO, int64_t M, int64_t N, double* partials, float* db,
                                hipStream_t stream) {
@@ -251,8 +361,31 @@ hipError_t launch_dgamma(const float* dYs, const float* w_scale, const void* x, 
                  dgamma, stream);
 }
 
+int64_t dw_split(int64_t M, int64_t N, int64_t K) {
+  // Split the contraction over tokens into S equal parts (S a power of two
+  // dividing M, parts of at least 1024 tokens) while the output has fewer than
+  // 128 tiles of 256 x 256: a long, narrow product otherwise leaves most of
+  // the matrix cores idle.
+  const int64_t tiles = ((N + 255) / 256) * ((K + 255) / 256);
+  int64_t S = 1;
+  while (S < 8 && tiles * S < 128 && M % (2 * S) == 0 && M / (2 * S) >= 1024) S *= 2;
+  return S;
+}
+
+hipError_t gemm_bf16_dw(int64_t M, int64_t N, int64_t K, const uint16_t* dO, const uint16_t* yq, float* dW,
+                        float* parts, hipStream_t stream) {
+  const int64_t S = dw_split(M, N, K);
+  if (S == 1) return gemm_bf16(true, false, N, K, M, dO, N, yq, K, dW, K, stream, 1, 0, 0, 0);
+  const int64_t Ms = M / S;
+  const hipError_t e = gemm_bf16(true, false, N, K, Ms, dO, N, yq, K, parts, K, stream, S, Ms * N, Ms * K, N * K);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(sum_parts_kernel, dim3(blocks_for(N * K)), dim3(kBlock), 0, stream, parts, S, N * K, dW);
+  return hipGetLastError();
+}
+
 hipError_t gemm_bf16(bool transA, bool transB, int64_t Mr, int64_t Nc, int64_t Kc, const uint16_t* A,
-                     int64_t lda, const uint16_t* B, int64_t ldb, float* C, int64_t ldc, hipStream_t stream) {
+                     int64_t lda, const uint16_t* B, int64_t ldb, float* C, int64_t ldc, hipStream_t stream,
+                     int64_t batch, int64_t strideA, int64_t strideB, int64_t strideC) {
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return hipErrorInvalidDevice;
   BlasHandles& bh = blas();
@@ -265,13 +398,23 @@ hipError_t gemm_bf16(bool transA, bool transB, int64_t Mr, int64_t Nc, int64_t K
   if (rocblas_set_stream(h, stream) != rocblas_status_success) return hipErrorUnknown;
   const float alpha = 1.0f, beta = 0.0f;
   // row-major C = op(A) op(B) is column-major C^T = op(B)^T op(A)^T
-  const rocblas_status st = rocblas_gemm_ex(
-      h, transB ? rocblas_operation_transpose : rocblas_operation_none,
-      transA ? rocblas_operation_transpose : rocblas_operation_none, static_cast<rocblas_int>(Nc),
-      static_cast<rocblas_int>(Mr), static_cast<rocblas_int>(Kc), &alpha, B, rocblas_datatype_bf16_r,
-      static_cast<rocblas_int>(ldb), A, rocblas_datatype_bf16_r, static_cast<rocblas_int>(lda), &beta, C,
-      rocblas_datatype_f32_r, static_cast<rocblas_int>(ldc), C, rocblas_datatype_f32_r,
-      static_cast<rocblas_int>(ldc), rocblas_datatype_f32_r, rocblas_gemm_algo_standard, 0, 0);
+  const rocblas_operation opB = transB ? rocblas_operation_transpose : rocblas_operation_none;
+  const rocblas_operation opA = transA ? rocblas_operation_transpose : rocblas_operation_none;
+  rocblas_status st;
+  if (batch == 1)
+    st = rocblas_gemm_ex(h, opB, opA, static_cast<rocblas_int>(Nc), static_cast<rocblas_int>(Mr),
+                         static_cast<rocblas_int>(Kc), &alpha, B, rocblas_datatype_bf16_r,
+                         static_cast<rocblas_int>(ldb), A, rocblas_datatype_bf16_r, static_cast<rocblas_int>(lda),
+                         &beta, C, rocblas_datatype_f32_r, static_cast<rocblas_int>(ldc), C,
+                         rocblas_datatype_f32_r, static_cast<rocblas_int>(ldc), rocblas_datatype_f32_r,
+                         rocblas_gemm_algo_standard, 0, 0);
+  else
+    st = rocblas_gemm_strided_batched_ex(
+        h, opB, opA, static_cast<rocblas_int>(Nc), static_cast<rocblas_int>(Mr), static_cast<rocblas_int>(Kc),
+        &alpha, B, rocblas_datatype_bf16_r, static_cast<rocblas_int>(ldb), strideB, A, rocblas_datatype_bf16_r,
+        static_cast<rocblas_int>(lda), strideA, &beta, C, rocblas_datatype_f32_r, static_cast<rocblas_int>(ldc),
+        strideC, C, rocblas_datatype_f32_r, static_cast<rocblas_int>(ldc), strideC,
+        static_cast<rocblas_int>(batch), rocblas_datatype_f32_r, rocblas_gemm_algo_standard, 0, 0);
   return st == rocblas_status_success ? hipSuccess : hipErrorUnknown;
 }
 

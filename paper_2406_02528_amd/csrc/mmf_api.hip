@@ -322,7 +322,7 @@ TrainScratch train_scratch(int64_t M, int64_t K, int64_t N) {
 }
 
 struct BwdScratch {
-  size_t t_off, yq_off, dy_off, part_off, total;
+  size_t t_off, yq_off, dy_off, part_off, dw_off, total;
 };
 BwdScratch bwd_scratch(int64_t M, int64_t K, int64_t N) {
   BwdScratch s;
@@ -331,11 +331,12 @@ BwdScratch bwd_scratch(int64_t M, int64_t K, int64_t N) {
   s.dy_off = s.yq_off + round_up(static_cast<size_t>(M) * static_cast<size_t>(K) * 2, kScratchAlign);
   s.part_off = s.dy_off + round_up(static_cast<size_t>(M) * static_cast<size_t>(K) * 4, kScratchAlign);
   const int64_t cols = N > K ? N : K;
-  s.total = s.part_off + round_up(sizeof(double) * static_cast<size_t>(mmf::col_sum_partials(M) * cols),
-                                  kScratchAlign);
+  s.dw_off = s.part_off + round_up(sizeof(double) * static_cast<size_t>(mmf::col_sum_partials(M) * cols),
+                                   kScratchAlign);
+  const int64_t S = mmf::dw_split(M, N, K);
+  s.total = s.dw_off + (S > 1 ? round_up(sizeof(float) * static_cast<size_t>(S * N * K), kScratchAlign) : 0);
   return s;
 }
-constexpr int64_t kMaxBwdRows = int64_t(65535) * 64;  // column sums: 64 rows per partial
 
 }  // namespace
 
@@ -675,7 +676,6 @@ int mmf_bitlinear_bwd(const uint16_t* dO, const void* x, int x_is_f32, const flo
                       int64_t K, int64_t N, void* workspace, size_t workspace_bytes, hipStream_t stream) {
   if (x_is_f32 != 0 && x_is_f32 != 1) return MMF_ERR_ARG;
   if (int st = check_shape(M, K, N)) return st;
-  if (M > kMaxBwdRows) return MMF_ERR_SHAPE;
   if (M == 0 || N == 0) return MMF_OK;
   if (!dO || !x || !rstd || !q || !a_scale || !Wpacked || !w_scale || !dx || !dW) return MMF_ERR_NULL;
   if (!aligned16(dO) || !aligned16(x) || !aligned16(rstd) || !aligned16(q) || !aligned16(a_scale) ||
@@ -696,7 +696,9 @@ int mmf_bitlinear_bwd(const uint16_t* dO, const void* x, int x_is_f32, const flo
       return MMF_ERR_HIP;
     // dW = dO^T Yq
     if (mmf::launch_dequant_bf16(q, a_scale, M, Ki, yq, stream) != hipSuccess) return MMF_ERR_HIP;
-    if (mmf::gemm_bf16(true, false, N, K, M, dO, N, yq, K, dW, K, stream) != hipSuccess) return MMF_ERR_HIP;
+    if (mmf::gemm_bf16_dw(M, N, K, dO, yq, dW, reinterpret_cast<float*>(scratch + s.dw_off), stream) !=
+        hipSuccess)
+      return MMF_ERR_HIP;
     if (db && mmf::launch_col_sum_bf16(dO, M, N, parts, db, stream) != hipSuccess) return MMF_ERR_HIP;
     if (dgamma && mmf::launch_dgamma(dYs, w_scale, x, x_is_f32 == 1, rstd, M, Ki, parts, dgamma, stream) !=
                       hipSuccess)

@@ -122,9 +122,17 @@ hipError_t launch_dgamma(const float* dYs, const float* w_scale, const void* x, 
                          hipStream_t stream);
 // Dense bf16 x bf16 -> fp32 products on the matrix cores through rocBLAS,
 // row-major operands:  C[Mr][Nc] = A[Mr][Kc] * B[Kc][Nc] (transB: B given as
-// [Nc][Kc]); (transA: A given as [Kc][Mr]).
+// [Nc][Kc]); (transA: A given as [Kc][Mr]); `batch` products at the given
+// element strides.
 hipError_t gemm_bf16(bool transA, bool transB, int64_t Mr, int64_t Nc, int64_t Kc, const uint16_t* A,
-                     int64_t lda, const uint16_t* B, int64_t ldb, float* C, int64_t ldc, hipStream_t stream);
+                     int64_t lda, const uint16_t* B, int64_t ldb, float* C, int64_t ldc, hipStream_t stream,
+                     int64_t batch = 1, int64_t strideA = 0, int64_t strideB = 0, int64_t strideC = 0);
+// dW [N][K] = dO^T yq (dO bf16 [M][N], yq bf16 [M][K]); long narrow products
+// are split over tokens into dw_split(M, N, K) parts summed in fp64 (`parts`
+// holds dw_split * N * K floats when the split is > 1).
+int64_t dw_split(int64_t M, int64_t N, int64_t K);
+hipError_t gemm_bf16_dw(int64_t M, int64_t N, int64_t K, const uint16_t* dO, const uint16_t* yq, float* dW,
+                        float* parts, hipStream_t stream);
 
 hipError_t launch_glu_pack(const uint32_t* Wg, const uint32_t* Wu, int64_t L, int K, uint32_t* Wgu,
                            hipStream_t stream);

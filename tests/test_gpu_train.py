@@ -165,7 +165,9 @@ def run_bwd(mmf, M, K, N, f32_x, with_gamma, int_grad=False, seed=0, dgamma=True
     return dx, dW, dbt, dgt
 
 
-@pytest.mark.parametrize("M,K,N", [(1, 16, 1), (5, 64, 36), (70, 256, 100), (300, 1024, 513)])
+@pytest.mark.parametrize("M,K,N", [(1, 16, 1), (5, 64, 36), (70, 256, 100), (300, 1024, 513),
+                                   (33, 2048, 40), (17, 4096, 24),   # rows held in registers / re-read
+                                   (4096, 256, 128)])                # dW split over tokens
 @pytest.mark.parametrize("f32_x,with_gamma", [(False, True), (True, False)])
 def test_bwd_random(mmf, M, K, N, f32_x, with_gamma):
     log(f"[bwd] M={M} K={K} N={N} f32_x={f32_x} gamma={with_gamma}")
