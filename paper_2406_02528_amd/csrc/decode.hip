@@ -111,12 +111,13 @@ struct RowStage {
   int row, gtid, nvec;
   bool active;
 
-  __device__ void load(const void* xv, const float* __restrict__ gamma, int K) {
+  __device__ void load(const void* xv, const float* __restrict__ gamma, int K, bool inactive_skip = false) {
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     row = wave / G;
     gtid = threadIdx.x - row * G * kWave;
     active = row < MT;  // waves past MT * G take no part in the row work
     nvec = K / E;
+    if (inactive_skip && !active) return;  // wave-uniform
     const int srow = active ? row : 0;
     const uint4* xrow = reinterpret_cast<const uint4*>(
         static_cast<const char*>(xv) + static_cast<int64_t>(srow) * K * (16 / E));
@@ -325,9 +326,17 @@ struct Params {
 // lane (c, h) is word row jb + H s + h.  Whether a slot exists is therefore
 // the same for the whole wave, and its address is a scalar base
 // (Wp + (jb + H s) N) plus a per-lane offset (h N + column) computed once.
-template <int MT, int H, Src S, int VP, int kPrefetch, Epilogue EP>
+//
+// kLdsW: the workgroup's whole weight block (K/16 word rows of 64 columns) is
+// copied into LDS by LDS-DMA at entry -- 16 bytes per lane, four word rows
+// per wave instruction, no registers held, everything in flight at once --
+// by the waves that do not normalise token rows (H = 1, at most 2 tokens),
+// so the norm's own LDS traffic never waits on the copies; the contraction
+// then reads the words from LDS.
+template <int MT, int H, Src S, int VP, int kPrefetch, Epilogue EP, bool kLdsW = false>
 __global__ __launch_bounds__(kThreads) void decode_kernel(const Params prm) {
   static_assert(kPrefetch % 4 == 0, "prefetch goes in groups of four");
+  static_assert(!kLdsW || (H == 1 && MT <= 2 && S != Src::kQuantised), "LDS weight staging: H = 1, <= 2 tokens");
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const int K = prm.K;
   const int64_t N = prm.N;
@@ -361,20 +370,58 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(const Params prm) {
   //    wave waits for that: x and gamma then cross a quiet memory system
   //    (issued together with 3 MB of weight misses they return late), and
   //    the rest of the norm overlaps the weight stream.
+  if constexpr (kLdsW) {
+    // word rows 4g .. 4g + 3 of the block: lane l copies row 4g + l / 16,
+    // columns 4 (l % 16) .. + 3 (N % 4 == 0: a 16-byte chunk is whole); rows
+    // past K/16 fall outside the buffer and read as zero; columns past N
+    // belong to outputs that are not stored.
+    // Issued first, by the waves that do no row work; those waves then issue
+    // no other vector memory load before the wait ahead of the contraction,
+    // so no wait the compiler places (it cannot see these copies) holds them
+    // up at the norm's barriers.  The copies are inline assembly, out of the
+    // compiler's sight:
+    // it would otherwise hold every barrier of the norm until they land.
+    // Loads retire in issue order, so the compiler's own waits can only wait
+    // longer because of them, never shorter; the wait for the copies
+    // themselves is the explicit vmcnt(0) before the contraction.
+    if (wave >= row_waves<MT>() * row_groups<MT>()) {
+      const int first = wave - row_waves<MT>() * row_groups<MT>();
+      const int issuers = kWaves - row_waves<MT>() * row_groups<MT>();
+      const int G = (J + 3) / 4;
+      const uint32_t n0 = static_cast<uint32_t>(blockIdx.x) * kWave;
+      const uint32_t lv = (static_cast<uint32_t>(lane >> 4) * static_cast<uint32_t>(N) + n0 +
+                           4u * static_cast<uint32_t>(lane & 15)) * 4u;
+      const uint64_t wa = reinterpret_cast<uint64_t>(prm.Wp);
+      const v4i desc = {static_cast<int>(static_cast<uint32_t>(wa)), static_cast<int>((wa >> 32) & 0xFFFF),
+                        static_cast<int>(static_cast<uint32_t>(J) * 4u * static_cast<uint32_t>(N)), kBufferFlags};
+      const uint32_t wl = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(smem)) +
+                          static_cast<uint32_t>(prm.q_bytes + kScalarBytes);
+      for (int g = first; g < G; g += issuers) {  // wave-uniform
+        const uint32_t dst = __builtin_amdgcn_readfirstlane(wl + static_cast<uint32_t>(g * kLdsDmaChunk));
+        const uint32_t soff = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(g) * 4u * row_bytes);
+        asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+                     :
+                     : "s"(dst), "v"(lv), "s"(desc), "s"(soff)
+                     : "memory", "m0");
+      }
+    }
+  }
   RowStage<MT, S == Src::kQuantised ? Src::kBf16 : S, VP> rows;
   QStage<MT> qs;
   if constexpr (S == Src::kQuantised) {
     qs.load(prm.q, prm.a_scale, prm.q_rowsum, K, sh);
   } else {
-    rows.load(prm.x, prm.gamma, K);
+    rows.load(prm.x, prm.gamma, K, kLdsW);
   }
   // the factors of the column this thread writes in the affine epilogue
   // (issued after the token rows, so a wait for those leaves them in flight)
   ColAffine col{};
   if constexpr (EP == Epilogue::kAffineF32) {
-    const int64_t cn = static_cast<int64_t>(blockIdx.x) * C + tid % C;
-    col = load_col_affine(prm.affine, prm.w_scale, static_cast<uint32_t>(N),
-                          cn < N ? static_cast<uint32_t>(cn) : 0u);
+    if (!kLdsW || tid < MT * C) {  // under kLdsW: the epilogue's threads only (row waves)
+      const int64_t cn = static_cast<int64_t>(blockIdx.x) * C + tid % C;
+      col = load_col_affine(prm.affine, prm.w_scale, static_cast<uint32_t>(N),
+                            cn < N ? static_cast<uint32_t>(cn) : 0u);
+    }
   }
   if constexpr (S != Src::kQuantised) {
     if constexpr (kWeightDelay < 0) {
@@ -394,20 +441,30 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(const Params prm) {
   //    without a memory access.
   uint32_t wbuf[kPrefetch];
   const int last = ns > 0 ? ns - 1 : 0;
+  if constexpr (!kLdsW) {
 #pragma unroll
-  for (int p = 0; p < kPrefetch; ++p) {
-    const uint32_t sp = static_cast<uint32_t>(p < last ? p : last);
-    wbuf[p] = __builtin_amdgcn_raw_buffer_load_b32(wrsrc, lane_off, wave_bytes + sp * slot_bytes, 0);
+    for (int p = 0; p < kPrefetch; ++p) {
+      const uint32_t sp = static_cast<uint32_t>(p < last ? p : last);
+      wbuf[p] = __builtin_amdgcn_raw_buffer_load_b32(wrsrc, lane_off, wave_bytes + sp * slot_bytes, 0);
+    }
   }
   __builtin_amdgcn_sched_barrier(0);
 
   // 3. quantised activations into LDS (waits for the activation loads only)
-  if (tid < kMaxTokens * kWave) sh.red[tid] = 0;
+  if constexpr (kLdsW) {
+    constexpr int kRowThreads = row_waves<MT>() * row_groups<MT>() * kWave;
+    if (tid < kRowThreads)
+      for (int i = tid; i < kMaxTokens * kWave; i += kRowThreads) sh.red[i] = 0;
+  } else {
+    if (tid < kMaxTokens * kWave) sh.red[tid] = 0;
+  }
   if constexpr (S == Src::kQuantised) {
     qs.store(sh);
   } else {
     rows.finish(prm.gamma != nullptr, K, sh, kWeightDelay >= 0);
   }
+  // every LDS-DMA copy of this wave has landed before the barrier
+  if constexpr (kLdsW) __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
   __syncthreads();
 
   // 4. contraction.  A slot past the wave's range gets the word 0 (code 0
@@ -417,7 +474,26 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(const Params prm) {
   int acc[MT];
 #pragma unroll
   for (int m = 0; m < MT; ++m) acc[m] = 0;
-  for (int base = 0; base < ns; base += kPrefetch) {
+  if constexpr (kLdsW) {
+    const uint32_t* wl = reinterpret_cast<const uint32_t*>(smem + prm.q_bytes + kScalarBytes);
+#pragma unroll 4
+    for (int s = 0; s < ns; ++s) {
+      const int j = jb + s;
+      const uint32_t w = wl[j * kWave + c];
+      const uint32_t c0 = codes4(w, 0), c1 = codes4(w, 1), c2 = codes4(w, 2), c3 = codes4(w, 3);
+#pragma unroll
+      for (int m = 0; m < MT; ++m) {
+        const uint4 q4 = *reinterpret_cast<const uint4*>(sh.q + m * K + 16 * j);
+        int a = acc[m];
+        a = dot4(c0, q4.x, a);
+        a = dot4(c1, q4.y, a);
+        a = dot4(c2, q4.z, a);
+        a = dot4(c3, q4.w, a);
+        acc[m] = a;
+      }
+    }
+  }
+  for (int base = 0; base < (kLdsW ? 0 : ns); base += kPrefetch) {
     uint32_t cur[kPrefetch];
 #pragma unroll
     for (int p = 0; p < kPrefetch; ++p) cur[p] = base + p < ns ? wbuf[p] : 0u;
@@ -489,7 +565,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(const Params prm) {
   }
 }
 
-template <int MT, int H, Src S, int VP, int PF, Epilogue EP>
+template <int MT, int H, Src S, int VP, int PF, Epilogue EP, bool kLdsW = false>
 hipError_t launch_one(const DecodeArgs& a, hipStream_t stream) {
   constexpr int C = kWave / H;
   // the q region is whole LDS-DMA chunks
@@ -497,8 +573,9 @@ hipError_t launch_one(const DecodeArgs& a, hipStream_t stream) {
   const dim3 grid(static_cast<unsigned>((a.N + C - 1) / C));
   const Params prm{a.Wpacked, a.x, a.gamma, a.q, a.a_scale, a.q_rowsum, a.w_scale, a.out,
                    a.N, a.K, region, a.affine};
-  hipLaunchKernelGGL((decode_kernel<MT, H, S, VP, PF, EP>), grid, dim3(kThreads), region + kScalarBytes,
-                     stream, prm);
+  const int wbytes = kLdsW ? ((a.K / 16 + 3) / 4) * kLdsDmaChunk : 0;
+  hipLaunchKernelGGL((decode_kernel<MT, H, S, VP, PF, EP, kLdsW>), grid, dim3(kThreads),
+                     region + kScalarBytes + wbytes, stream, prm);
   return hipGetLastError();
 }
 
@@ -535,8 +612,28 @@ hipError_t dispatch_vp(const DecodeArgs& a, hipStream_t stream) {
   }
 }
 
+// The LDS weight staging pays when a workgroup's block is large (many word
+// rows per lane); it needs N % 4 == 0 (16-byte row chunks) and room in LDS
+// next to the q region.
+constexpr int kLdsWMinRows = 256;
+constexpr int kLdsLimit = 160 * 1024;
+inline bool use_lds_weights(int mt, int K, int64_t N, bool from_x) {
+  const int J = K / 16;
+  if (!from_x || mt > 2 || N % 4 != 0 || J < kLdsWMinRows) return false;
+  const int region = ((mt * K + kLdsDmaChunk - 1) / kLdsDmaChunk) * kLdsDmaChunk;
+  return region + kScalarBytes + ((J + 3) / 4) * kLdsDmaChunk <= kLdsLimit;
+}
+
 template <int MT, Src S, Epilogue EP>
 hipError_t dispatch_h(const DecodeArgs& a, hipStream_t stream) {
+  if constexpr (MT <= 2 && S != Src::kQuantised) {
+    if (use_lds_weights(MT, a.K, a.N, true)) {
+      const int vp = needed_vp(MT, a.K, S == Src::kF32);
+      if (vp <= 1) return launch_one<MT, 1, S, 1, 4, EP, true>(a, stream);
+      if (vp <= 2) return launch_one<MT, 1, S, 2, 4, EP, true>(a, stream);
+      if (vp <= 4) return launch_one<MT, 1, S, 4, 4, EP, true>(a, stream);
+    }
+  }
   // A 1024-thread workgroup fills a CU, so the grid should stay within one
   // round of the 256 CUs: the most lanes per column (more workgroups, fewer
   // words per lane) that still does and that divides K/16.

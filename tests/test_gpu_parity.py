@@ -353,3 +353,40 @@ def test_decode_fallback_shapes(mmf, M, K, N):
     assert np.array_equal(acc, acc_ref)
     y = run_forward(mmf, case, Wp, ws, "auto").cpu().numpy()
     compare_y(y, y_ref, acc_ref, flip)
+
+
+@pytest.mark.parametrize("M,K,N,f32", [(1, 4096, 324, False), (2, 4112, 1000, False), (1, 8192, 96, True),
+                                       (2, 5120, 15360, False), (1, 4608, 4, True)])
+def test_decode_lds_weight_staging(mmf, M, K, N, f32):
+    """Decode shapes of at most two tokens with at least 256 word rows and
+    N % 4 == 0 stage each workgroup's weight block in LDS by LDS-DMA: ragged
+    column tails (N % 64 != 0), K/16 not a multiple of 4 (the last copy group
+    reads past the array: zeros), bf16 and fp32 activations, and through the
+    affine epilogue (a bias and the three MLGRU activations)."""
+    rs = np.random.default_rng(M * 13 + K + N)
+    bits, xf, g, W = workloads.random_case(rs, M, K, N)
+    x_form = xf if f32 else bits
+    case = Case(x_form, xf, g, W, f"lds M{M}K{K}N{N}")
+    case.oracle_weights()
+    case.oracle_act()
+    acc_ref = oracle.ternary_accumulate(case.q_ref, case.t)
+    y_ref = oracle.dequant(acc_ref, case.a_ref, case.ws_ref)
+    case.upload()
+    log(f"[lds weights] M={M} K={K} N={N} f32={f32}")
+    Wp, ws = gpu_weights(mmf, case)
+    check_weights(case, Wp, ws)
+    q, a, r = gpu_act(mmf, case)
+    qn, flip_rows, _ = check_act(case, q, a, r)
+    flip = np.zeros(M, bool)
+    flip[flip_rows] = True
+    y = run_forward(mmf, case, Wp, ws, "auto").cpu().numpy()
+    compare_y(y, y_ref, acc_ref, flip)
+    # the same staging under the affine epilogue: y + b must equal the plain
+    # forward plus b, rounded once more
+    b = rs.uniform(-0.5, 0.5, N).astype(np.float32)
+    yb = torch.empty((M, N), dtype=torch.float32, device=dev())
+    mmf.mmf_bitlinear_fwd_bias(case.x_d, case.g_d, Wp, ws, torch.from_numpy(b).to(dev()), yb)
+    yp = run_forward(mmf, case, Wp, ws, "auto")
+    torch.cuda.synchronize()
+    expect = (yp.cpu().numpy().astype(np.float32) + b).astype(np.float32)
+    assert np.array_equal(yb.cpu().numpy(), expect)
