@@ -505,9 +505,14 @@ def bench_mlgru(torch, mmf, name, args):
                       device=dev)
     sws_arg = sws if mmf.mmf_mlgru_scan_workspace_bytes(w.B, w.T, d) else None
 
+    # the state alternates between two arrays (the decode step then runs the
+    # recurrence inside the output projection); a prefill carries it in place
+    h_alt = h.clone()
+
     def mixer(i):
         Wfp, wsf, Wop, wso = st["sets"][i]
-        mmf.mmf_mlgru_fwd(x, w.B, w.T, st["gamma"], Wfp, wsf, st["bias"], st["lb"], h, h,
+        h_in, h_new = (h, h_alt) if (w.T == 1 and i % 2 == 0) else ((h_alt, h) if w.T == 1 else (h, h))
+        mmf.mmf_mlgru_fwd(x, w.B, w.T, st["gamma"], Wfp, wsf, st["bias"], st["lb"], h_in, h_new,
                           st["gamma_o"], Wop, wso, st["b_o"], o, wsb)
 
     def proj(i):

@@ -35,7 +35,10 @@ constexpr int kMaxQChunks = (kDecodeMaxLdsQ / kLdsDmaChunk + kWaves - 1) / kWave
 constexpr int kWeightDelay = -1;         // < 0: all waves wait for the row waves' x
 constexpr int kGridRound = 256;           // workgroups that run at once (one per CU)
 
-enum class Src { kBf16, kF32, kQuantised };
+// kMlgru: the activations are the MLGRU's output gate o' = g sigmoid(f h +
+// (1 - f) c), formed on load from the gates fcg [M][3K] and the state h [M][K]
+// (fp32); workgroup 0 also stores the new state.
+enum class Src { kBf16, kF32, kQuantised, kMlgru };
 
 // Token rows are normalised and quantised by groups of G = min(16 / P, 4)
 // waves, P = MT rounded up to a power of two; group g owns row g and the
@@ -50,7 +53,7 @@ constexpr int row_waves() {
   return kWaves / row_groups<MT>() < kMaxRowWaves ? kWaves / row_groups<MT>() : kMaxRowWaves;
 }
 template <Src S>
-constexpr int vec_elems() { return S == Src::kF32 ? 4 : 8; }
+constexpr int vec_elems() { return (S == Src::kF32 || S == Src::kMlgru) ? 4 : 8; }
 
 struct Shared {
   int8_t* q;        // [MT][K]
@@ -106,26 +109,52 @@ template <int MT, Src S, int VP>
 struct RowStage {
   static constexpr int E = vec_elems<S>();
   static constexpr int G = row_waves<MT>();  // waves per row
+  static constexpr int VM = S == Src::kMlgru ? VP : 1;
   uint4 xr[VP];
+  uint4 xc[VM], xg[VM], xh[VM];  // kMlgru: c, g and h beside f in xr
   float4 gr[VP][E / 4];
   int row, gtid, nvec;
   bool active;
+  float* h_out;
 
-  __device__ void load(const void* xv, const float* __restrict__ gamma, int K, bool inactive_skip = false) {
+  __device__ __forceinline__ void load(const void* xv, const float* __restrict__ gamma, int K, bool inactive_skip = false,
+                       const float* h_in = nullptr, float* h_store = nullptr) {
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     row = wave / G;
     gtid = threadIdx.x - row * G * kWave;
     active = row < MT;  // waves past MT * G take no part in the row work
     nvec = K / E;
+    h_out = h_store;
     if (inactive_skip && !active) return;  // wave-uniform
     const int srow = active ? row : 0;
-    const uint4* xrow = reinterpret_cast<const uint4*>(
-        static_cast<const char*>(xv) + static_cast<int64_t>(srow) * K * (16 / E));
+    if constexpr (S == Src::kMlgru) {
+      // f, c, g of row srow side by side in fcg; h through a buffer resource
+      // of size 0 when there is no state (reads as h = 0)
+      const float* fr = static_cast<const float*>(xv) + static_cast<int64_t>(srow) * 3 * K;
+      const uint4* fv = reinterpret_cast<const uint4*>(fr);
+      const uint4* cv = reinterpret_cast<const uint4*>(fr + K);
+      const uint4* gv = reinterpret_cast<const uint4*>(fr + 2 * K);
+      const __amdgpu_buffer_rsrc_t hrsrc = __builtin_amdgcn_make_buffer_rsrc(
+          const_cast<float*>(h_in), 0, h_in != nullptr ? MT * K * 4 : 0, 0x00020000);
 #pragma unroll
-    for (int p = 0; p < VP; ++p) {
-      const int v = gtid + G * kWave * p;
-      const int sv = (active && v < nvec) ? v : 0;
-      xr[p] = xrow[sv];
+      for (int p = 0; p < VP; ++p) {
+        const int v = gtid + G * kWave * p;
+        const int sv = (active && v < nvec) ? v : 0;
+        xr[p] = fv[sv];
+        xc[p] = cv[sv];
+        xg[p] = gv[sv];
+        xh[p] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
+                                              hrsrc, static_cast<uint32_t>((srow * K + sv * E) * 4), 0, 0));
+      }
+    } else {
+      const uint4* xrow = reinterpret_cast<const uint4*>(
+          static_cast<const char*>(xv) + static_cast<int64_t>(srow) * K * (16 / E));
+#pragma unroll
+      for (int p = 0; p < VP; ++p) {
+        const int v = gtid + G * kWave * p;
+        const int sv = (active && v < nvec) ? v : 0;
+        xr[p] = xrow[sv];
+      }
     }
     // gamma through a buffer resource of size 0 when it is NULL: the loads
     // then return zeros without touching memory, and no branch separates them
@@ -146,10 +175,29 @@ struct RowStage {
   }
 
   // values of vector p as fp32 (zero outside the row)
-  __device__ void values(int p, float* f) const {
+  __device__ __forceinline__ void values(int p, float* f) const {
     const int v = gtid + G * kWave * p;
     const bool ok = active && v < nvec;
-    if constexpr (E == 8) {
+    if constexpr (S == Src::kMlgru) {
+      const float fv[4] = {__uint_as_float(xr[p].x), __uint_as_float(xr[p].y), __uint_as_float(xr[p].z),
+                           __uint_as_float(xr[p].w)};
+      const float cv[4] = {__uint_as_float(xc[p].x), __uint_as_float(xc[p].y), __uint_as_float(xc[p].z),
+                           __uint_as_float(xc[p].w)};
+      const float gv[4] = {__uint_as_float(xg[p].x), __uint_as_float(xg[p].y), __uint_as_float(xg[p].z),
+                           __uint_as_float(xg[p].w)};
+      const float hv[4] = {__uint_as_float(xh[p].x), __uint_as_float(xh[p].y), __uint_as_float(xh[p].z),
+                           __uint_as_float(xh[p].w)};
+      float hn[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        hn[e] = mlgru_step(hv[e], fv[e], cv[e]);
+        f[e] = ok ? mlgru_out_gate(gv[e], hn[e]) : 0.0f;
+      }
+      // the new state, once per call: workgroup 0 stores it
+      if (ok && h_out != nullptr && blockIdx.x == 0)
+        *reinterpret_cast<float4*>(h_out + static_cast<int64_t>(row) * (nvec * 4) + v * 4) =
+            make_float4(hn[0], hn[1], hn[2], hn[3]);
+    } else if constexpr (E == 8) {
       const uint32_t w[4] = {xr[p].x, xr[p].y, xr[p].z, xr[p].w};
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
@@ -163,7 +211,7 @@ struct RowStage {
       f[3] = ok ? __uint_as_float(xr[p].w) : 0.0f;
     }
   }
-  __device__ float gamma_at(int p, int e) const {
+  __device__ __forceinline__ float gamma_at(int p, int e) const {
     const float4 g = gr[p][e / 4];
     const int k = e % 4;
     return k == 0 ? g.x : k == 1 ? g.y : k == 2 ? g.z : g.w;
@@ -176,7 +224,7 @@ struct RowStage {
   // do the work (`active` is uniform across a wave).  The row sum of q is
   // left in the per-wave slots.
   float f[VP][E];
-  __device__ void begin(const Shared& sh) {
+  __device__ __forceinline__ void begin(const Shared& sh) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     if (active) {
 #pragma unroll
@@ -194,7 +242,7 @@ struct RowStage {
     }
   }
 
-  __device__ void finish(bool has_gamma, int K, const Shared& sh, bool first_barrier = true) {
+  __device__ __forceinline__ void finish(bool has_gamma, int K, const Shared& sh, bool first_barrier = true) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int w0 = row * G;
     if (first_barrier) __syncthreads();
@@ -319,6 +367,8 @@ struct Params {
   int K;
   int q_bytes;
   Affine affine;
+  const float* h_in;  // kMlgru
+  float* h_out;       // kMlgru
 };
 
 // The weights of a workgroup's columns are streamed in "slots": wave w owns
@@ -341,6 +391,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(const Params prm) {
   const int K = prm.K;
   const int64_t N = prm.N;
   const Shared sh = carve(smem, prm.q_bytes);
+  static_assert(S != Src::kMlgru || EP == Epilogue::kAffineF32, "the MLGRU prologue feeds the output projection");
   // read at entry: its latency then overlaps the rest of the kernel
   const float wscale = EP == Epilogue::kDequantF32 ? prm.w_scale[0] : 0.0f;
   static_assert(EP != Epilogue::kAffineF32 || S != Src::kQuantised, "affine epilogue from x only");
@@ -411,7 +462,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(const Params prm) {
   if constexpr (S == Src::kQuantised) {
     qs.load(prm.q, prm.a_scale, prm.q_rowsum, K, sh);
   } else {
-    rows.load(prm.x, prm.gamma, K, kLdsW);
+    rows.load(prm.x, prm.gamma, K, kLdsW, prm.h_in, prm.h_out);
   }
   // the factors of the column this thread writes in the affine epilogue
   // (issued after the token rows, so a wait for those leaves them in flight)
@@ -572,7 +623,7 @@ hipError_t launch_one(const DecodeArgs& a, hipStream_t stream) {
   const int region = ((MT * a.K + kLdsDmaChunk - 1) / kLdsDmaChunk) * kLdsDmaChunk;
   const dim3 grid(static_cast<unsigned>((a.N + C - 1) / C));
   const Params prm{a.Wpacked, a.x, a.gamma, a.q, a.a_scale, a.q_rowsum, a.w_scale, a.out,
-                   a.N, a.K, region, a.affine};
+                   a.N, a.K, region, a.affine, a.h_in, a.h_out};
   const int wbytes = kLdsW ? ((a.K / 16 + 3) / 4) * kLdsDmaChunk : 0;
   hipLaunchKernelGGL((decode_kernel<MT, H, S, VP, PF, EP, kLdsW>), grid, dim3(kThreads),
                      region + kScalarBytes + wbytes, stream, prm);
@@ -604,7 +655,7 @@ hipError_t dispatch_vp(const DecodeArgs& a, hipStream_t stream) {
   if constexpr (S == Src::kQuantised) {
     return dispatch_pf<MT, H, S, 1, EP>(a, stream);
   } else {
-    const int vp = needed_vp(MT, a.K, S == Src::kF32);
+    const int vp = needed_vp(MT, a.K, S == Src::kF32 || S == Src::kMlgru);
     if (vp <= 1) return dispatch_pf<MT, H, S, 1, EP>(a, stream);
     if (vp <= 2) return dispatch_pf<MT, H, S, 2, EP>(a, stream);
     if (vp <= 4) return dispatch_pf<MT, H, S, 4, EP>(a, stream);
@@ -628,7 +679,7 @@ template <int MT, Src S, Epilogue EP>
 hipError_t dispatch_h(const DecodeArgs& a, hipStream_t stream) {
   if constexpr (MT <= 2 && S != Src::kQuantised) {
     if (use_lds_weights(MT, a.K, a.N, true)) {
-      const int vp = needed_vp(MT, a.K, S == Src::kF32);
+      const int vp = needed_vp(MT, a.K, S == Src::kF32 || S == Src::kMlgru);
       if (vp <= 1) return launch_one<MT, 1, S, 1, 4, EP, true>(a, stream);
       if (vp <= 2) return launch_one<MT, 1, S, 2, 4, EP, true>(a, stream);
       if (vp <= 4) return launch_one<MT, 1, S, 4, 4, EP, true>(a, stream);
@@ -672,6 +723,7 @@ hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream) {
   const int mt = static_cast<int>(a.M);  // 1..8; the caller slices larger M
   if (a.epilogue == Epilogue::kAffineF32) {
     if (a.q != nullptr) return hipErrorInvalidValue;
+    if (a.mlgru_in) return dispatch_mt<Src::kMlgru, Epilogue::kAffineF32>(mt, a, stream);
     if (a.x_is_f32) return dispatch_mt<Src::kF32, Epilogue::kAffineF32>(mt, a, stream);
     return dispatch_mt<Src::kBf16, Epilogue::kAffineF32>(mt, a, stream);
   }

@@ -30,9 +30,6 @@ constexpr int64_t kMaxChunks = 128;
 __device__ __forceinline__ float4 ld4(const float* p) { return *reinterpret_cast<const float4*>(p); }
 __device__ __forceinline__ void st4(float* p, float4 v) { *reinterpret_cast<float4*>(p) = v; }
 
-// one step of the recurrence on one channel
-__device__ __forceinline__ float mlgru_step(float h, float f, float c) { return f * h + (1.0f - f) * c; }
-__device__ __forceinline__ float out_gate(float g, float h) { return g * sigmoid_hw(h); }
 
 struct ChunkIdx {
   int64_t b, k, i;  // sequence, chunk, first channel (multiple of 4)
@@ -182,8 +179,8 @@ __global__ __launch_bounds__(kBlock) void mlgru_apply_kernel(const float* __rest
         h.y = mlgru_step(h.y, fv[u].y, cv[u].y);
         h.z = mlgru_step(h.z, fv[u].z, cv[u].z);
         h.w = mlgru_step(h.w, fv[u].w, cv[u].w);
-        const float4 ov = {out_gate(gv[u].x, h.x), out_gate(gv[u].y, h.y), out_gate(gv[u].z, h.z),
-                           out_gate(gv[u].w, h.w)};
+        const float4 ov = {mlgru_out_gate(gv[u].x, h.x), mlgru_out_gate(gv[u].y, h.y), mlgru_out_gate(gv[u].z, h.z),
+                           mlgru_out_gate(gv[u].w, h.w)};
         st4(obase + (t + u) * d, ov);
       }
     }

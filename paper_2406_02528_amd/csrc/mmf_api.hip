@@ -618,13 +618,29 @@ int mmf_mlgru_fwd(const void* x, int x_is_f32, const float* gamma, const uint32_
     int st = run_affine(x, x_is_f32 == 1, gamma, Wfcg, w_scales, in, fcg, M, d, 3 * d,
                         scratch + s.q_off, stream);
     if (st != MMF_OK) return st;
-    if (mmf::launch_mlgru_scan(fcg, h0, op, h_last, B, T, d, reinterpret_cast<float*>(scratch + s.scan_off),
-                               stream) != hipSuccess)
-      return MMF_ERR_HIP;
     mmf::Affine out;
     out.bias = b_o;
     out.seg = d;
     out.acts = mmf::kActIdentity;
+    // A decode step (one token per sequence) with the new state in its own
+    // array: the recurrence and output gate run in the output projection's
+    // prologue (no launch, no o' round trip).  Identical arithmetic to the
+    // separate kernels, so identical results.
+    if (T == 1 && (h_last == nullptr || h_last != h0) && fused_decode(M, d, d, true)) {
+      for (int64_t m0 = 0; m0 < M; m0 += kDecodeMaxTokens) {
+        const int64_t mt = M - m0 < kDecodeMaxTokens ? M - m0 : kDecodeMaxTokens;
+        mmf::DecodeArgs a{fcg + m0 * 3 * d, true, gamma_o, nullptr, nullptr, nullptr, Wo, w_scale_o,
+                          o + m0 * d, mt, static_cast<int>(d), d, mmf::Epilogue::kAffineF32, out};
+        a.mlgru_in = true;
+        a.h_in = h0 ? h0 + m0 * d : nullptr;
+        a.h_out = h_last ? h_last + m0 * d : nullptr;
+        if (mmf::launch_decode(a, stream) != hipSuccess) return MMF_ERR_HIP;
+      }
+      return MMF_OK;
+    }
+    if (mmf::launch_mlgru_scan(fcg, h0, op, h_last, B, T, d, reinterpret_cast<float*>(scratch + s.scan_off),
+                               stream) != hipSuccess)
+      return MMF_ERR_HIP;
     return run_affine(op, true, gamma_o, Wo, w_scale_o, out, o, M, d, d, scratch + s.q_off, stream);
   });
 }

@@ -161,6 +161,15 @@ __device__ __forceinline__ float sigmoid_hw(float v) {
 }
 
 // ---------------------------------------------------------------------------
+// MLGRU recurrence step and output gate on one channel, fp32, one rounding
+// per operation (the recurrence kernels and the fused decode prologue share
+// them, so both give the same bits):
+//   h' = f h + (1 - f) c,   o' = g sigmoid(h')
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float mlgru_step(float h, float f, float c) { return f * h + (1.0f - f) * c; }
+__device__ __forceinline__ float mlgru_out_gate(float g, float h) { return g * sigmoid_hw(h); }
+
+// ---------------------------------------------------------------------------
 // Affine epilogue.  z = (float)acc * (a_scale * w_scale[s]) + bias[n] in
 // fp32, one rounding per operation, then the activation of segment s:
 // identity, (1 - lb) sigmoid(z) + lb (sigmoid with a lower bound) or

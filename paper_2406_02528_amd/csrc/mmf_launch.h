@@ -80,6 +80,13 @@ struct DecodeArgs {
   int64_t N;
   Epilogue epilogue;
   Affine affine{};          // kAffineF32 only
+  // MLGRU output projection (kAffineF32): x is the gates fcg [M][3K] and the
+  // activations are o' = g sigmoid(f h + (1 - f) c) with h = h_in [M][K]
+  // (nullptr: 0); the new state goes to h_out (nullptr: not stored), which
+  // must not be h_in (every workgroup reads all of h_in).
+  bool mlgru_in = false;
+  const float* h_in = nullptr;
+  float* h_out = nullptr;
 };
 bool decode_fits(int64_t mt, int K, int64_t N, bool from_x, bool x_is_f32);
 hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream);

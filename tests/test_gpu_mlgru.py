@@ -418,3 +418,38 @@ def test_mlgru_workloads(mmf, name):
     out = oracle.bitlinear_fwd(r["op"][rows], inp["gamma_o"], r["t_o"], r["ws_o"])
     check_bias_out(r["o"][rows], out["y"], inp["b_o"], flips(r["q_o"][rows], out["q"]),
                    a_rel(r["a_o"][rows], out["a_scale"]))
+
+
+@pytest.mark.parametrize("B,d", [(1, 2048), (5, 96), (11, 64)])
+def test_mlgru_decode_step_fused_equals_in_place(mmf, B, d):
+    """A decode step (T = 1) whose new state goes to its own array runs the
+    recurrence and output gate in the output projection's prologue; with the
+    state updated in place it runs the recurrence kernel and the plain
+    projection.  Same arithmetic: the same bits (B = 11 spans two 8-token
+    slices)."""
+    rs = np.random.default_rng(7700 + B + d)
+    bits, xf, gamma, W = workloads.random_case(rs, B, d, 3 * d)
+    Wp, w_scales, _, _ = pack_fcg(mmf, W, True)
+    Wo, wso = mmf.ternarize(T_((rs.standard_normal((d, d)) * 0.02).astype(np.float32)))
+    x_d, g_d = to_dev_x(bits), T_(gamma)
+    go = T_(rs.uniform(0.5, 1.5, d).astype(np.float32))
+    bias = T_(rs.uniform(-0.5, 0.5, 3 * d).astype(np.float32))
+    lb = T_(rs.uniform(0.0, 0.95, d).astype(np.float32))
+    b_o = T_(rs.uniform(-0.5, 0.5, d).astype(np.float32))
+    h0 = rs.standard_normal((B, d)).astype(np.float32)
+    log(f"[mlgru step] B={B} d={d}")
+    o1 = torch.empty((B, d), dtype=torch.float32, device=dev())
+    h_in, h_out = T_(h0), torch.full((B, d), float("nan"), dtype=torch.float32, device=dev())
+    mmf.mmf_mlgru_fwd(x_d, B, 1, g_d, Wp, w_scales, bias, lb, h_in, h_out, go, Wo, wso, b_o, o1)
+    o2 = torch.empty_like(o1)
+    h_ip = T_(h0)
+    mmf.mmf_mlgru_fwd(x_d, B, 1, g_d, Wp, w_scales, bias, lb, h_ip, h_ip, go, Wo, wso, b_o, o2)
+    o3 = torch.empty_like(o1)   # no state at all: h_0 = 0, nothing stored
+    mmf.mmf_mlgru_fwd(x_d, B, 1, g_d, Wp, w_scales, bias, lb, None, None, go, Wo, wso, b_o, o3)
+    o4 = torch.empty_like(o1)
+    h_zero = torch.zeros((B, d), dtype=torch.float32, device=dev())
+    mmf.mmf_mlgru_fwd(x_d, B, 1, g_d, Wp, w_scales, bias, lb, h_zero, h_zero, go, Wo, wso, b_o, o4)
+    torch.cuda.synchronize()
+    assert torch.equal(o1, o2) and torch.equal(h_out, h_ip)
+    assert torch.equal(o3, o4)
+    assert torch.equal(h_in, T_(h0))   # the fused path leaves the input state alone
