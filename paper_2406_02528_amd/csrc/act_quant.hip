@@ -33,25 +33,20 @@ template <> struct Vec<float> {
   }
 };
 
+// q of one 16-byte vector (E values) into its row: E / 4 packed words, and
+// their byte sum added to rs
 template <int E>
-__device__ __forceinline__ void store_q(int8_t* dst, const int* qi);
-template <>
-__device__ __forceinline__ void store_q<8>(int8_t* dst, const int* qi) {
-  uint2 v;
-  v.x = (qi[0] & 0xFF) | ((qi[1] & 0xFF) << 8) | ((qi[2] & 0xFF) << 16) | ((uint32_t)qi[3] << 24);
-  v.y = (qi[4] & 0xFF) | ((qi[5] & 0xFF) << 8) | ((qi[6] & 0xFF) << 16) | ((uint32_t)qi[7] << 24);
-  *reinterpret_cast<uint2*>(dst) = v;
-}
-template <>
-__device__ __forceinline__ void store_q<4>(int8_t* dst, const int* qi) {
-  uint32_t v = (qi[0] & 0xFF) | ((qi[1] & 0xFF) << 8) | ((qi[2] & 0xFF) << 16) | ((uint32_t)qi[3] << 24);
-  *reinterpret_cast<uint32_t*>(dst) = v;
-}
-
-__device__ __forceinline__ int quantise(float y, float s) {
-  float v = __builtin_rintf(y * s);  // round half to even
-  v = fminf(fmaxf(v, -128.0f), 127.0f);
-  return static_cast<int>(v);
+__device__ __forceinline__ void quantise_store(int8_t* dst, const float* y, float s, int& rs) {
+  uint32_t w[E / 4];
+#pragma unroll
+  for (int g = 0; g < E / 4; ++g) {
+    w[g] = quantise4(y + 4 * g, s);
+    rs = byte_sum4(w[g], rs);
+  }
+  if constexpr (E == 8)
+    *reinterpret_cast<uint2*>(dst) = make_uint2(w[0], w[1]);
+  else
+    *reinterpret_cast<uint32_t*>(dst) = w[0];
 }
 
 __device__ __forceinline__ float row_rstd(double ss, int K) { return rms_rstd(ss, K); }
@@ -86,10 +81,7 @@ __global__ __launch_bounds__(256) void act_quant_kernel(
         for (int e = 0; e < E; ++e) xf[i][e] = 0.0f;
       }
 #pragma unroll
-      for (int e = 0; e < E; ++e) {
-        const double d = static_cast<double>(xf[i][e]);
-        ss += d * d;  // exact product of an fp32 value in fp64
-      }
+      for (int e = 0; e < E; ++e) ss = sum_sq(ss, xf[i][e]);
     }
     ss = wave_sum_f64(ss);
     const float r = row_rstd(ss, K);
@@ -118,15 +110,7 @@ __global__ __launch_bounds__(256) void act_quant_kernel(
 #pragma unroll
     for (int i = 0; i < VPL; ++i) {
       const int v = lane + kWave * i;
-      if (v < nvec) {
-        int qi[E];
-#pragma unroll
-        for (int e = 0; e < E; ++e) {
-          qi[e] = quantise(xf[i][e], s);
-          rs += qi[e];
-        }
-        store_q<E>(qr + v * E, qi);
-      }
+      if (v < nvec) quantise_store<E>(qr + v * E, xf[i], s, rs);
     }
     rs = wave_sum_i32(rs);
     if (lane == 0) {
@@ -141,7 +125,7 @@ __global__ __launch_bounds__(256) void act_quant_kernel(
       float f[E];
       V::to_f32(xr[v], f);
 #pragma unroll
-      for (int e = 0; e < E; ++e) ss += static_cast<double>(f[e]) * static_cast<double>(f[e]);
+      for (int e = 0; e < E; ++e) ss = sum_sq(ss, f[e]);
     }
     ss = wave_sum_f64(ss);
     const float r = row_rstd(ss, K);
@@ -164,15 +148,12 @@ __global__ __launch_bounds__(256) void act_quant_kernel(
     for (int v = lane; v < nvec; v += kWave) {
       float f[E];
       V::to_f32(xr[v], f);
-      int qi[E];
 #pragma unroll
       for (int e = 0; e < E; ++e) {
-        float y = f[e] * r;
-        if (gamma != nullptr) y = y * gamma[v * E + e];
-        qi[e] = quantise(y, s);
-        rs += qi[e];
+        f[e] = f[e] * r;
+        if (gamma != nullptr) f[e] = f[e] * gamma[v * E + e];
       }
-      store_q<E>(qr + v * E, qi);
+      quantise_store<E>(qr + v * E, f, s, rs);
     }
     rs = wave_sum_i32(rs);
     if (lane == 0) {

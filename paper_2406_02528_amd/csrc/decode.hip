@@ -87,12 +87,6 @@ constexpr int kScalarBytes = sizeof(int) * kMaxTokens * kWave +
                              (sizeof(double) + sizeof(float) + sizeof(int)) * kWaves +
                              (sizeof(float) + sizeof(int)) * kMaxTokens;
 
-__device__ __forceinline__ int quantise(float y, float s) {
-  float v = __builtin_rintf(y * s);  // round half to even
-  v = fminf(fmaxf(v, -128.0f), 127.0f);
-  return static_cast<int>(v);
-}
-
 __device__ __forceinline__ void unpack_bf16x8(const uint4& r, float* f) {
   const uint32_t w[4] = {r.x, r.y, r.z, r.w};
 #pragma unroll
@@ -147,13 +141,17 @@ struct RowStage {
                                               hrsrc, static_cast<uint32_t>((srow * K + sv * E) * 4), 0, 0));
       }
     } else {
-      const uint4* xrow = reinterpret_cast<const uint4*>(
-          static_cast<const char*>(xv) + static_cast<int64_t>(srow) * K * (16 / E));
+      // the row through a buffer resource of its own K elements (size 0 for
+      // a wave without a row): vectors past its end read as zero, so the
+      // values need no mask
+      const __amdgpu_buffer_rsrc_t xrsrc = __builtin_amdgcn_make_buffer_rsrc(
+          const_cast<char*>(static_cast<const char*>(xv) + static_cast<int64_t>(srow) * K * (16 / E)), 0,
+          active ? K * (16 / E) : 0, 0x00020000);
 #pragma unroll
       for (int p = 0; p < VP; ++p) {
         const int v = gtid + G * kWave * p;
-        const int sv = (active && v < nvec) ? v : 0;
-        xr[p] = xrow[sv];
+        xr[p] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
+                                              xrsrc, static_cast<uint32_t>(v * 16), 0, 0));
       }
     }
     // gamma through a buffer resource of size 0 when it is NULL: the loads
@@ -197,18 +195,18 @@ struct RowStage {
       if (ok && h_out != nullptr && blockIdx.x == 0)
         *reinterpret_cast<float4*>(h_out + static_cast<int64_t>(row) * (nvec * 4) + v * 4) =
             make_float4(hn[0], hn[1], hn[2], hn[3]);
-    } else if constexpr (E == 8) {
+    } else if constexpr (E == 8) {  // zero past the row's end (see load)
       const uint32_t w[4] = {xr[p].x, xr[p].y, xr[p].z, xr[p].w};
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        f[2 * i] = ok ? __uint_as_float(w[i] << 16) : 0.0f;
-        f[2 * i + 1] = ok ? __uint_as_float(w[i] & 0xFFFF0000u) : 0.0f;
+        f[2 * i] = __uint_as_float(w[i] << 16);
+        f[2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
       }
     } else {
-      f[0] = ok ? __uint_as_float(xr[p].x) : 0.0f;
-      f[1] = ok ? __uint_as_float(xr[p].y) : 0.0f;
-      f[2] = ok ? __uint_as_float(xr[p].z) : 0.0f;
-      f[3] = ok ? __uint_as_float(xr[p].w) : 0.0f;
+      f[0] = __uint_as_float(xr[p].x);
+      f[1] = __uint_as_float(xr[p].y);
+      f[2] = __uint_as_float(xr[p].z);
+      f[3] = __uint_as_float(xr[p].w);
     }
   }
   __device__ __forceinline__ float gamma_at(int p, int e) const {
@@ -233,10 +231,7 @@ struct RowStage {
 #pragma unroll
       for (int p = 0; p < VP; ++p)
 #pragma unroll
-        for (int e = 0; e < E; ++e) {
-          const double d = static_cast<double>(f[p][e]);
-          ss += d * d;  // exact square of an fp32 value
-        }
+        for (int e = 0; e < E; ++e) ss = sum_sq(ss, f[p][e]);
       ss = wave_sum_f64(ss);
       if (lane == 0) sh.slot_d[wave] = ss;
     }
@@ -276,14 +271,8 @@ struct RowStage {
         uint32_t packed[E / 4];
 #pragma unroll
         for (int gq = 0; gq < E / 4; ++gq) {
-          uint32_t word = 0;
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const int qi = quantise(f[p][4 * gq + e], s);
-            rs += qi;
-            word |= (static_cast<uint32_t>(qi) & 0xFFu) << (8 * e);
-          }
-          packed[gq] = word;
+          packed[gq] = quantise4(&f[p][4 * gq], s);
+          rs = byte_sum4(packed[gq], rs);
         }
         if (v < nvec) {
           int8_t* dst = sh.q + row * K + v * E;

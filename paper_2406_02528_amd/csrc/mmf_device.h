@@ -149,6 +149,43 @@ __device__ __forceinline__ float bf16_to_f32(uint16_t b) {
 }
 
 // ---------------------------------------------------------------------------
+// Activation quantisation steps (Sec. on the BitLinear layer: per-token
+// absmax int8 quantisation).
+//
+// sum_sq(ss, f): ss + f^2 in fp64 with one fused multiply-add -- the square
+// of an fp32 value is exact in fp64, so this is the same bits as a separate
+// multiply and add.
+//
+// quantise4(y, s): q_e = round-half-even(fl(y_e s)) for four values, packed
+// little-endian into one word.  Adding 1.5 2^23 (an even integer, where the
+// fp32 spacing is 1) rounds fl(y s) to an integer with ties to even, as rint
+// does, and leaves it in two's complement in the low byte of the sum's bits.
+// With s = 127 / a and a >= max |y| the product stays within 127 (1 + 2u), so
+// q lies in [-127, 127] without a clamp.  The product and the sum are rounded
+// separately (__fmul_rn / __fadd_rn are never fused).  Inputs must be finite.
+//
+// byte_sum4(w, acc): acc + the four signed bytes of w.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ double sum_sq(double ss, float f) {
+  const double d = static_cast<double>(f);
+  return __builtin_fma(d, d, ss);
+}
+
+__device__ __forceinline__ uint32_t quantise4(const float* y, float s) {
+  constexpr float kRound = 12582912.0f;  // 1.5 * 2^23
+  uint32_t b[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) b[e] = __float_as_uint(__fadd_rn(__fmul_rn(y[e], s), kRound));
+  // v_perm_b32: selector bytes 0-3 take bytes of the second operand, 4-7 of
+  // the first, 0x0c gives zero
+  const uint32_t lo = __builtin_amdgcn_perm(b[1], b[0], 0x0c0c0400u);  // q0, q1 in bytes 0, 1
+  const uint32_t hi = __builtin_amdgcn_perm(b[3], b[2], 0x04000c0cu);  // q2, q3 in bytes 2, 3
+  return lo | hi;
+}
+
+__device__ __forceinline__ int byte_sum4(uint32_t w, int acc) { return dot4(w, 0x01010101u, acc); }
+
+// ---------------------------------------------------------------------------
 // Logistic sigmoid 1 / (1 + e^-v) from the hardware base-2 exponential and
 // reciprocal (v_exp_f32, v_rcp_f32, 1 ulp each): e^-v = 2^(-v log2 e) with
 // the argument rounded once in fp32, so the result carries a relative error
