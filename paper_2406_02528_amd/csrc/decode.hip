@@ -30,10 +30,14 @@ constexpr int kWaves = 16;
 constexpr int kThreads = kWaves * kWave;  // 1024
 constexpr int kMaxTokens = 8;
 constexpr int kMaxRowWaves = 4;           // waves that normalise one token row
+// column sums of token m at red[m * kRedStride + column]: the odd stride puts
+// the same column of different tokens on different LDS banks
+constexpr int kRedStride = kWave + 1;
 constexpr int kLdsDmaChunk = 1024;        // bytes of q one LDS-DMA wave instruction copies
 constexpr int kMaxQChunks = (kDecodeMaxLdsQ / kLdsDmaChunk + kWaves - 1) / kWaves;  // per wave
 constexpr int kWeightDelay = -1;         // < 0: all waves wait for the row waves' x
 constexpr int kGridRound = 256;           // workgroups that run at once (one per CU)
+constexpr int kMfmaMinTokens = 2;         // token counts contracted on the matrix cores
 
 // kMlgru: the activations are the MLGRU's output gate o' = g sigmoid(f h +
 // (1 - f) c), formed on load from the gates fcg [M][3K] and the state h [M][K]
@@ -56,8 +60,9 @@ template <Src S>
 constexpr int vec_elems() { return (S == Src::kF32 || S == Src::kMlgru) ? 4 : 8; }
 
 struct Shared {
-  int8_t* q;        // [MT][K]
-  int* red;         // [kMaxTokens][64] column sums (LDS atomics)
+  int8_t* q;        // [MT][q_stride]
+  int q_stride;     // bytes from one token row of q to the next
+  int* red;         // [kMaxTokens][kRedStride] column sums (LDS atomics)
   double* slot_d;   // [kWaves]
   float* slot_f;    // [kWaves]
   int* slot_i;      // [kWaves]
@@ -65,12 +70,13 @@ struct Shared {
   int* rowsum;      // [kMaxTokens]
 };
 
-__device__ __forceinline__ Shared carve(char* base, int q_bytes) {
+__device__ __forceinline__ Shared carve(char* base, int q_bytes, int q_stride) {
   Shared s;
   s.q = reinterpret_cast<int8_t*>(base);
+  s.q_stride = q_stride;
   char* p = base + q_bytes;
   s.red = reinterpret_cast<int*>(p);
-  p += sizeof(int) * kMaxTokens * kWave;
+  p += sizeof(int) * kMaxTokens * kRedStride;
   s.slot_d = reinterpret_cast<double*>(p);
   p += sizeof(double) * kWaves;
   s.slot_f = reinterpret_cast<float*>(p);
@@ -83,7 +89,7 @@ __device__ __forceinline__ Shared carve(char* base, int q_bytes) {
   return s;
 }
 
-constexpr int kScalarBytes = sizeof(int) * kMaxTokens * kWave +
+constexpr int kScalarBytes = sizeof(int) * kMaxTokens * kRedStride +
                              (sizeof(double) + sizeof(float) + sizeof(int)) * kWaves +
                              (sizeof(float) + sizeof(int)) * kMaxTokens;
 
@@ -275,7 +281,7 @@ struct RowStage {
           rs = byte_sum4(packed[gq], rs);
         }
         if (v < nvec) {
-          int8_t* dst = sh.q + row * K + v * E;
+          int8_t* dst = sh.q + row * sh.q_stride + v * E;
           if constexpr (E == 8)
             *reinterpret_cast<uint2*>(dst) = make_uint2(packed[0], packed[1]);
           else
@@ -297,6 +303,32 @@ struct RowStage {
 // operations and passed a barrier.
 constexpr int kBufferFlags = 0x00020000;  // gfx9 buffer descriptor word 3
 typedef int v4i __attribute__((ext_vector_type(4)));
+
+// F consecutive packed words (one 4-, 8- or 16-byte buffer load).
+template <int F>
+struct Words {
+  uint32_t w[F];
+};
+template <int F>
+__device__ __forceinline__ Words<F> load_words(__amdgpu_buffer_rsrc_t rsrc, uint32_t voff, uint32_t soff) {
+  Words<F> r;
+  if constexpr (F == 1) {
+    r.w[0] = __builtin_amdgcn_raw_buffer_load_b32(rsrc, voff, soff, 0);
+  } else if constexpr (F == 2) {
+    const uint2 v = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(rsrc, voff, soff, 0));
+    r.w[0] = v.x;
+    r.w[1] = v.y;
+  } else {
+    static_assert(F == 4, "one, two or four words");
+    const uint4 v = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rsrc, voff, soff, 0));
+    r.w[0] = v.x;
+    r.w[1] = v.y;
+    r.w[2] = v.z;
+    r.w[3] = v.w;
+  }
+  return r;
+}
+
 template <int MT>
 struct QStage {
   float a;
@@ -311,12 +343,17 @@ struct QStage {
     const v4i desc = {static_cast<int>(static_cast<uint32_t>(qa)), static_cast<int>((qa >> 32) & 0xFFFF), bytes,
                       kBufferFlags};
     const uint32_t lds_q = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(sh.q));
+    // with padded rows (q_stride > K, only when K % 1024 == 0) a chunk lies
+    // inside one row: chunk ch is row ch / cpr, bytes (ch % cpr) KB of it
+    const int cpr = sh.q_stride > K ? K / kLdsDmaChunk : 1;
+    const int rstride = sh.q_stride > K ? sh.q_stride : kLdsDmaChunk;
 #pragma unroll
     for (int i = 0; i < kMaxQChunks; ++i) {
       const int ch = wave + kWaves * i;
       if (ch < chunks) {  // wave-uniform
         const uint32_t off = static_cast<uint32_t>(ch * kLdsDmaChunk + lane * 16);
-        const uint32_t dst = __builtin_amdgcn_readfirstlane(lds_q + static_cast<uint32_t>(ch * kLdsDmaChunk));
+        const int lds_off = (ch / cpr) * rstride + (ch % cpr) * kLdsDmaChunk;
+        const uint32_t dst = __builtin_amdgcn_readfirstlane(lds_q + static_cast<uint32_t>(lds_off));
         asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
                      :
                      : "s"(dst), "v"(off), "s"(desc)
@@ -355,6 +392,7 @@ struct Params {
   int64_t N;
   int K;
   int q_bytes;
+  int q_stride;
   Affine affine;
   const float* h_in;  // kMlgru
   float* h_out;       // kMlgru
@@ -372,37 +410,44 @@ struct Params {
 // by the waves that do not normalise token rows (H = 1, at most 2 tokens),
 // so the norm's own LDS traffic never waits on the copies; the contraction
 // then reads the words from LDS.
-template <int MT, int H, Src S, int VP, int kPrefetch, Epilogue EP, bool kLdsW = false>
+template <int MT, int H, Src S, int VP, int kPrefetch, Epilogue EP, bool kLdsW = false, bool kMfma = false>
 __global__ __launch_bounds__(kThreads) void decode_kernel(const Params prm) {
-  static_assert(kPrefetch % 4 == 0, "prefetch goes in groups of four");
+  static_assert(kMfma || kPrefetch % 4 == 0, "prefetch goes in groups of four");
+  static_assert(!(kMfma && kLdsW), "the matrix-core contraction streams its words from memory");
   static_assert(!kLdsW || (H == 1 && MT <= 2 && S != Src::kQuantised), "LDS weight staging: H = 1, <= 2 tokens");
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const int K = prm.K;
   const int64_t N = prm.N;
-  const Shared sh = carve(smem, prm.q_bytes);
+  const Shared sh = carve(smem, prm.q_bytes, prm.q_stride);
   static_assert(S != Src::kMlgru || EP == Epilogue::kAffineF32, "the MLGRU prologue feeds the output projection");
   // read at entry: its latency then overlaps the rest of the kernel
   const float wscale = EP == Epilogue::kDequantF32 ? prm.w_scale[0] : 0.0f;
   static_assert(EP != Epilogue::kAffineF32 || S != Src::kQuantised, "affine epilogue from x only");
   constexpr int C = kWave / H;  // columns per workgroup
+  // kMfma: F = C / 16 column blocks of 16; a slot is one k64 step (4 word
+  // rows), lane (g, l16) reading word row 4 s + g of columns F l16 .. + F - 1
+  constexpr int F = C / 16;
+  constexpr int RS = kMfma ? 4 : H;  // word rows per slot
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int c = lane % C, h = lane / C;
-  const int64_t n = static_cast<int64_t>(blockIdx.x) * C + c;
+  const int l16 = lane & 15, g16 = lane >> 4;
+  const int64_t n = kMfma ? static_cast<int64_t>(blockIdx.x) * C + F * l16
+                          : static_cast<int64_t>(blockIdx.x) * C + c;
   const bool col_ok = n < N;
   const int J = K / 16;
-  const int per_wave = ((J + kWaves * H - 1) / (kWaves * H)) * H;
+  const int per_wave = ((J + kWaves * RS - 1) / (kWaves * RS)) * RS;
   const int jb = min(wave * per_wave, J);
   const int je = min(jb + per_wave, J);
-  const int ns = (je - jb) / H;  // slots of this wave (uniform)
+  const int ns = kMfma ? (je - jb + 3) / 4 : (je - jb) / H;  // slots of this wave (uniform)
   // byte offsets from Wp: packed weights are < 4 GiB
   const __amdgpu_buffer_rsrc_t wrsrc = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint32_t*>(prm.Wp), 0, static_cast<int>(static_cast<uint32_t>(J) * 4u * static_cast<uint32_t>(N)),
       kBufferFlags);
   const uint32_t row_bytes = 4u * static_cast<uint32_t>(N);
-  const uint32_t lane_off = static_cast<uint32_t>(h) * row_bytes +
+  const uint32_t lane_off = static_cast<uint32_t>(kMfma ? g16 : h) * row_bytes +
                             4u * static_cast<uint32_t>(col_ok ? n : 0);
-  const uint32_t slot_bytes = static_cast<uint32_t>(H) * row_bytes;
+  const uint32_t slot_bytes = static_cast<uint32_t>(RS) * row_bytes;
   const uint32_t wave_bytes = static_cast<uint32_t>(jb) * row_bytes;
 
   // 1. activation loads.  The waves that normalise the token rows wait for
@@ -480,8 +525,15 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(const Params prm) {
   //    without slots reads past the end of the buffer, which returns zeros
   //    without a memory access.
   uint32_t wbuf[kPrefetch];
+  Words<F> wmf[kPrefetch];
   const int last = ns > 0 ? ns - 1 : 0;
-  if constexpr (!kLdsW) {
+  if constexpr (kMfma) {
+#pragma unroll
+    for (int p = 0; p < kPrefetch; ++p) {
+      const uint32_t sp = static_cast<uint32_t>(p < last ? p : last);
+      wmf[p] = load_words<F>(wrsrc, lane_off, wave_bytes + sp * slot_bytes);
+    }
+  } else if constexpr (!kLdsW) {
 #pragma unroll
     for (int p = 0; p < kPrefetch; ++p) {
       const uint32_t sp = static_cast<uint32_t>(p < last ? p : last);
@@ -494,9 +546,9 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(const Params prm) {
   if constexpr (kLdsW) {
     constexpr int kRowThreads = row_waves<MT>() * row_groups<MT>() * kWave;
     if (tid < kRowThreads)
-      for (int i = tid; i < kMaxTokens * kWave; i += kRowThreads) sh.red[i] = 0;
+      for (int i = tid; i < kMaxTokens * kRedStride; i += kRowThreads) sh.red[i] = 0;
   } else {
-    if (tid < kMaxTokens * kWave) sh.red[tid] = 0;
+    if (tid < kMaxTokens * kRedStride) sh.red[tid] = 0;
   }
   if constexpr (S == Src::kQuantised) {
     qs.store(sh);
@@ -533,7 +585,52 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(const Params prm) {
       }
     }
   }
-  for (int base = 0; base < (kLdsW ? 0 : ns); base += kPrefetch) {
+  if constexpr (kMfma) {
+    // 16 x 16 x 64 int8 matrix-core products: the code bytes of F column
+    // blocks (first operand, rows = columns F i + f) against the token rows
+    // of q (second operand, rows l16 < MT; the others and word rows past K/16
+    // give zeros).  Lane (g, l16) ends with block f's columns F (4 g + r) + f,
+    // r < 4, of token l16.
+    v4i accf[F];
+#pragma unroll
+    for (int f = 0; f < F; ++f) accf[f] = v4i{0, 0, 0, 0};
+    const bool tok = l16 < MT;
+    const int8_t* qrow = sh.q + (tok ? l16 : 0) * sh.q_stride;
+    for (int base = 0; base < ns; base += kPrefetch) {
+      Words<F> cur[kPrefetch];
+#pragma unroll
+      for (int p = 0; p < kPrefetch; ++p) cur[p] = wmf[p];
+      const int nb = base + kPrefetch;
+      if (nb < ns) {
+#pragma unroll
+        for (int p = 0; p < kPrefetch; ++p) {
+          const uint32_t sp = static_cast<uint32_t>(nb + p < ns ? nb + p : ns - 1);
+          wmf[p] = load_words<F>(wrsrc, lane_off, wave_bytes + sp * slot_bytes);
+        }
+      }
+#pragma unroll
+      for (int p = 0; p < kPrefetch; ++p) {
+        const int j = jb + 4 * (base + p) + g16;
+        const bool ok = tok && base + p < ns && j < J;
+        const uint4 qv = *reinterpret_cast<const uint4*>(qrow + 16 * (j < J ? j : J - 1));
+        const v4i qf = ok ? __builtin_bit_cast(v4i, qv) : v4i{0, 0, 0, 0};
+#pragma unroll
+        for (int f = 0; f < F; ++f) {
+          const uint32_t w = cur[p].w[f];
+          const v4i cw = {static_cast<int>(codes4(w, 0)), static_cast<int>(codes4(w, 1)),
+                          static_cast<int>(codes4(w, 2)), static_cast<int>(codes4(w, 3))};
+          accf[f] = __builtin_amdgcn_mfma_i32_16x16x64_i8(cw, qf, accf[f], 0, 0, 0);
+        }
+      }
+    }
+    if (tok) {
+#pragma unroll
+      for (int f = 0; f < F; ++f)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) atomicAdd(&sh.red[l16 * kRedStride + F * (4 * g16 + r) + f], accf[f][r]);
+    }
+  }
+  for (int base = 0; base < ((kLdsW || kMfma) ? 0 : ns); base += kPrefetch) {
     uint32_t cur[kPrefetch];
 #pragma unroll
     for (int p = 0; p < kPrefetch; ++p) cur[p] = base + p < ns ? wbuf[p] : 0u;
@@ -577,8 +674,10 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(const Params prm) {
   }
 
   // 5. column sums over (wave, h) with LDS atomics, then dequantise
+  if constexpr (!kMfma) {
 #pragma unroll
-  for (int m = 0; m < MT; ++m) atomicAdd(&sh.red[m * kWave + c], acc[m]);
+    for (int m = 0; m < MT; ++m) atomicAdd(&sh.red[m * kRedStride + c], acc[m]);
+  }
   __syncthreads();
   if (tid < MT * C) {
     const int m = tid / C, cc = tid % C;
@@ -593,7 +692,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(const Params prm) {
       for (int w = 0; w < G; ++w) rsum += sh.slot_i[m * G + w];
     }
     if (nn < N) {
-      const int v = sh.red[m * kWave + cc] - rsum;
+      const int v = sh.red[m * kRedStride + cc] - rsum;
       if constexpr (EP == Epilogue::kDequantF32) {
         static_cast<float*>(prm.out)[m * N + nn] = static_cast<float>(v) * (sh.a_scale[m] * wscale);
       } else if constexpr (EP == Epilogue::kAffineF32) {
@@ -605,29 +704,45 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(const Params prm) {
   }
 }
 
-template <int MT, int H, Src S, int VP, int PF, Epilogue EP, bool kLdsW = false>
+// q row stride in LDS.  The matrix-core contraction reads 16 bytes of one k
+// group from each token row at once; rows padded by 16 bytes put those reads
+// on distinct banks.  Pre-quantised q is copied in whole 1 KB chunks, so it
+// is padded only when a chunk never straddles two rows (K % 1024 == 0).
+inline int q_stride_for(bool mfma, bool quantised, int K) {
+  return (mfma && (!quantised || K % kLdsDmaChunk == 0)) ? K + 16 : K;
+}
+
+template <int MT, int H, Src S, int VP, int PF, Epilogue EP, bool kLdsW = false, bool kMfma = false>
 hipError_t launch_one(const DecodeArgs& a, hipStream_t stream) {
   constexpr int C = kWave / H;
   // the q region is whole LDS-DMA chunks
-  const int region = ((MT * a.K + kLdsDmaChunk - 1) / kLdsDmaChunk) * kLdsDmaChunk;
+  const int q_stride = q_stride_for(kMfma, S == Src::kQuantised, a.K);
+  const int region = ((MT * q_stride + kLdsDmaChunk - 1) / kLdsDmaChunk) * kLdsDmaChunk;
   const dim3 grid(static_cast<unsigned>((a.N + C - 1) / C));
   const Params prm{a.Wpacked, a.x, a.gamma, a.q, a.a_scale, a.q_rowsum, a.w_scale, a.out,
-                   a.N, a.K, region, a.affine, a.h_in, a.h_out};
+                   a.N, a.K, region, q_stride, a.affine, a.h_in, a.h_out};
   const int wbytes = kLdsW ? ((a.K / 16 + 3) / 4) * kLdsDmaChunk : 0;
-  hipLaunchKernelGGL((decode_kernel<MT, H, S, VP, PF, EP, kLdsW>), grid, dim3(kThreads),
+  hipLaunchKernelGGL((decode_kernel<MT, H, S, VP, PF, EP, kLdsW, kMfma>), grid, dim3(kThreads),
                      region + kScalarBytes + wbytes, stream, prm);
   return hipGetLastError();
 }
 
 // Weight words in flight per lane: a wave's whole range when it holds at most
 // four slots, else eight at a time (measured: deeper prefetch only delays
-// the loads of the waves that also normalise the token rows).
-template <int MT, int H, Src S, int VP, Epilogue EP>
+// the loads of the waves that also normalise the token rows).  Matrix-core
+// contraction: slots are k64 steps of F words each, two or four in flight.
+template <int MT, int H, Src S, int VP, Epilogue EP, bool kMfma>
 hipError_t dispatch_pf(const DecodeArgs& a, hipStream_t stream) {
   const int J = a.K / 16;
-  const int slots = (J + kWaves * H - 1) / (kWaves * H);
-  if (slots <= 4) return launch_one<MT, H, S, VP, 4, EP>(a, stream);
-  return launch_one<MT, H, S, VP, 8, EP>(a, stream);
+  if constexpr (kMfma) {
+    const int steps = (J + kWaves * 4 - 1) / (kWaves * 4);
+    if (steps <= 2) return launch_one<MT, H, S, VP, 2, EP, false, true>(a, stream);
+    return launch_one<MT, H, S, VP, 4, EP, false, true>(a, stream);
+  } else {
+    const int slots = (J + kWaves * H - 1) / (kWaves * H);
+    if (slots <= 4) return launch_one<MT, H, S, VP, 4, EP>(a, stream);
+    return launch_one<MT, H, S, VP, 8, EP>(a, stream);
+  }
 }
 
 // vectors of 16 bytes per thread a row needs: ceil(K / E / (G * 64))
@@ -639,15 +754,15 @@ inline int needed_vp(int64_t mt, int K, bool f32) {
   return static_cast<int>((nvec + lanes - 1) / lanes);
 }
 
-template <int MT, int H, Src S, Epilogue EP>
+template <int MT, int H, Src S, Epilogue EP, bool kMfma = false>
 hipError_t dispatch_vp(const DecodeArgs& a, hipStream_t stream) {
   if constexpr (S == Src::kQuantised) {
-    return dispatch_pf<MT, H, S, 1, EP>(a, stream);
+    return dispatch_pf<MT, H, S, 1, EP, kMfma>(a, stream);
   } else {
     const int vp = needed_vp(MT, a.K, S == Src::kF32 || S == Src::kMlgru);
-    if (vp <= 1) return dispatch_pf<MT, H, S, 1, EP>(a, stream);
-    if (vp <= 2) return dispatch_pf<MT, H, S, 2, EP>(a, stream);
-    if (vp <= 4) return dispatch_pf<MT, H, S, 4, EP>(a, stream);
+    if (vp <= 1) return dispatch_pf<MT, H, S, 1, EP, kMfma>(a, stream);
+    if (vp <= 2) return dispatch_pf<MT, H, S, 2, EP, kMfma>(a, stream);
+    if (vp <= 4) return dispatch_pf<MT, H, S, 4, EP, kMfma>(a, stream);
     return hipErrorInvalidValue;  // excluded by decode_fits
   }
 }
@@ -673,6 +788,20 @@ hipError_t dispatch_h(const DecodeArgs& a, hipStream_t stream) {
       if (vp <= 2) return launch_one<MT, 1, S, 2, 4, EP, true>(a, stream);
       if (vp <= 4) return launch_one<MT, 1, S, 4, 4, EP, true>(a, stream);
     }
+  }
+  // Two or more tokens: the matrix cores.  Each packed word (16 weights)
+  // costs 4 MT v_dot4 on the vector ALU, and at 8 tokens that work alone
+  // takes longer than streaming the weights; one 16x16x64 MFMA covers four
+  // words of 16 columns for 16 token rows.  Column blocks per workgroup: as few as
+  // keep the grid within one round of the CUs, with loads aligned to their
+  // width (N % F == 0).
+  if constexpr (MT >= kMfmaMinTokens) {
+    const int64_t N = a.N;
+    if ((N + 15) / 16 <= kGridRound) return dispatch_vp<MT, 4, S, EP, true>(a, stream);
+    if (N % 2 == 0 && ((N + 31) / 32 <= kGridRound || N % 4 != 0))
+      return dispatch_vp<MT, 2, S, EP, true>(a, stream);
+    if (N % 4 == 0) return dispatch_vp<MT, 1, S, EP, true>(a, stream);
+    return dispatch_vp<MT, 4, S, EP, true>(a, stream);
   }
   // A 1024-thread workgroup fills a CU, so the grid should stay within one
   // round of the 256 CUs: the most lanes per column (more workgroups, fewer

@@ -390,3 +390,44 @@ def test_decode_lds_weight_staging(mmf, M, K, N, f32):
     torch.cuda.synchronize()
     expect = (yp.cpu().numpy().astype(np.float32) + b).astype(np.float32)
     assert np.array_equal(yb.cpu().numpy(), expect)
+
+
+@pytest.mark.parametrize("M,K,N,f32", [(4, 1040, 9000, False), (3, 2048, 8194, False), (3, 8192, 2000, False),
+                                       (5, 1024, 1000, True), (8, 4096, 640, False), (2, 2064, 6146, True)])
+def test_decode_matrix_core_layouts(mmf, M, K, N, f32):
+    """Two to eight tokens are contracted on the matrix cores inside the fused
+    decode kernel.  Column blocks of 16 per workgroup: four with 16-byte
+    weight loads (N = 9000), two (N = 6146), two because N % 4 != 0 although
+    the grid then exceeds one round of CUs (N = 8194), one (the rest).  K/16
+    not a multiple of 4 (the last k64 step masks its missing word rows, and
+    waves past K/16 hold no step), more k64 steps per wave than are in flight
+    at once (K = 8192), the largest bf16 row set (8 x 4096), fp32
+    activations; the integer hook from pre-quantised q (padded LDS rows when
+    K % 1024 == 0, unpadded otherwise) and the affine epilogue (N % 4 == 0)."""
+    rs = np.random.default_rng(M * 31 + K + N)
+    bits, xf, g, W = workloads.random_case(rs, M, K, N)
+    x_form = xf if f32 else bits
+    case = Case(x_form, xf, g, W, f"mfma M{M}K{K}N{N}")
+    case.oracle_weights()
+    case.oracle_act()
+    acc_ref = oracle.ternary_accumulate(case.q_ref, case.t)
+    y_ref = oracle.dequant(acc_ref, case.a_ref, case.ws_ref)
+    case.upload()
+    log(f"[decode mfma] M={M} K={K} N={N} f32={f32}")
+    Wp, ws = gpu_weights(mmf, case)
+    check_weights(case, Wp, ws)
+    q, a, r = gpu_act(mmf, case)
+    qn, flip_rows, _ = check_act(case, q, a, r)
+    flip = np.zeros(M, bool)
+    flip[flip_rows] = True
+    acc = run_i32(mmf, torch.from_numpy(case.q_ref).to(dev()), Wp, M, N, "auto").cpu().numpy()
+    assert np.array_equal(acc, acc_ref)
+    y = run_forward(mmf, case, Wp, ws, "auto").cpu().numpy()
+    compare_y(y, y_ref, acc_ref, flip)
+    if N % 4 == 0:  # the entry point with a bias takes N % 4 == 0 only
+        b = rs.uniform(-0.5, 0.5, N).astype(np.float32)
+        yb = torch.empty((M, N), dtype=torch.float32, device=dev())
+        mmf.mmf_bitlinear_fwd_bias(case.x_d, case.g_d, Wp, ws, torch.from_numpy(b).to(dev()), yb)
+        torch.cuda.synchronize()
+        expect = (y.astype(np.float32) + b).astype(np.float32)
+        assert np.array_equal(yb.cpu().numpy(), expect)
