@@ -7,14 +7,18 @@
 // the code c = t + 1 in {0,1,2}; the epilogue subtracts sum_k q (sum q*t =
 // sum q*c - sum q) and dequantises.
 //
-// Tiling: a workgroup of 8 waves computes a 256 x 256 output tile; wave
-// (wm, wn) owns a 128 x 64 block as 8 x 4 MFMA tiles of 16 x 16.  Each
-// expanded weight fragment therefore feeds eight MFMAs, which keeps the VALU
-// work of the 2-bit expansion small against the matrix work.
+// Tiling: a workgroup of 8 waves computes a 128 x 512 output tile (256 x 256
+// when N % 4 != 0); wave (wm, wn) owns a 128 x 64 block as 8 x 4 MFMA tiles
+// of 16 x 16.  Each expanded weight fragment therefore feeds eight MFMAs,
+// which keeps the VALU work of the 2-bit expansion small against the matrix
+// work.  The wide tile moves fewer operand bytes per MAC into LDS than a
+// square one (the int8 rows of q are the heavy operand, the 2-bit weight
+// columns the light one): 32 KB per 128-deep stage for 128 x 512 against
+// 40 KB for 256 x 256, and the global->LDS copies are what limits the loop.
 //
 // Operands and pipeline:
 //  - The operands of one BK = 128 deep k stage stream through a 3-slot LDS
-//    ring: A (q, int8 [M][K]) as 256 rows of 128 bytes, B as 8 rows of 256
+//    ring: A (q, int8 [M][K]) as BM rows of 128 bytes, B as 8 rows of BN
 //    packed words.  The global->LDS copies are LDS-DMA buffer loads (the data
 //    goes from the memory pipeline straight into LDS, not through registers).
 //  - The copies of a stage are issued one per group of MFMAs through the step
@@ -145,19 +149,20 @@ __global__ __launch_bounds__((Tiling<BM, BN, WM, WN, BK, S, BX4>::kThreads)) voi
     a_chunk[i] = c * 16;
     a_src[i] = static_cast<uint32_t>(m0 + r) * static_cast<uint32_t>(K) + static_cast<uint32_t>(c * 16);
   }
-  // B instruction i: word row jj, columns of this tile.  Columns past N read
-  // the next word row or zero; their outputs are dropped.
+  // B instruction i: word row jj, a 256-word (BX4) or 64-word chunk of this
+  // tile's columns.  Columns past N read the next word row or zero; their
+  // outputs are dropped.
   uint32_t b_src[T::kBPerWave];
   int b_jj[T::kBPerWave], b_dst[T::kBPerWave];
 #pragma unroll
   for (int i = 0; i < T::kBPerWave; ++i) {
     const int idx = wave * T::kBPerWave + i;
     if constexpr (BX4) {
-      const int jj = idx;
+      const int jj = idx / (BN / 256), q256 = idx % (BN / 256);
       b_jj[i] = jj;
-      b_dst[i] = jj * T::kBRow * 4;
+      b_dst[i] = jj * T::kBRow * 4 + q256 * 1024;
       b_src[i] = 4u * (static_cast<uint32_t>(jj) * static_cast<uint32_t>(N) +
-                       static_cast<uint32_t>(n0 + 4 * lane));
+                       static_cast<uint32_t>(n0 + q256 * 256 + 4 * lane));
     } else {
       const int jj = idx / (BN / 64), q64 = idx % (BN / 64);
       b_jj[i] = jj;
@@ -242,11 +247,11 @@ __global__ __launch_bounds__((Tiling<BM, BN, WM, WN, BK, S, BX4>::kThreads)) voi
   };
 
   // The tile's per-row dequantisation inputs (q_rowsum, then a_scale) go
-  // into LDS by LDS-DMA too, one 64-row chunk per wave, ahead of the ring's
+  // into LDS by LDS-DMA too, one 64-row chunk per wave (2 BM / 64 waves), ahead of the ring's
   // first stages, so the prologue's wait covers them and the epilogue finds
   // them there.  Rows past M read zero.
-  {
-    static_assert(2 * BM == 64 * T::kWaves, "one row-factor chunk per wave");
+  if (wave < 2 * BM / 64) {  // wave-uniform
+    static_assert(2 * BM <= 64 * T::kWaves, "one row-factor chunk per wave");
     const int arr = wave / (BM / 64), chunk = wave % (BM / 64);
     const int row = m0 + chunk * 64 + lane;
     const uint32_t off = row < M ? 4u * static_cast<uint32_t>(row) : 0x80000000u;
@@ -461,7 +466,7 @@ hipError_t launch_gemm(const ContractArgs& a, hipStream_t stream) {
   const bool bx4 = (a.N % 4) == 0;
   for (int64_t m0 = 0; m0 < a.M; m0 += slice) {
     const int64_t rows = a.M - m0 < slice ? a.M - m0 : slice;
-    const hipError_t e = bx4 ? launch_cfg<256, 256, 128, 64, 128, 3, true>(a, m0, rows, stream)
+    const hipError_t e = bx4 ? launch_cfg<128, 512, 128, 64, 128, 3, true>(a, m0, rows, stream)
                              : launch_cfg<256, 256, 128, 64, 128, 3, false>(a, m0, rows, stream);
     if (e != hipSuccess) return e;
   }
