@@ -10,6 +10,7 @@ namespace mmf {
 namespace {
 
 constexpr int kRowsPerBlock = 4;  // 4 waves, one row each
+constexpr int kBufferFlags = 0x00020000;  // gfx9 buffer descriptor word 3
 
 // 16-byte vector of activations: 8 bf16 or 4 fp32.
 template <typename XT> struct Vec;
@@ -69,17 +70,33 @@ __global__ __launch_bounds__(256) void act_quant_kernel(
   int8_t* qr = q + row * K;
 
   if constexpr (VPL > 0) {
+    // Every load of the row and of gamma is issued at once, without branches:
+    // both go through buffer resources of the row's (gamma's) size, so the
+    // vectors past the row's end read as zero (and gamma == NULL as a
+    // resource of size 0).  Guarded loads would each wait for the last.
+    const __amdgpu_buffer_rsrc_t xrsrc = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<XT*>(x + row * K), 0, static_cast<int>(K * sizeof(XT)), kBufferFlags);
+    const __amdgpu_buffer_rsrc_t grsrc = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float*>(gamma), 0, gamma != nullptr ? K * 4 : 0, kBufferFlags);
+    typename V::Raw raw[VPL];
+    float4 gv[VPL][E / 4];
+#pragma unroll
+    for (int i = 0; i < VPL; ++i)
+      raw[i] = __builtin_bit_cast(typename V::Raw, __builtin_amdgcn_raw_buffer_load_b128(
+                                                       xrsrc, static_cast<uint32_t>((lane + kWave * i) * 16), 0, 0));
+#pragma unroll
+    for (int i = 0; i < VPL; ++i)
+#pragma unroll
+      for (int e4 = 0; e4 < E / 4; ++e4)
+        gv[i][e4] = __builtin_bit_cast(
+            float4, __builtin_amdgcn_raw_buffer_load_b128(
+                        grsrc, static_cast<uint32_t>(((lane + kWave * i) * E + 4 * e4) * 4), 0, 0));
+    __builtin_amdgcn_sched_barrier(0);  // all loads before the first wait
     float xf[VPL][E];
     double ss = 0.0;
 #pragma unroll
     for (int i = 0; i < VPL; ++i) {
-      const int v = lane + kWave * i;
-      if (v < nvec) {
-        V::to_f32(xr[v], xf[i]);
-      } else {
-#pragma unroll
-        for (int e = 0; e < E; ++e) xf[i][e] = 0.0f;
-      }
+      V::to_f32(raw[i], xf[i]);  // zero past the row's end
 #pragma unroll
       for (int e = 0; e < E; ++e) ss = sum_sq(ss, xf[i][e]);
     }
@@ -89,19 +106,20 @@ __global__ __launch_bounds__(256) void act_quant_kernel(
     float amax = 0.0f;
 #pragma unroll
     for (int i = 0; i < VPL; ++i) {
-      const int v = lane + kWave * i;
-      if (v < nvec) {
-        if (gamma != nullptr) {
-          const float* g = gamma + v * E;
+      if (gamma != nullptr) {  // uniform
 #pragma unroll
-          for (int e = 0; e < E; ++e) xf[i][e] = (xf[i][e] * r) * g[e];
-        } else {
-#pragma unroll
-          for (int e = 0; e < E; ++e) xf[i][e] = xf[i][e] * r;
+        for (int e4 = 0; e4 < E / 4; ++e4) {
+          xf[i][4 * e4 + 0] = (xf[i][4 * e4 + 0] * r) * gv[i][e4].x;
+          xf[i][4 * e4 + 1] = (xf[i][4 * e4 + 1] * r) * gv[i][e4].y;
+          xf[i][4 * e4 + 2] = (xf[i][4 * e4 + 2] * r) * gv[i][e4].z;
+          xf[i][4 * e4 + 3] = (xf[i][4 * e4 + 3] * r) * gv[i][e4].w;
         }
+      } else {
 #pragma unroll
-        for (int e = 0; e < E; ++e) amax = fmaxf(amax, fabsf(xf[i][e]));
+        for (int e = 0; e < E; ++e) xf[i][e] = xf[i][e] * r;
       }
+#pragma unroll
+      for (int e = 0; e < E; ++e) amax = fmaxf(amax, fabsf(xf[i][e]));
     }
     amax = fmaxf(wave_max_f32(amax), 1e-5f);
     const float s = 127.0f / amax;
