@@ -86,6 +86,30 @@ __device__ __forceinline__ void load_x4(const float* x, float* f) {
   f[0] = v.x; f[1] = v.y; f[2] = v.z; f[3] = v.w;
 }
 
+// four activations from a buffer resource (zero past its range): the raw
+// words, then their fp32 values
+constexpr int kBufFlags = 0x00020000;  // gfx9 buffer descriptor word 3
+template <typename XT> struct Raw4;
+template <> struct Raw4<uint16_t> {
+  uint2 v;
+  __device__ void load(__amdgpu_buffer_rsrc_t rs, uint32_t k) {
+    v = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(rs, 2u * k, 0, 0));
+  }
+  __device__ void to_f32(float* f) const {
+    f[0] = __uint_as_float(v.x << 16);
+    f[1] = __uint_as_float(v.x & 0xFFFF0000u);
+    f[2] = __uint_as_float(v.y << 16);
+    f[3] = __uint_as_float(v.y & 0xFFFF0000u);
+  }
+};
+template <> struct Raw4<float> {
+  float4 v;
+  __device__ void load(__amdgpu_buffer_rsrc_t rs, uint32_t k) {
+    v = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(rs, 4u * k, 0, 0));
+  }
+  __device__ void to_f32(float* f) const { f[0] = v.x; f[1] = v.y; f[2] = v.z; f[3] = v.w; }
+};
+
 // One wave per row: s = sum_k g_k x_k in fp64 over the row, then
 // dx = r g - coef x with coef = r^3 s / K (rounded from fp64 once).  VPL > 0:
 // the lane keeps its VPL groups of 4 (g and x) in registers between the two
@@ -122,15 +146,38 @@ __global__ __launch_bounds__(kBlock) void rms_norm_bwd_kernel(const float* __res
   };
   double s = 0.0;
   if constexpr (VPL > 0) {
+    // every load of the lane issued at entry, without a branch: dY, x and
+    // gamma through buffer resources of the row's size (gamma's: 0 when it
+    // is NULL), which read as zero past their ends
+    const __amdgpu_buffer_rsrc_t drs =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(dr), 0, K * 4, kBufFlags);
+    const __amdgpu_buffer_rsrc_t xrs =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<XT*>(xr), 0, K * static_cast<int>(sizeof(XT)), kBufFlags);
+    const __amdgpu_buffer_rsrc_t grs =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(gamma), 0, gamma != nullptr ? K * 4 : 0, kBufFlags);
+    float4 dv[VPL], gv[VPL];
+    Raw4<XT> xv[VPL];
     float g[VPL][4], xf[VPL][4];
 #pragma unroll
     for (int i = 0; i < VPL; ++i) {
-      const int k = 4 * (lane + kWave * i);
-      if (k < K) {
-        load_gx(k, g[i], xf[i]);
+      const uint32_t k = 4u * static_cast<uint32_t>(lane + kWave * i);
+      dv[i] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(drs, 4u * k, 0, 0));
+      xv[i].load(xrs, k);
+      gv[i] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(grs, 4u * k, 0, 0));
+    }
+    __builtin_amdgcn_sched_barrier(0);  // all loads before the first wait
 #pragma unroll
-        for (int e = 0; e < 4; ++e) s += static_cast<double>(g[i][e]) * static_cast<double>(xf[i][e]);
+    for (int i = 0; i < VPL; ++i) {
+      xv[i].to_f32(xf[i]);
+      const float d4[4] = {dv[i].x, dv[i].y, dv[i].z, dv[i].w};
+      const float g4[4] = {gv[i].x, gv[i].y, gv[i].z, gv[i].w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float dy = w * d4[e];
+        g[i][e] = gamma != nullptr ? g4[e] * dy : dy;
       }
+#pragma unroll
+      for (int e = 0; e < 4; ++e) s += static_cast<double>(g[i][e]) * static_cast<double>(xf[i][e]);
     }
     s = wave_sum_f64(s);
     const double rd = static_cast<double>(r);
