@@ -115,7 +115,8 @@ int mmf_act_quant_f32(const float *x, const float *gamma, int8_t *q,
  *   y[m][n] = a_scale[m] * w_scale * sum_k q[m][k] t[n][k]
  * with q, a_scale from the act-quant step above and t from Wpacked.  The
  * integer sum is exact; the product is fp32 (a_scale[m] * w_scale first).
- * Tokens M <= 8 take the decode kernel (VALU dot products), larger M the
+ * Tokens M <= 8 take the decode kernel (VALU dot products for one token,
+ * 16x16x64 int8 MFMA for two to eight), larger M the
  * int8 MFMA kernel.  Allocates its M*K + 8*M byte scratch stream-ordered
  * (hipMallocAsync); mmf_bitlinear_fwd_ws takes caller scratch instead.
  * x: [M][K] bf16 bits; gamma: [K] or NULL; Wpacked: [K/16][N]; w_scale: [1];

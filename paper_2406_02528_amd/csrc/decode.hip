@@ -16,10 +16,13 @@
 // All of these loads are straight-line (clamped addresses, masked values), so
 // the compiler can keep them in flight together.
 //
-// Per word of 16 weights and per token: four v_dot4_i32_i8 of the codes
-// c = t + 1 against q (one broadcast ds_read_b128); the epilogue subtracts
-// sum_k q, giving the ternary sum of the paper (+q where t = 1, -q where
-// t = -1, nothing where t = 0), and dequantises.
+// One token: per word of 16 weights, four v_dot4_i32_i8 of the codes
+// c = t + 1 against q (one broadcast ds_read_b128).  Two to eight tokens:
+// v_mfma_i32_16x16x64_i8 over the same codes, 16 columns by the token rows of
+// q (the vector ALU's dot4 rate would fall behind the weight stream at eight
+// tokens).  Either way the epilogue subtracts sum_k q, giving the ternary sum
+// of the paper (+q where t = 1, -q where t = -1, nothing where t = 0), and
+// dequantises.
 #include "mmf_device.h"
 #include "mmf_launch.h"
 
