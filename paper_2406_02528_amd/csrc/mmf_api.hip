@@ -42,11 +42,17 @@ FwdScratch fwd_scratch(int64_t M, int64_t K) {
   return s;
 }
 
+// Automatic choice: up to kDecodeSliceMaxTokens tokens run as decode launches
+// of at most 8 tokens each.  Measured (K = 2048, N = 2048 / 6144 / 11264): the
+// MFMA kernel takes >= 26 us at any small M (each output tile's k loop runs
+// on one CU), the decode slices ~5 us each, so the slices win up to ~44
+// tokens (M = 16: 9.9 vs 26.3 us; M = 32: 19.5 vs 27.3; M = 48: 29.2 vs 28.1).
+constexpr int64_t kDecodeSliceMaxTokens = 40;
 bool use_gemv(int64_t M) {
   const int p = g_path.load(std::memory_order_relaxed);
   if (p == MMF_PATH_GEMV) return true;
   if (p == MMF_PATH_GEMM) return false;
-  return M <= kDecodeMaxTokens;
+  return M <= kDecodeSliceMaxTokens;
 }
 
 // Contraction from quantised activations.  Decode-sized slices of at most 8
