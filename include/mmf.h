@@ -195,7 +195,9 @@ int mmf_ternary_gemm_i32(const int8_t *q, const uint32_t *Wpacked,
  *
  * mmf_glu_fwd: x [M][K] bf16 bits (mmf_glu_fwd_f32: float32); gamma [K] or
  * NULL; Wgu_packed [K/16][2L] from mmf_glu_pack; w_scales [2] = gate, up;
- * p [M][L] float32 out.  Every M runs the int8 MFMA kernel.  Allocates the
+ * p [M][L] float32 out.  Up to 40 tokens run the fused decode kernel with
+ * the same SiLU(g) * u epilogue (launches of at most 8 tokens; the result is
+ * bit-identical to the MFMA kernel's), larger M the int8 MFMA kernel.  Allocates the
  * same stream-ordered scratch as mmf_bitlinear_fwd; mmf_glu_fwd_ws takes
  * caller scratch of mmf_bitlinear_workspace_bytes(M, K) bytes instead.
  */

@@ -424,9 +424,12 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(const Params prm) {
   const Shared sh = carve(smem, prm.q_bytes, prm.q_stride);
   static_assert(S != Src::kMlgru || EP == Epilogue::kAffineF32, "the MLGRU prologue feeds the output projection");
   // read at entry: its latency then overlaps the rest of the kernel
-  const float wscale = EP == Epilogue::kDequantF32 ? prm.w_scale[0] : 0.0f;
+  const float wscale = (EP == Epilogue::kDequantF32 || EP == Epilogue::kGluF32) ? prm.w_scale[0] : 0.0f;
+  const float wscale_u = EP == Epilogue::kGluF32 ? prm.w_scale[1] : 0.0f;
   static_assert(EP != Epilogue::kAffineF32 || S != Src::kQuantised, "affine epilogue from x only");
   constexpr int C = kWave / H;  // columns per workgroup
+  static_assert(EP != Epilogue::kGluF32 || (C >= 32 && S != Src::kQuantised && S != Src::kMlgru),
+                "GLU output: whole gate/up block pairs per workgroup, activations from x");
   // kMfma: F = C / 16 column blocks of 16; a slot is one k64 step (4 word
   // rows), lane (g, l16) reading word row 4 s + g of columns F l16 .. + F - 1
   constexpr int F = C / 16;
@@ -682,7 +685,29 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(const Params prm) {
     for (int m = 0; m < MT; ++m) atomicAdd(&sh.red[m * kRedStride + c], acc[m]);
   }
   __syncthreads();
-  if (tid < MT * C) {
+  if constexpr (EP == Epilogue::kGluF32) {
+    // The packed columns alternate 16 gate and 16 up columns, and a
+    // workgroup's C columns are C / 32 whole pairs: thread (m, channel) forms
+    // SiLU(g) * u of its channel (the formula and order of the MFMA kernel's
+    // GLU epilogue, so both give the same bits) into the L = N / 2 wide output.
+    constexpr int kHalf = C / 2;
+    if (tid < MT * kHalf) {
+      const int m = tid / kHalf, hc = tid % kHalf;
+      const int cg = (hc / 16) * 32 + hc % 16;  // gate column; up column cg + 16
+      const int64_t L = N / 2;
+      const int64_t ch = static_cast<int64_t>(blockIdx.x) * kHalf + hc;
+      constexpr int G = row_waves<MT>();
+      int rsum = 0;
+#pragma unroll
+      for (int w = 0; w < G; ++w) rsum += sh.slot_i[m * G + w];
+      if (ch < L) {
+        const float sg = sh.a_scale[m] * wscale, su = sh.a_scale[m] * wscale_u;
+        const float gv = static_cast<float>(sh.red[m * kRedStride + cg] - rsum) * sg;
+        const float uv = static_cast<float>(sh.red[m * kRedStride + cg + 16] - rsum) * su;
+        static_cast<float*>(prm.out)[m * L + ch] = gv * sigmoid_hw(gv) * uv;
+      }
+    }
+  } else if (tid < MT * C) {
     const int m = tid / C, cc = tid % C;
     const int64_t nn = static_cast<int64_t>(blockIdx.x) * C + cc;
     int rsum;
@@ -798,19 +823,25 @@ hipError_t dispatch_h(const DecodeArgs& a, hipStream_t stream) {
   // words of 16 columns for 16 token rows.  Column blocks per workgroup: as few as
   // keep the grid within one round of the CUs, with loads aligned to their
   // width (N % F == 0).
+  constexpr bool kGlu = EP == Epilogue::kGluF32;  // needs C >= 32 (N % 32 == 0)
   if constexpr (MT >= kMfmaMinTokens) {
     const int64_t N = a.N;
-    if ((N + 15) / 16 <= kGridRound) return dispatch_vp<MT, 4, S, EP, true>(a, stream);
+    if constexpr (!kGlu) {
+      if ((N + 15) / 16 <= kGridRound) return dispatch_vp<MT, 4, S, EP, true>(a, stream);
+    }
     if (N % 2 == 0 && ((N + 31) / 32 <= kGridRound || N % 4 != 0))
       return dispatch_vp<MT, 2, S, EP, true>(a, stream);
     if (N % 4 == 0) return dispatch_vp<MT, 1, S, EP, true>(a, stream);
-    return dispatch_vp<MT, 4, S, EP, true>(a, stream);
+    if constexpr (!kGlu) return dispatch_vp<MT, 4, S, EP, true>(a, stream);
+    return hipErrorInvalidValue;
   }
   // A 1024-thread workgroup fills a CU, so the grid should stay within one
   // round of the 256 CUs: the most lanes per column (more workgroups, fewer
   // words per lane) that still does and that divides K/16.
   const int J = a.K / 16;
-  if (J % 4 == 0 && (a.N + 15) / 16 <= kGridRound) return dispatch_vp<MT, 4, S, EP>(a, stream);
+  if constexpr (!kGlu) {
+    if (J % 4 == 0 && (a.N + 15) / 16 <= kGridRound) return dispatch_vp<MT, 4, S, EP>(a, stream);
+  }
   if (J % 2 == 0 && (a.N + 31) / 32 <= kGridRound) return dispatch_vp<MT, 2, S, EP>(a, stream);
   return dispatch_vp<MT, 1, S, EP>(a, stream);
 }
@@ -842,6 +873,11 @@ bool decode_fits(int64_t mt, int K, int64_t N, bool from_x, bool x_is_f32) {
 
 hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream) {
   const int mt = static_cast<int>(a.M);  // 1..8; the caller slices larger M
+  if (a.epilogue == Epilogue::kGluF32) {
+    if (a.q != nullptr || a.mlgru_in || a.N % 32 != 0) return hipErrorInvalidValue;
+    if (a.x_is_f32) return dispatch_mt<Src::kF32, Epilogue::kGluF32>(mt, a, stream);
+    return dispatch_mt<Src::kBf16, Epilogue::kGluF32>(mt, a, stream);
+  }
   if (a.epilogue == Epilogue::kAffineF32) {
     if (a.q != nullptr) return hipErrorInvalidValue;
     if (a.mlgru_in) return dispatch_mt<Src::kMlgru, Epilogue::kAffineF32>(mt, a, stream);

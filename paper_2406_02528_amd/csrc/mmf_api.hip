@@ -162,8 +162,8 @@ int act_quant_common(const void* x, bool x_is_f32, const float* gamma, int8_t* q
 }
 
 // GLU (gated up-projection): x -> RMSNorm + quantisation -> the interleaved
-// gate/up contraction with the SiLU(g) * u epilogue.  Any M runs on the MFMA
-// kernel.
+// gate/up contraction with the SiLU(g) * u epilogue: fused decode launches for
+// the token counts the decode kernel takes, the MFMA kernel otherwise.
 int check_glu(const void* x, const float* gamma, const uint32_t* Wgu, const float* w_scales,
               const float* p, int64_t M, int64_t K, int64_t L) {
   if (L < 0 || L > kMaxMN / 2 || (L % 16) != 0) return MMF_ERR_SHAPE;
@@ -178,6 +178,18 @@ int check_glu(const void* x, const float* gamma, const uint32_t* Wgu, const floa
 int run_glu(const void* x, bool x_is_f32, const float* gamma, const uint32_t* Wgu,
             const float* w_scales, float* p, int64_t M, int64_t K, int64_t L, char* scratch,
             hipStream_t stream) {
+  // few tokens: fused decode launches with the GLU epilogue (no scratch)
+  if (fused_decode(M, K, 2 * L, x_is_f32)) {
+    const size_t xsz = x_is_f32 ? 4 : 2;
+    for (int64_t m0 = 0; m0 < M; m0 += kDecodeMaxTokens) {
+      const int64_t mt = M - m0 < kDecodeMaxTokens ? M - m0 : kDecodeMaxTokens;
+      mmf::DecodeArgs d{static_cast<const char*>(x) + m0 * K * xsz, x_is_f32, gamma, nullptr,
+                        nullptr, nullptr, Wgu, w_scales, p + m0 * L, mt,
+                        static_cast<int>(K), 2 * L, mmf::Epilogue::kGluF32};
+      if (mmf::launch_decode(d, stream) != hipSuccess) return MMF_ERR_HIP;
+    }
+    return MMF_OK;
+  }
   const FwdScratch s = fwd_scratch(M, K);
   int8_t* q = reinterpret_cast<int8_t*>(scratch + s.q_off);
   float* a_scale = reinterpret_cast<float*>(scratch + s.a_off);

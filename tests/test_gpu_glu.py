@@ -163,3 +163,42 @@ def test_glu_up_full_size_sampled(mmf):
         ref = oracle.glu_fwd(case.x_f32[m:m + 1], case.gamma, t_g, ws_g, t_u, ws_u)
         compare_p(p[m:m + 1].cpu().numpy(), ref["p"], ref["acc_g"], ref["acc_u"],
                   np.array([m in flip_rows]))
+
+
+@pytest.mark.parametrize("M,K,L,f32", [(1, 2064, 48, False), (1, 4096, 160, False), (3, 1024, 1024, False),
+                                       (8, 2048, 4160, False), (17, 256, 16, True), (40, 512, 5632, False),
+                                       (2, 4096, 1040, True)])
+def test_glu_decode_epilogue(mmf, M, K, L, f32):
+    """Few tokens take the fused decode kernel with the GLU epilogue (launches
+    of at most 8 tokens): one token on the vector ALU with 32- or 64-column
+    workgroups (and the LDS-staged weights at K = 4096), two to eight on the
+    matrix cores with two or four 16-column blocks per workgroup, several
+    slices, bf16 and fp32 x.  p against the oracle, and bit for bit against
+    the MFMA kernel's GLU epilogue."""
+    rs = np.random.default_rng(3000 + M + K + L)
+    bits, xf, g, W = workloads.random_case(rs, M, K, 2 * L)
+    x_form = xf if f32 else bits
+    Wgu, w_scales, t_g, t_u, ws_g, ws_u = gpu_pack(mmf, W[:L], W[L:], bool((K + L) % 2))
+    ref = oracle.glu_fwd(xf, g, t_g, ws_g, t_u, ws_u)
+    case = Case(x_form, xf, g, W, "")
+    case.upload()
+    log(f"[glu decode] M={M} K={K} L={L} f32={f32}")
+    outs = []
+    for path in (mmf.MMF_PATH_GEMV, mmf.MMF_PATH_GEMM):
+        prev = mmf.mmf_set_path(path)
+        try:
+            p = torch.full((M, L), float("nan"), dtype=torch.float32, device=dev())
+            mmf.mmf_glu_fwd(case.x_d, case.g_d, Wgu, w_scales, p)  # bf16 or fp32 x by dtype
+            torch.cuda.synchronize()
+        finally:
+            mmf.mmf_set_path(prev)
+        outs.append(p.cpu().numpy())
+    q = torch.empty((M, K), dtype=torch.int8, device=dev())
+    a = torch.empty((M,), dtype=torch.float32, device=dev())
+    mmf.mmf_act_quant(case.x_d, case.g_d, q, a)
+    torch.cuda.synchronize()
+    flip_rows, _ = compare_q(q.cpu().numpy(), ref["q"])
+    flip = np.zeros(M, bool)
+    flip[flip_rows] = True
+    compare_p(outs[0], ref["p"], ref["acc_g"], ref["acc_u"], flip)
+    assert np.array_equal(outs[0].view(np.uint32), outs[1].view(np.uint32))
