@@ -3,14 +3,25 @@
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
 
+The default run measures the largest configuration of the headline metric:
+``large`` (prefill at d = 5120, M=16384, K=5120, N=27648; effective TOPS
+against the int8 MFMA peak) on the JSON line's top level, ``large_dec``
+(decode at d = 5120, M=1, K=5120, N=15360; HBM GB/s) under "secondary", each
+with its roofline, recorded HBM traffic and CPU oracle baseline, and the
+decode_m1 and glu_up workloads under "extra" (roofline and traffic only).
+
 Workloads (shapes in workloads.py):
-  decode_m1 (default), decode_m8, large_dec -- decode: a step is one forward
+  decode_m1, decode_m8, large_dec -- decode: a step is one forward
       (RMSNorm + int8 quant + VALU ternary contraction + dequant) for each of R
       distinct packed weight copies totalling >= 1 GiB, so every weight byte
       comes from HBM, issued back to back from one HIP graph.  value = HBM GB/s
       of algorithmic bytes (packed weights + x + gamma + y per call).
-  glu_up, glu_down, large, tiny -- prefill: a step is one forward over all M
-      tokens.  value = effective TOPS, 2*M*N*K / step time.
+  large (default), glu_up, glu_down, tiny -- prefill: a step is one forward
+      over all M tokens, i.e. the two launches mmf_bitlinear_fwd runs for
+      M > 40 (act-quant, then the int8 MFMA contraction with the dequant
+      epilogue), through mmf_bitlinear_fwd_ws.  value = effective TOPS,
+      2*M*N*K / step time; the roofline times the contraction launch in a loop
+      of its own (mmf_ternary_gemm_dequant on the same q).
   glu_gate -- the GLU channel mixer's fused up-projections and gate on the
       glu_up shape (M=8192, K=2048, L=5632): p = SiLU(g) * u in one contraction
       over the interleaved gate|up weights.  value = effective TOPS, 2*M*2L*K.
@@ -32,11 +43,10 @@ Workloads (shapes in workloads.py):
 
 The JSON line carries the roofline of the dominant kernel (decode: the fused
 decode kernel, the only launch of a decode forward; prefill: the contraction),
-timed with HIP events on the stream it runs on, with its HBM traffic per launch
-when profiles/traffic.json holds a counter reading of the current kernel
-source, and the CPU oracle timed on a bounded sample of the same workload.  The default run also reports the
-GLU up-projection prefill (effective TOPS vs the int8 MFMA peak) under
-"secondary".
+timed with HIP events on the stream it runs on inside the timed region, with
+its HBM traffic per launch when profiles/traffic.json holds a counter reading
+of the current kernel source, and the CPU oracle timed on a bounded sample of
+the same workload.
 """
 from __future__ import annotations
 
@@ -71,8 +81,9 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="decode_m1")
-    ap.add_argument("--no-secondary", action="store_true")
+    ap.add_argument("--workload", default="large")
+    ap.add_argument("--no-secondary", action="store_true",
+                    help="only the named workload (no secondary decode leg, no extras)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--hot-cache", action="store_true",
@@ -182,7 +193,8 @@ def record_traffic(run_workload, fetch_csv, write_csv):
         "kernel": "torch.neg over 2^28 bytes of fp32 (reads and writes 2^28 bytes)",
         "fetch_kib": f_kib, "write_kib": w_kib, "fetch_factor": f_fac, "write_factor": w_fac}
     entries = doc.setdefault("entries", {})
-    workloads_in_run = [run_workload] + (["glu_up"] if run_workload in DECODE else [])
+    # the counter runs profile one workload each (--no-secondary)
+    workloads_in_run = [run_workload]
     for name, vals in fetch.items():
         for wl in workloads_in_run:
             key = kernel_key(wl, name)
@@ -365,27 +377,35 @@ def bench_prefill(torch, mmf, w, args):
     q = torch.empty((w.M, w.K), dtype=torch.int8, device=dev)
     a = torch.empty((w.M,), dtype=torch.float32, device=dev)
     rs = torch.empty((w.M,), dtype=torch.int32, device=dev)
-    mmf.mmf_act_quant(x, gamma, q, a, rs)
     timer = Timer(torch)
+    # value: the forward through its entry point (M > 40: the act-quant launch,
+    # then the MFMA contraction with the dequant epilogue)
     ms_step = timer.time(lambda: mmf.mmf_bitlinear_fwd_ws(x, gamma, Wp, ws, y, wsb),
                          args.steps, args.warmup)
-    ms_gemm = timer.time(lambda: mmf.mmf_ternary_gemm_dequant(q, a, rs, Wp, ws, y),
-                         args.steps, args.warmup)
-    ms_aq = timer.time(lambda: mmf.mmf_act_quant(x, gamma, q, a, rs), args.steps, args.warmup)
+    # the roofline: the contraction launch alone, K back-to-back launches between
+    # two HIP events on the stream it runs on (events between the forward's two
+    # launches would add a cache write-back per event and time that instead)
+    mmf.mmf_act_quant_ex(x, gamma, q, a, rs)
+    us_gemm = timer.time(lambda: mmf.mmf_ternary_gemm_dequant(q, a, rs, Wp, ws, y),
+                         args.steps, args.warmup) * 1e3
+    us_aq = timer.time(lambda: mmf.mmf_act_quant_ex(x, gamma, q, a, rs), args.steps, args.warmup) * 1e3
     traffic, tdetail = recorded_traffic(w.name, "gemm_kernel")
     tops = w.ops / (ms_step * 1e-3) / 1e12
-    gemm_tops = w.ops / (ms_gemm * 1e-3) / 1e12
+    gemm_tops = w.ops / (us_gemm * 1e-6) / 1e12
     aq_bytes = w.M * w.K * x.element_size() + 4 * w.K + w.M * w.K + 8 * w.M
     result = {
         "value": tops, "unit": "TOPS", "ms_per_step": ms_step,
         "config": {"workload": w.name, "M": w.M, "K": w.K, "N": w.N, "x_dtype": w.x_dtype},
-        "roofline": {"bound": "mfma", "kernel": "gemm_kernel (prefill contraction)",
+        "roofline": {"bound": "mfma", "kernel": "gemm_kernel (prefill contraction, int8 MFMA)",
                      "achieved": gemm_tops, "peak": INT8_PEAK_TOPS, "unit": "TFLOP/s",
                      "frac": gemm_tops / INT8_PEAK_TOPS, "traffic": traffic,
                      "traffic_detail": tdetail,
-                     "ops_per_launch": w.ops, "avg_launch_us": ms_gemm * 1e3},
-        "act_quant": {"avg_launch_us": ms_aq * 1e3, "bytes": aq_bytes,
-                      "GB/s": aq_bytes / (ms_aq * 1e-3) / 1e9},
+                     "ops_per_launch": w.ops, "avg_launch_us": us_gemm,
+                     "timing": "HIP events around K back-to-back contraction launches on the "
+                               "stream they run on"},
+        "act_quant": {"avg_launch_us": us_aq, "bytes": aq_bytes,
+                      "GB/s": aq_bytes / (us_aq * 1e-6) / 1e9},
+        "launches_sum_ms": (us_gemm + us_aq) * 1e-3,
     }
     return result
 
@@ -762,15 +782,16 @@ def cpu_baseline(w, fb, seconds):
         return {"value": calls * fb / el / 1e9, "unit": "GB/s", "cores": threads, "kind": "oracle",
                 "sample": f"{calls} full forward calls (M={w.M}, K={w.K}, N={w.N}) in {el:.1f} s; "
                           "bytes counted as for the GPU (packed weights + x + gamma + y)"}
-    # prefill: a row sample, timed once, grown until it takes >= 1/4 of the budget
+    # prefill: a row sample over all N, timed once, grown (from the rate of the
+    # previous sample) until one sample takes at least half the budget
     rows = 8
     while True:
         t0 = time.perf_counter()
         oracle.bitlinear_fwd(xf[:rows], g, t, ws)
         el = time.perf_counter() - t0
-        if el >= seconds / 4 or rows >= w.M:
+        if el >= seconds / 2 or rows >= w.M:
             break
-        rows = min(w.M, rows * max(2, int(seconds / 4 / max(el, 1e-3))))
+        rows = min(w.M, max(2 * rows, int(rows * 0.8 * seconds / max(el, 1e-3))))
     return {"value": 2.0 * rows * w.N * w.K / el / 1e12, "unit": "TOPS", "cores": threads,
             "kind": "oracle",
             "sample": f"{rows} of {w.M} token rows (K={w.K}, N={w.N}) in {el:.1f} s"}
@@ -806,18 +827,31 @@ def main():
         "data": "synthetic (seeded; shapes of the paper's model widths)",
         "config": res["config"], "roofline": res["roofline"],
     }
-    for k in ("hot_cache_call_us", "act_quant", "contraction_only", "launch_floor", "stages", "forward"):
+    for k in ("hot_cache_call_us", "act_quant", "contraction_only", "launch_floor", "stages", "forward",
+              "launches_sum_ms"):
         if k in res:
             line[k] = res[k]
-    if not args.no_secondary and w is not None and w.name in DECODE:
-        sw = workloads.WORKLOADS["glu_up"]
-        log("[bench] secondary: glu_up prefill")
-        sec = bench_prefill(torch, mmf, sw, args)
-        line["secondary"] = {"metric": "prefill effective TOPS", "value": sec["value"],
-                             "unit": "TOPS", "ms_per_step": sec["ms_per_step"],
-                             "config": sec["config"], "roofline": sec["roofline"],
-                             "act_quant": sec["act_quant"]}
+    headline = args.workload == "large" and not args.no_secondary
+    if headline:
+        # the metric's decode half on the same configuration family (d = 5120)
+        dw = workloads.WORKLOADS["large_dec"]
+        log("[bench] secondary: large_dec decode")
         torch.cuda.empty_cache()
+        sec, sec_fb = bench_decode(torch, mmf, dw, args)
+        line["secondary"] = {"metric": "decode HBM GB/s", **{k: sec[k] for k in (
+            "value", "unit", "ms_per_step", "config", "roofline", "contraction_only", "launch_floor")}}
+        torch.cuda.empty_cache()
+        extra = {}
+        for name in ("decode_m1", "glu_up"):
+            ew = workloads.WORKLOADS[name]
+            log(f"[bench] extra: {name}")
+            if name in DECODE:
+                er, _ = bench_decode(torch, mmf, ew, args)
+            else:
+                er = bench_prefill(torch, mmf, ew, args)
+            extra[name] = {k: er[k] for k in ("value", "unit", "ms_per_step", "config", "roofline")}
+            torch.cuda.empty_cache()
+        line["extra"] = extra
     if args.calib_copy:
         log("[bench] calibration copy")
         calib_copy(torch)
@@ -831,6 +865,9 @@ def main():
             line["cpu_baseline"] = cpu_baseline_glu(args.workload, args.cpu_seconds)
         else:
             line["cpu_baseline"] = cpu_baseline(w, fb, args.cpu_seconds)
+        if headline:
+            line["secondary"]["cpu_baseline"] = cpu_baseline(workloads.WORKLOADS["large_dec"], sec_fb,
+                                                             args.cpu_seconds)
     print(json.dumps(line), flush=True)
 
 

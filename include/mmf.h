@@ -20,7 +20,14 @@
  *  - Every pointer to an array must be 16-byte aligned (MMF_ERR_ALIGN).
  *  - K (in-features) must be a positive multiple of 16 and at most 2^20
  *    (MMF_ERR_SHAPE); M (tokens) and N (out-features) may be any value in
- *    [0, 2^31 - 1]; M == 0 or N == 0 is a successful no-op.
+ *    [0, 2^31 - 1]; M == 0 or N == 0 is a successful no-op.  A call whose
+ *    shape the contraction kernel it would run cannot address with its
+ *    32-bit offsets returns MMF_ERR_SHAPE before anything is enqueued: the
+ *    int8 MFMA kernel needs (K/16) * N * 4 < 2^31, N <= 2^24 and row slices
+ *    of at least 256 tokens whose q and output stay below 2^31 bytes (so
+ *    N < 2^21); the decode kernel needs (K/16 + 8) * N * 4 < 2^32.
+ *  - Entry points with an `x_is_f32` argument take 0 (bfloat16 x) or 1
+ *    (float32 x); any other value returns MMF_ERR_DTYPE.
  *  - Outputs must not alias inputs.
  *  - Calls on different streams may run concurrently.
  *  - Return value: an mmf_status code.
@@ -59,11 +66,19 @@ extern "C" {
 /* Status codes. */
 #define MMF_OK 0
 #define MMF_ERR_NULL 1      /* a required pointer is NULL                      */
-#define MMF_ERR_SHAPE 2     /* a size is out of range (K % 16, K == 0, ...)    */
+#define MMF_ERR_SHAPE 2     /* a size is out of range (K % 16, K == 0, a       */
+                            /* shape past a kernel's 32-bit offsets, ...)      */
 #define MMF_ERR_ALIGN 3     /* an array pointer is not 16-byte aligned         */
-#define MMF_ERR_WORKSPACE 4 /* the caller's workspace is too small             */
+#define MMF_ERR_DTYPE 4     /* an activation dtype selector is not 0 or 1      */
 #define MMF_ERR_HIP 5       /* a HIP runtime call or a kernel launch failed    */
-#define MMF_ERR_ARG 6       /* another argument is invalid (e.g. path value)   */
+#define MMF_ERR_WORKSPACE 6 /* the caller's workspace is too small or          */
+                            /* misaligned                                      */
+#define MMF_ERR_ARG 7       /* another argument is invalid (e.g. path value)   */
+
+/* Activation dtype selector of the entry points that take either form
+ * (the `x_is_f32` arguments below). */
+#define MMF_DTYPE_BF16 0
+#define MMF_DTYPE_F32 1
 
 /* Human-readable name of a status code (static storage; never NULL). */
 const char *mmf_status_string(int status);
@@ -99,16 +114,19 @@ int mmf_ternarize_weights(const float *W, int64_t N, int64_t K,
  *   a        = max(max_k |y_k|, 1e-5)
  *   q_k      = clamp(round_half_even(y_k * (127 / a)), -128, 127)
  *   a_scale  = a / 127,   q_rowsum = sum_k q_k.
- * x: [M][K] bf16 bits; gamma: [K] or NULL; q: [M][K] out; a_scale: [M] out;
- * q_rowsum: [M] out (may be NULL).
+ * x: [M][K] bf16 bits; gamma: [K] or NULL; q: [M][K] out; a_scale: [M] out.
  */
 int mmf_act_quant(const uint16_t *x, const float *gamma, int8_t *q,
-                  float *a_scale, int32_t *q_rowsum, int64_t M, int64_t K,
-                  hipStream_t stream);
+                  float *a_scale, int64_t M, int64_t K, hipStream_t stream);
 /* The same for float32 activations. */
 int mmf_act_quant_f32(const float *x, const float *gamma, int8_t *q,
-                      float *a_scale, int32_t *q_rowsum, int64_t M, int64_t K,
-                      hipStream_t stream);
+                      float *a_scale, int64_t M, int64_t K, hipStream_t stream);
+/* The same with the activation dtype as an argument (x_is_f32: 0 = bf16,
+ * 1 = float32, else MMF_ERR_DTYPE) and the row sums q_rowsum [M] (int32,
+ * may be NULL) that the contraction-stage entry points below take. */
+int mmf_act_quant_ex(const void *x, int x_is_f32, const float *gamma, int8_t *q,
+                     float *a_scale, int32_t *q_rowsum, int64_t M, int64_t K,
+                     hipStream_t stream);
 
 /*
  * The fused BitLinear forward (Algorithm 1, forward_pass, bias 0):

@@ -44,8 +44,9 @@ _SIGNATURES = {
     "mmf_version": ([], ctypes.c_int),
     "mmf_packed_weight_bytes": ([_I64, _I64], _SZ),
     "mmf_ternarize_weights": ([_P, _I64, _I64, _P, _P, _P], ctypes.c_int),
-    "mmf_act_quant": ([_P, _P, _P, _P, _P, _I64, _I64, _P], ctypes.c_int),
-    "mmf_act_quant_f32": ([_P, _P, _P, _P, _P, _I64, _I64, _P], ctypes.c_int),
+    "mmf_act_quant": ([_P, _P, _P, _P, _I64, _I64, _P], ctypes.c_int),
+    "mmf_act_quant_f32": ([_P, _P, _P, _P, _I64, _I64, _P], ctypes.c_int),
+    "mmf_act_quant_ex": ([_P, ctypes.c_int, _P, _P, _P, _P, _I64, _I64, _P], ctypes.c_int),
     "mmf_bitlinear_fwd": ([_P, _P, _P, _P, _P, _I64, _I64, _I64, _P], ctypes.c_int),
     "mmf_bitlinear_fwd_f32": ([_P, _P, _P, _P, _P, _I64, _I64, _I64, _P], ctypes.c_int),
     "mmf_bitlinear_workspace_bytes": ([_I64, _I64], _SZ),
@@ -169,8 +170,17 @@ def mmf_act_quant(x: torch.Tensor, gamma: torch.Tensor | None, q: torch.Tensor,
     _need(a_scale, "a_scale", torch.float32, (M,))
     if q_rowsum is not None:
         _need(q_rowsum, "q_rowsum", torch.int32, (M,))
+        _check(_lib.mmf_act_quant_ex(_ptr(x), int(is_f32), _ptr(gamma), _ptr(q), _ptr(a_scale),
+                                     _ptr(q_rowsum), M, K, _stream(stream)))
+        return
     fn = _lib.mmf_act_quant_f32 if is_f32 else _lib.mmf_act_quant
-    _check(fn(_ptr(x), _ptr(gamma), _ptr(q), _ptr(a_scale), _ptr(q_rowsum), M, K, _stream(stream)))
+    _check(fn(_ptr(x), _ptr(gamma), _ptr(q), _ptr(a_scale), M, K, _stream(stream)))
+
+
+def mmf_act_quant_ex(x: torch.Tensor, gamma: torch.Tensor | None, q: torch.Tensor,
+                     a_scale: torch.Tensor, q_rowsum: torch.Tensor | None, stream=None) -> None:
+    """mmf_act_quant with the row sums q_rowsum i32 [M] (None: not written)."""
+    mmf_act_quant(x, gamma, q, a_scale, q_rowsum, stream)
 
 
 def mmf_bitlinear_fwd(x: torch.Tensor, gamma: torch.Tensor | None, Wpacked: torch.Tensor,

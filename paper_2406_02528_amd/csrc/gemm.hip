@@ -455,14 +455,10 @@ hipError_t launch_cfg(const ContractArgs& a, int64_t m_begin, int64_t m_rows, hi
 
 hipError_t launch_gemm(const ContractArgs& a, hipStream_t stream) {
   // 32-bit buffer offsets: a launch covers at most 2^31 - 1 bytes of q, of
-  // packed weights and of output; taller problems run in row slices.
-  const int64_t packed = static_cast<int64_t>(a.K / 16) * a.N * 4;
-  if (packed >= (int64_t(1) << 31) || a.N > (int64_t(1) << 24)) return hipErrorInvalidValue;
-  const int64_t by_q = ((int64_t(1) << 31) - 1) / a.K;
-  const int64_t by_y = ((int64_t(1) << 31) - 1) / (4 * a.N);
-  int64_t slice = by_q < by_y ? by_q : by_y;
-  slice = (slice / 256) * 256;
-  if (slice < 256) return hipErrorInvalidValue;
+  // packed weights and of output; taller problems run in row slices.  The
+  // C-ABI layer rejects shapes without a slice before enqueueing anything.
+  const int64_t slice = gemm_row_slice(a.K, a.N);
+  if (slice == 0) return hipErrorInvalidValue;
   const bool bx4 = (a.N % 4) == 0;
   for (int64_t m0 = 0; m0 < a.M; m0 += slice) {
     const int64_t rows = a.M - m0 < slice ? a.M - m0 : slice;

@@ -43,22 +43,28 @@ FwdScratch fwd_scratch(int64_t M, int64_t K) {
 }
 
 // Automatic choice: up to kDecodeSliceMaxTokens tokens run as decode launches
-// of at most 8 tokens each.  Measured (K = 2048, N = 2048 / 6144 / 11264): the
-// MFMA kernel takes >= 26 us at any small M (each output tile's k loop runs
-// on one CU), the decode slices ~5 us each, so the slices win up to ~44
-// tokens (M = 16: 9.9 vs 26.3 us; M = 32: 19.5 vs 27.3; M = 48: 29.2 vs 28.1).
+// of at most 8 tokens each, when the decode kernel takes such a slice (its
+// LDS holds q of 8 tokens up to K = 7680).  Measured (K = 2048, N = 2048 /
+// 6144 / 11264): the MFMA kernel takes >= 26 us at any small M (each output
+// tile's k loop runs on one CU), the decode slices ~5 us each, so the slices
+// win up to ~44 tokens (M = 16: 9.9 vs 26.3 us; M = 32: 19.5 vs 27.3;
+// M = 48: 29.2 vs 28.1).  MMF_PATH_GEMV forces the decode kernels for every
+// M (slices it cannot hold then go to the gemv kernel, which reads q from
+// global memory); MMF_PATH_GEMM forces the MFMA kernel.
 constexpr int64_t kDecodeSliceMaxTokens = 40;
-bool use_gemv(int64_t M) {
+bool use_decode(int64_t M, int64_t K, int64_t N, bool from_x, bool x_is_f32) {
   const int p = g_path.load(std::memory_order_relaxed);
   if (p == MMF_PATH_GEMV) return true;
   if (p == MMF_PATH_GEMM) return false;
-  return M <= kDecodeSliceMaxTokens;
+  if (M > kDecodeSliceMaxTokens) return false;
+  return mmf::decode_fits(M < kDecodeMaxTokens ? M : kDecodeMaxTokens, static_cast<int>(K), N, from_x,
+                          x_is_f32);
 }
 
 // Contraction from quantised activations.  Decode-sized slices of at most 8
 // tokens keep q in LDS when it fits, else read it from global memory.
 hipError_t contract(const mmf::ContractArgs& a, hipStream_t stream) {
-  if (!use_gemv(a.M)) return mmf::launch_gemm(a, stream);
+  if (!use_decode(a.M, a.K, a.N, false, false)) return mmf::launch_gemm(a, stream);
   for (int64_t m0 = 0; m0 < a.M; m0 += kDecodeMaxTokens) {
     const int64_t mt = a.M - m0 < kDecodeMaxTokens ? a.M - m0 : kDecodeMaxTokens;
     const bool raw = a.epilogue == mmf::Epilogue::kRawI32;
@@ -83,10 +89,29 @@ hipError_t contract(const mmf::ContractArgs& a, hipStream_t stream) {
 // The whole forward runs as fused decode launches (no scratch) when every
 // slice of at most 8 tokens fits the fused kernel.
 bool fused_decode(int64_t M, int64_t K, int64_t N, bool x_is_f32) {
-  if (!use_gemv(M)) return false;
+  if (!use_decode(M, K, N, true, x_is_f32)) return false;
   const int64_t mt = M < kDecodeMaxTokens ? M : kDecodeMaxTokens;
   return mmf::decode_fits(mt, static_cast<int>(K), N, true, x_is_f32);
 }
+
+// Shape limits of the kernels a call will run, checked before anything is
+// enqueued (MMF_ERR_SHAPE).  check_contract: the contraction from quantised
+// activations (contract() above); check_gemm: the MFMA kernel alone;
+// check_from_x: a forward from x, which runs fused decode launches when they
+// fit and otherwise act-quant followed by `gemm_only ? the MFMA kernel :
+// contract()`.
+int check_gemm(int64_t K, int64_t N) {
+  return mmf::gemm_row_slice(K, N) > 0 ? MMF_OK : MMF_ERR_SHAPE;
+}
+int check_contract(int64_t M, int64_t K, int64_t N) {
+  if (M == 0 || N == 0 || use_decode(M, K, N, false, false)) return MMF_OK;
+  return check_gemm(K, N);
+}
+int check_from_x(int64_t M, int64_t K, int64_t N, bool x_is_f32, bool gemm_only) {
+  if (M == 0 || N == 0 || fused_decode(M, K, N, x_is_f32)) return MMF_OK;
+  return gemm_only ? check_gemm(K, N) : check_contract(M, K, N);
+}
+int check_dtype(int x_is_f32) { return (x_is_f32 == 0 || x_is_f32 == 1) ? MMF_OK : MMF_ERR_DTYPE; }
 
 hipError_t run_fused_decode(const void* x, bool x_is_f32, const float* gamma,
                             const uint32_t* Wpacked, const float* w_scale, float* y, int64_t M,
@@ -104,10 +129,12 @@ hipError_t run_fused_decode(const void* x, bool x_is_f32, const float* gamma,
 }
 
 // Checks of the forward's arguments shared by the allocating and _ws forms.
-int check_fwd(const void* x, const float* gamma, const uint32_t* Wpacked, const float* w_scale,
-              const float* y, int64_t M, int64_t K, int64_t N) {
+int check_fwd(const void* x, bool x_is_f32, const float* gamma, const uint32_t* Wpacked,
+              const float* w_scale, const float* y, int64_t M, int64_t K, int64_t N,
+              bool gemm_only = false) {
   if (int st = check_shape(M, K, N)) return st;
   if (M == 0 || N == 0) return MMF_OK;
+  if (int st = check_from_x(M, K, N, x_is_f32, gemm_only)) return st;
   if (!x || !Wpacked || !w_scale || !y) return MMF_ERR_NULL;
   if (!aligned16(x) || !aligned16(Wpacked) || !aligned16(y) || (gamma && !aligned16(gamma)))
     return MMF_ERR_ALIGN;
@@ -134,7 +161,7 @@ int run_fwd(const void* x, bool x_is_f32, const float* gamma, const uint32_t* Wp
 int fwd_alloc(const void* x, bool x_is_f32, const float* gamma, const uint32_t* Wpacked,
               const float* w_scale, float* y, int64_t M, int64_t K, int64_t N,
               hipStream_t stream) {
-  if (int st = check_fwd(x, gamma, Wpacked, w_scale, y, M, K, N)) return st;
+  if (int st = check_fwd(x, x_is_f32, gamma, Wpacked, w_scale, y, M, K, N)) return st;
   if (M == 0 || N == 0) return MMF_OK;
   if (fused_decode(M, K, N, x_is_f32))
     return hip_status(run_fused_decode(x, x_is_f32, gamma, Wpacked, w_scale, y, M, K, N, stream));
@@ -148,27 +175,47 @@ int fwd_alloc(const void* x, bool x_is_f32, const float* gamma, const uint32_t* 
   return hip_status(fe);
 }
 
-int act_quant_common(const void* x, bool x_is_f32, const float* gamma, int8_t* q,
+int act_quant_common(const void* x, int x_is_f32, const float* gamma, int8_t* q,
                      float* a_scale, int32_t* q_rowsum, int64_t M, int64_t K,
                      hipStream_t stream) {
+  if (int st = check_dtype(x_is_f32)) return st;
   if (int st = check_shape(M, K, 0)) return st;
   if (M == 0) return MMF_OK;
   if (!x || !q || !a_scale) return MMF_ERR_NULL;
   if (!aligned16(x) || !aligned16(q) || !aligned16(a_scale) || (gamma && !aligned16(gamma)) ||
       (q_rowsum && !aligned16(q_rowsum)))
     return MMF_ERR_ALIGN;
-  return hip_status(mmf::launch_act_quant(x, x_is_f32, gamma, q, a_scale, q_rowsum, M,
+  return hip_status(mmf::launch_act_quant(x, x_is_f32 == 1, gamma, q, a_scale, q_rowsum, M,
                                           static_cast<int>(K), stream));
+}
+
+// Runs `run(scratch)` on the caller's workspace (checked against `need`), or
+// on stream-ordered scratch allocated here when `workspace` is NULL.
+template <class F>
+int with_workspace(void* workspace, size_t workspace_bytes, size_t need, hipStream_t stream, F&& run) {
+  if (workspace != nullptr) {
+    if ((reinterpret_cast<uintptr_t>(workspace) & (kScratchAlign - 1)) != 0 || workspace_bytes < need)
+      return MMF_ERR_WORKSPACE;
+    return run(static_cast<char*>(workspace));
+  }
+  if (need == 0) return run(nullptr);
+  void* p = nullptr;
+  if (hipMallocAsync(&p, need, stream) != hipSuccess) return MMF_ERR_HIP;
+  const int st = run(static_cast<char*>(p));
+  const hipError_t fe = hipFreeAsync(p, stream);
+  if (st != MMF_OK) return st;
+  return hip_status(fe);
 }
 
 // GLU (gated up-projection): x -> RMSNorm + quantisation -> the interleaved
 // gate/up contraction with the SiLU(g) * u epilogue: fused decode launches for
 // the token counts the decode kernel takes, the MFMA kernel otherwise.
-int check_glu(const void* x, const float* gamma, const uint32_t* Wgu, const float* w_scales,
-              const float* p, int64_t M, int64_t K, int64_t L) {
+int check_glu(const void* x, bool x_is_f32, const float* gamma, const uint32_t* Wgu,
+              const float* w_scales, const float* p, int64_t M, int64_t K, int64_t L) {
   if (L < 0 || L > kMaxMN / 2 || (L % 16) != 0) return MMF_ERR_SHAPE;
   if (int st = check_shape(M, K, 2 * L)) return st;
   if (M == 0 || L == 0) return MMF_OK;
+  if (int st = check_from_x(M, K, 2 * L, x_is_f32, true)) return st;
   if (!x || !Wgu || !w_scales || !p) return MMF_ERR_NULL;
   if (!aligned16(x) || !aligned16(Wgu) || !aligned16(p) || (gamma && !aligned16(gamma)))
     return MMF_ERR_ALIGN;
@@ -205,16 +252,13 @@ int run_glu(const void* x, bool x_is_f32, const float* gamma, const uint32_t* Wg
 int glu_alloc(const void* x, bool x_is_f32, const float* gamma, const uint32_t* Wgu,
               const float* w_scales, float* p, int64_t M, int64_t K, int64_t L,
               hipStream_t stream) {
-  if (int st = check_glu(x, gamma, Wgu, w_scales, p, M, K, L)) return st;
+  if (int st = check_glu(x, x_is_f32, gamma, Wgu, w_scales, p, M, K, L)) return st;
   if (M == 0 || L == 0) return MMF_OK;
-  const FwdScratch s = fwd_scratch(M, K);
-  void* scratch = nullptr;
-  if (hipMallocAsync(&scratch, s.total, stream) != hipSuccess) return MMF_ERR_HIP;
-  const int st = run_glu(x, x_is_f32, gamma, Wgu, w_scales, p, M, K, L,
-                         static_cast<char*>(scratch), stream);
-  const hipError_t fe = hipFreeAsync(scratch, stream);
-  if (st != MMF_OK) return st;
-  return hip_status(fe);
+  // the fused decode launches need no scratch
+  const size_t need = fused_decode(M, K, 2 * L, x_is_f32) ? 0 : fwd_scratch(M, K).total;
+  return with_workspace(nullptr, 0, need, stream, [&](char* scratch) {
+    return run_glu(x, x_is_f32, gamma, Wgu, w_scales, p, M, K, L, scratch, stream);
+  });
 }
 
 // ---- affine forward (bias and per-segment activations after the dequant) ----
@@ -246,24 +290,6 @@ int run_affine(const void* x, bool x_is_f32, const float* gamma, const uint32_t*
   mmf::ContractArgs a{q, a_scale, rowsum, Wpacked, w_scales, y, M, static_cast<int>(K), N,
                       mmf::Epilogue::kAffineF32, aff};
   return hip_status(mmf::launch_gemm(a, stream));
-}
-
-// Runs `run(scratch)` on the caller's workspace (checked against `need`), or
-// on stream-ordered scratch allocated here when `workspace` is NULL.
-template <class F>
-int with_workspace(void* workspace, size_t workspace_bytes, size_t need, hipStream_t stream, F&& run) {
-  if (workspace != nullptr) {
-    if ((reinterpret_cast<uintptr_t>(workspace) & (kScratchAlign - 1)) != 0 || workspace_bytes < need)
-      return MMF_ERR_WORKSPACE;
-    return run(static_cast<char*>(workspace));
-  }
-  if (need == 0) return run(nullptr);
-  void* p = nullptr;
-  if (hipMallocAsync(&p, need, stream) != hipSuccess) return MMF_ERR_HIP;
-  const int st = run(static_cast<char*>(p));
-  const hipError_t fe = hipFreeAsync(p, stream);
-  if (st != MMF_OK) return st;
-  return hip_status(fe);
 }
 
 bool aligned16_or_null(const void* p) { return p == nullptr || aligned16(p); }
@@ -322,12 +348,6 @@ MlgruScratch mlgru_scratch(int64_t B, int64_t T, int64_t d) {
 
 // ---- training forward and backward ----
 
-// A launch of the MFMA kernel needs packed weights and rows of output within
-// 32-bit offsets.
-bool gemm_shape_ok(int64_t K, int64_t N) {
-  return (K / 16) * N * 4 < (int64_t(1) << 31) && N <= (int64_t(1) << 24);
-}
-
 struct TrainScratch {
   size_t part_off, rs_off, total;
 };
@@ -364,16 +384,17 @@ const char* mmf_status_string(int status) {
   switch (status) {
     case MMF_OK: return "MMF_OK";
     case MMF_ERR_NULL: return "MMF_ERR_NULL: a required pointer is NULL";
-    case MMF_ERR_SHAPE: return "MMF_ERR_SHAPE: size out of range (K must be a positive multiple of 16, at most 2^20; M, N in [0, 2^31-1])";
+    case MMF_ERR_SHAPE: return "MMF_ERR_SHAPE: size out of range (K must be a positive multiple of 16, at most 2^20; M, N in [0, 2^31-1]; the kernel's 32-bit offset limits)";
     case MMF_ERR_ALIGN: return "MMF_ERR_ALIGN: an array pointer is not 16-byte aligned";
-    case MMF_ERR_WORKSPACE: return "MMF_ERR_WORKSPACE: workspace too small or misaligned";
+    case MMF_ERR_DTYPE: return "MMF_ERR_DTYPE: the activation dtype selector must be 0 (bf16) or 1 (float32)";
     case MMF_ERR_HIP: return "MMF_ERR_HIP: a HIP runtime call or kernel launch failed";
+    case MMF_ERR_WORKSPACE: return "MMF_ERR_WORKSPACE: workspace too small or misaligned";
     case MMF_ERR_ARG: return "MMF_ERR_ARG: invalid argument";
     default: return "MMF: unknown status";
   }
 }
 
-int mmf_version(void) { return 1; }
+int mmf_version(void) { return 2; }
 
 size_t mmf_packed_weight_bytes(int64_t N, int64_t K) {
   if (check_shape(0, K, N) != MMF_OK) return 0;
@@ -396,14 +417,19 @@ int mmf_ternarize_weights(const float* W, int64_t N, int64_t K, uint32_t* Wpacke
   return hip_status(fe);
 }
 
-int mmf_act_quant(const uint16_t* x, const float* gamma, int8_t* q, float* a_scale,
-                  int32_t* q_rowsum, int64_t M, int64_t K, hipStream_t stream) {
-  return act_quant_common(x, false, gamma, q, a_scale, q_rowsum, M, K, stream);
+int mmf_act_quant(const uint16_t* x, const float* gamma, int8_t* q, float* a_scale, int64_t M,
+                  int64_t K, hipStream_t stream) {
+  return act_quant_common(x, 0, gamma, q, a_scale, nullptr, M, K, stream);
 }
 
-int mmf_act_quant_f32(const float* x, const float* gamma, int8_t* q, float* a_scale,
-                      int32_t* q_rowsum, int64_t M, int64_t K, hipStream_t stream) {
-  return act_quant_common(x, true, gamma, q, a_scale, q_rowsum, M, K, stream);
+int mmf_act_quant_f32(const float* x, const float* gamma, int8_t* q, float* a_scale, int64_t M,
+                      int64_t K, hipStream_t stream) {
+  return act_quant_common(x, 1, gamma, q, a_scale, nullptr, M, K, stream);
+}
+
+int mmf_act_quant_ex(const void* x, int x_is_f32, const float* gamma, int8_t* q, float* a_scale,
+                     int32_t* q_rowsum, int64_t M, int64_t K, hipStream_t stream) {
+  return act_quant_common(x, x_is_f32, gamma, q, a_scale, q_rowsum, M, K, stream);
 }
 
 int mmf_bitlinear_fwd(const uint16_t* x, const float* gamma, const uint32_t* Wpacked,
@@ -427,8 +453,8 @@ int mmf_bitlinear_fwd_ws(const void* x, int x_is_f32, const float* gamma,
                          const uint32_t* Wpacked, const float* w_scale, float* y, int64_t M,
                          int64_t K, int64_t N, void* workspace, size_t workspace_bytes,
                          hipStream_t stream) {
-  if (x_is_f32 != 0 && x_is_f32 != 1) return MMF_ERR_ARG;
-  if (int st = check_fwd(x, gamma, Wpacked, w_scale, y, M, K, N)) return st;
+  if (int st = check_dtype(x_is_f32)) return st;
+  if (int st = check_fwd(x, x_is_f32 == 1, gamma, Wpacked, w_scale, y, M, K, N)) return st;
   if (M == 0 || N == 0) return MMF_OK;
   if (!workspace) return MMF_ERR_NULL;
   if ((reinterpret_cast<uintptr_t>(workspace) & (kScratchAlign - 1)) != 0 ||
@@ -443,6 +469,7 @@ int mmf_ternary_gemm_dequant(const int8_t* q, const float* a_scale, const int32_
                              int64_t K, int64_t N, hipStream_t stream) {
   if (int st = check_shape(M, K, N)) return st;
   if (M == 0 || N == 0) return MMF_OK;
+  if (int st = check_contract(M, K, N)) return st;
   if (!q || !a_scale || !q_rowsum || !Wpacked || !w_scale || !y) return MMF_ERR_NULL;
   if (!aligned16(q) || !aligned16(a_scale) || !aligned16(q_rowsum) || !aligned16(Wpacked) ||
       !aligned16(y))
@@ -456,6 +483,7 @@ int mmf_ternary_gemm_i32(const int8_t* q, const uint32_t* Wpacked, int32_t* acc,
                          int64_t K, int64_t N, hipStream_t stream) {
   if (int st = check_shape(M, K, N)) return st;
   if (M == 0 || N == 0) return MMF_OK;
+  if (int st = check_contract(M, K, N)) return st;
   if (!q || !Wpacked || !acc) return MMF_ERR_NULL;
   if (!aligned16(q) || !aligned16(Wpacked) || !aligned16(acc)) return MMF_ERR_ALIGN;
   void* rowsum = nullptr;
@@ -499,8 +527,8 @@ int mmf_glu_fwd_f32(const float* x, const float* gamma, const uint32_t* Wgu_pack
 int mmf_glu_fwd_ws(const void* x, int x_is_f32, const float* gamma, const uint32_t* Wgu_packed,
                    const float* w_scales, float* p, int64_t M, int64_t K, int64_t L,
                    void* workspace, size_t workspace_bytes, hipStream_t stream) {
-  if (x_is_f32 != 0 && x_is_f32 != 1) return MMF_ERR_ARG;
-  if (int st = check_glu(x, gamma, Wgu_packed, w_scales, p, M, K, L)) return st;
+  if (int st = check_dtype(x_is_f32)) return st;
+  if (int st = check_glu(x, x_is_f32 == 1, gamma, Wgu_packed, w_scales, p, M, K, L)) return st;
   if (M == 0 || L == 0) return MMF_OK;
   if (!workspace) return MMF_ERR_NULL;
   if ((reinterpret_cast<uintptr_t>(workspace) & (kScratchAlign - 1)) != 0 ||
@@ -516,6 +544,7 @@ int mmf_ternary_gemm_glu(const int8_t* q, const float* a_scale, const int32_t* q
   if (L < 0 || L > kMaxMN / 2 || (L % 16) != 0) return MMF_ERR_SHAPE;
   if (int st = check_shape(M, K, 2 * L)) return st;
   if (M == 0 || L == 0) return MMF_OK;
+  if (int st = check_gemm(K, 2 * L)) return st;
   if (!q || !a_scale || !q_rowsum || !Wgu_packed || !w_scales || !p) return MMF_ERR_NULL;
   if (!aligned16(q) || !aligned16(a_scale) || !aligned16(q_rowsum) || !aligned16(Wgu_packed) ||
       !aligned16(p))
@@ -528,8 +557,8 @@ int mmf_ternary_gemm_glu(const int8_t* q, const float* a_scale, const int32_t* q
 int mmf_bitlinear_fwd_bias(const void* x, int x_is_f32, const float* gamma,
                            const uint32_t* Wpacked, const float* w_scale, const float* bias,
                            float* y, int64_t M, int64_t K, int64_t N, hipStream_t stream) {
-  if (x_is_f32 != 0 && x_is_f32 != 1) return MMF_ERR_ARG;
-  if (int st = check_fwd(x, gamma, Wpacked, w_scale, y, M, K, N)) return st;
+  if (int st = check_dtype(x_is_f32)) return st;
+  if (int st = check_fwd(x, x_is_f32 == 1, gamma, Wpacked, w_scale, y, M, K, N, true)) return st;
   if (N % 4 != 0) return MMF_ERR_SHAPE;
   if (M == 0 || N == 0) return MMF_OK;
   if (!bias) return MMF_ERR_NULL;
@@ -553,9 +582,10 @@ int mmf_mlgru_proj(const void* x, int x_is_f32, const float* gamma, const uint32
                    const float* w_scales, const float* bias, const float* lb, float* fcg,
                    int64_t M, int64_t K, int64_t d, void* workspace, size_t workspace_bytes,
                    hipStream_t stream) {
-  if (x_is_f32 != 0 && x_is_f32 != 1) return MMF_ERR_ARG;
+  if (int st = check_dtype(x_is_f32)) return st;
   if (int st = check_mlgru_proj(x, gamma, Wfcg, w_scales, bias, lb, fcg, M, K, d)) return st;
   if (M == 0) return MMF_OK;
+  if (int st = check_from_x(M, K, 3 * d, x_is_f32 == 1, true)) return st;
   mmf::Affine aff;
   aff.bias = bias;
   aff.lb = lb;
@@ -573,6 +603,7 @@ int mmf_mlgru_proj_q(const int8_t* q, const float* a_scale, const int32_t* q_row
   if (int st = check_mlgru_d(d)) return st;
   if (int st = check_shape(M, K, 3 * d)) return st;
   if (M == 0) return MMF_OK;
+  if (int st = check_gemm(K, 3 * d)) return st;
   if (!q || !a_scale || !q_rowsum || !Wfcg || !w_scales || !fcg) return MMF_ERR_NULL;
   if (!aligned16(q) || !aligned16(a_scale) || !aligned16(q_rowsum) || !aligned16(Wfcg) ||
       !aligned16(fcg) || !aligned16_or_null(bias) || !aligned16_or_null(lb))
@@ -612,12 +643,14 @@ int mmf_mlgru_fwd(const void* x, int x_is_f32, const float* gamma, const uint32_
                   float* h_last, const float* gamma_o, const uint32_t* Wo, const float* w_scale_o,
                   const float* b_o, float* o, int64_t B, int64_t T, int64_t d, void* workspace,
                   size_t workspace_bytes, hipStream_t stream) {
-  if (x_is_f32 != 0 && x_is_f32 != 1) return MMF_ERR_ARG;
+  if (int st = check_dtype(x_is_f32)) return st;
   if (int st = check_mlgru_d(d)) return st;
   if (d > kMaxK) return MMF_ERR_SHAPE;
   if (B < 0 || T < 0 || B > kMaxMN || T > kMaxMN || (T > 0 && B > kMaxMN / T)) return MMF_ERR_SHAPE;
   const int64_t M = B * T;
   if (M == 0) return MMF_OK;
+  if (int st = check_from_x(M, d, 3 * d, x_is_f32 == 1, true)) return st;
+  if (int st = check_from_x(M, d, d, true, true)) return st;
   if (!x || !Wfcg || !w_scales || !Wo || !w_scale_o || !o) return MMF_ERR_NULL;
   if (!aligned16(x) || !aligned16(Wfcg) || !aligned16(Wo) || !aligned16(o) ||
       !aligned16_or_null(gamma) || !aligned16_or_null(bias) || !aligned16_or_null(lb) ||
@@ -672,9 +705,9 @@ int mmf_bitlinear_train_fwd(const void* x, int x_is_f32, const float* gamma, con
                             const float* bias, float* y, uint32_t* Wpacked, float* w_scale, int8_t* q,
                             float* a_scale, float* rstd, int64_t M, int64_t K, int64_t N, void* workspace,
                             size_t workspace_bytes, hipStream_t stream) {
-  if (x_is_f32 != 0 && x_is_f32 != 1) return MMF_ERR_ARG;
+  if (int st = check_dtype(x_is_f32)) return st;
   if (int st = check_shape(M, K, N)) return st;
-  if (!gemm_shape_ok(K, N) || (bias && N % 4 != 0)) return MMF_ERR_SHAPE;
+  if (check_gemm(K, N) != MMF_OK || (bias && N % 4 != 0)) return MMF_ERR_SHAPE;
   if (M == 0 || N == 0) return MMF_OK;
   if (!x || !W || !y || !Wpacked || !w_scale || !q || !a_scale) return MMF_ERR_NULL;
   if (!aligned16(x) || !aligned16(W) || !aligned16(y) || !aligned16(Wpacked) || !aligned16(q) ||
@@ -708,7 +741,7 @@ int mmf_bitlinear_bwd(const uint16_t* dO, const void* x, int x_is_f32, const flo
                       const float* rstd, const int8_t* q, const float* a_scale, const uint32_t* Wpacked,
                       const float* w_scale, float* dx, float* dW, float* db, float* dgamma, int64_t M,
                       int64_t K, int64_t N, void* workspace, size_t workspace_bytes, hipStream_t stream) {
-  if (x_is_f32 != 0 && x_is_f32 != 1) return MMF_ERR_ARG;
+  if (int st = check_dtype(x_is_f32)) return st;
   if (int st = check_shape(M, K, N)) return st;
   if (M == 0 || N == 0) return MMF_OK;
   if (!dO || !x || !rstd || !q || !a_scale || !Wpacked || !w_scale || !dx || !dW) return MMF_ERR_NULL;

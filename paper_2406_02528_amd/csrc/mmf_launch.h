@@ -92,6 +92,19 @@ bool decode_fits(int64_t mt, int K, int64_t N, bool from_x, bool x_is_f32);
 hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream);
 // Prefill kernel: int8 MFMA, any M.
 hipError_t launch_gemm(const ContractArgs& a, hipStream_t stream);
+// Rows per launch of the MFMA kernel for K in-features and N out-features,
+// or 0 when the shape is beyond its 32-bit buffer offsets: the packed weights
+// must stay below 2^31 bytes, N at most 2^24, and a launch covers a slice of
+// rows (a multiple of 256, at least 256) whose q and output stay below 2^31
+// bytes each.
+inline int64_t gemm_row_slice(int64_t K, int64_t N) {
+  if (K <= 0 || N <= 0) return 0;
+  if ((K / 16) * N * 4 >= (int64_t(1) << 31) || N > (int64_t(1) << 24)) return 0;
+  const int64_t by_q = ((int64_t(1) << 31) - 1) / K;
+  const int64_t by_y = ((int64_t(1) << 31) - 1) / (4 * N);
+  const int64_t slice = ((by_q < by_y ? by_q : by_y) / 256) * 256;
+  return slice < 256 ? 0 : slice;
+}
 
 // Interleave the packed gate and up projections of a GLU, [K/16][L] each,
 // into [K/16][2L] blocks of 16 columns (gate, up, gate, ...); L % 16 == 0.

@@ -40,8 +40,10 @@ def test_library_exports_every_declared_symbol(mmf):
 def test_status_strings_and_sizes(mmf):
     assert mmf.mmf_version() >= 1
     assert mmf.mmf_status_string(0) == "MMF_OK"
-    for s in range(1, 7):
+    for s in range(1, 8):
         assert mmf.mmf_status_string(s).startswith("MMF_ERR")
+    assert "DTYPE" in mmf.mmf_status_string(4) and "HIP" in mmf.mmf_status_string(5)
+    assert "WORKSPACE" in mmf.mmf_status_string(6)
     assert "unknown" in mmf.mmf_status_string(99)
     assert mmf.mmf_packed_weight_bytes(6144, 2048) == 6144 * 2048 // 4
     assert mmf.mmf_packed_weight_bytes(3, 48) == 3 * 3 * 4
@@ -77,7 +79,8 @@ def _c(mmf):
 def test_bad_k_is_rejected(mmf, K):
     lib = _c(mmf)
     assert lib.mmf_bitlinear_fwd(A, B, C, D, E, 4, K, 4, S) == 2
-    assert lib.mmf_act_quant(A, B, C, D, E, 4, K, S) == 2
+    assert lib.mmf_act_quant(A, B, C, D, 4, K, S) == 2
+    assert lib.mmf_act_quant_ex(A, 0, B, C, D, E, 4, K, S) == 2
     assert lib.mmf_ternarize_weights(A, 4, K, B, C, S) == 2
     assert lib.mmf_ternary_gemm_i32(A, B, C, 4, K, 4, S) == 2
     assert lib.mmf_ternary_gemm_dequant(A, B, C, D, E, A, 4, K, 4, S) == 2
@@ -96,8 +99,9 @@ def test_null_pointers(mmf):
     assert lib.mmf_bitlinear_fwd(A, B, None, D, E, 4, 16, 4, S) == 1
     assert lib.mmf_bitlinear_fwd(A, B, C, None, E, 4, 16, 4, S) == 1
     assert lib.mmf_bitlinear_fwd(A, B, C, D, None, 4, 16, 4, S) == 1
-    assert lib.mmf_act_quant(A, None, None, D, E, 4, 16, S) == 1
-    assert lib.mmf_act_quant(A, None, C, None, E, 4, 16, S) == 1
+    assert lib.mmf_act_quant(A, None, None, D, 4, 16, S) == 1
+    assert lib.mmf_act_quant(A, None, C, None, 4, 16, S) == 1
+    assert lib.mmf_act_quant_f32(None, None, C, D, 4, 16, S) == 1
     assert lib.mmf_ternarize_weights(None, 4, 16, B, C, S) == 1
     assert lib.mmf_ternarize_weights(A, 4, 16, B, None, S) == 1
     assert lib.mmf_ternary_gemm_i32(A, None, C, 4, 16, 4, S) == 1
@@ -111,7 +115,8 @@ def test_misaligned_pointers(mmf):
     assert lib.mmf_bitlinear_fwd(A, BAD, C, D, E, 4, 16, 4, S) == 3
     assert lib.mmf_bitlinear_fwd(A, B, BAD, D, E, 4, 16, 4, S) == 3
     assert lib.mmf_bitlinear_fwd(A, B, C, D, BAD, 4, 16, 4, S) == 3
-    assert lib.mmf_act_quant(A, B, BAD, D, E, 4, 16, S) == 3
+    assert lib.mmf_act_quant(A, B, BAD, D, 4, 16, S) == 3
+    assert lib.mmf_act_quant_ex(A, 0, B, C, D, BAD, 4, 16, S) == 3
     assert lib.mmf_ternarize_weights(BAD, 4, 16, B, C, S) == 3
     assert lib.mmf_ternary_gemm_i32(A, B, BAD, 4, 16, 4, S) == 3
 
@@ -119,9 +124,9 @@ def test_misaligned_pointers(mmf):
 def test_workspace_checks(mmf):
     lib = _c(mmf)
     need = mmf.mmf_bitlinear_workspace_bytes(4, 16)
-    assert lib.mmf_bitlinear_fwd_ws(A, 0, B, C, D, E, 4, 16, 4, 0x100000, need - 1, S) == 4
-    assert lib.mmf_bitlinear_fwd_ws(A, 0, B, C, D, E, 4, 16, 4, 0x100010, need, S) == 4
-    assert lib.mmf_bitlinear_fwd_ws(A, 2, B, C, D, E, 4, 16, 4, 0x100000, need, S) == 6
+    assert lib.mmf_bitlinear_fwd_ws(A, 0, B, C, D, E, 4, 16, 4, 0x100000, need - 1, S) == 6
+    assert lib.mmf_bitlinear_fwd_ws(A, 0, B, C, D, E, 4, 16, 4, 0x100010, need, S) == 6
+    assert lib.mmf_bitlinear_fwd_ws(A, 2, B, C, D, E, 4, 16, 4, 0x100000, need, S) == 4
 
 
 def test_empty_shapes_are_noops(mmf):
@@ -129,7 +134,7 @@ def test_empty_shapes_are_noops(mmf):
     lib = _c(mmf)
     assert lib.mmf_bitlinear_fwd(None, None, None, None, None, 0, 16, 4, S) == 0
     assert lib.mmf_bitlinear_fwd(None, None, None, None, None, 4, 16, 0, S) == 0
-    assert lib.mmf_act_quant(None, None, None, None, None, 0, 16, S) == 0
+    assert lib.mmf_act_quant(None, None, None, None, 0, 16, S) == 0
     assert lib.mmf_ternarize_weights(None, 0, 16, None, None, S) == 0
     assert lib.mmf_ternary_gemm_i32(None, None, None, 0, 16, 5, S) == 0
 
@@ -162,9 +167,9 @@ def test_glu_argument_checks(mmf):
     assert lib.mmf_glu_pack(A, B, 32, 16, BAD, S) == 3
     # workspace variant
     need = mmf.mmf_bitlinear_workspace_bytes(4, 16)
-    assert lib.mmf_glu_fwd_ws(A, 0, B, C, D, E, 4, 16, 32, 0x100000, need - 1, S) == 4
+    assert lib.mmf_glu_fwd_ws(A, 0, B, C, D, E, 4, 16, 32, 0x100000, need - 1, S) == 6
     assert lib.mmf_glu_fwd_ws(A, 0, B, C, D, E, 4, 16, 32, None, need, S) == 1
-    assert lib.mmf_glu_fwd_ws(A, 3, B, C, D, E, 4, 16, 32, 0x100000, need, S) == 6
+    assert lib.mmf_glu_fwd_ws(A, 3, B, C, D, E, 4, 16, 32, 0x100000, need, S) == 4
     # empty shapes are no-ops
     assert lib.mmf_glu_fwd(None, None, None, None, None, 0, 16, 32, S) == 0
     assert lib.mmf_glu_fwd(None, None, None, None, None, 4, 16, 0, S) == 0
@@ -179,7 +184,7 @@ def test_bias_argument_checks(mmf):
     assert lib.mmf_bitlinear_fwd_bias(A, 0, B, C, D, E, A, 4, 16, 6, S) == 2    # N % 4
     assert lib.mmf_bitlinear_fwd_bias(A, 0, B, C, D, None, A, 4, 16, 8, S) == 1
     assert lib.mmf_bitlinear_fwd_bias(A, 0, B, C, D, BAD, A, 4, 16, 8, S) == 3
-    assert lib.mmf_bitlinear_fwd_bias(A, 2, B, C, D, E, A, 4, 16, 8, S) == 6
+    assert lib.mmf_bitlinear_fwd_bias(A, 2, B, C, D, E, A, 4, 16, 8, S) == 4
     assert lib.mmf_bitlinear_fwd_bias(A, 0, B, C, D, E, A, 4, 24, 8, S) == 2
     assert lib.mmf_bitlinear_fwd_bias(None, 0, None, None, None, None, None, 0, 16, 8, S) == 0
 
@@ -197,11 +202,11 @@ def test_mlgru_argument_checks(mmf):
     assert lib.mmf_mlgru_proj(A, 0, B, C, D, E, A, None, 4, 16, 16, None, 0, S) == 1
     assert lib.mmf_mlgru_proj(A, 0, B, C, D, BAD, A, B, 4, 16, 16, None, 0, S) == 3
     assert lib.mmf_mlgru_proj(A, 0, B, C, D, E, BAD, B, 4, 16, 16, None, 0, S) == 3
-    assert lib.mmf_mlgru_proj(A, 5, B, C, D, E, A, B, 4, 16, 16, None, 0, S) == 6
+    assert lib.mmf_mlgru_proj(A, 5, B, C, D, E, A, B, 4, 16, 16, None, 0, S) == 4
     need = mmf.mmf_mlgru_proj_workspace_bytes(4, 16, 16)
     assert need > 0 and need % 256 == 0
-    assert lib.mmf_mlgru_proj(A, 0, B, C, D, E, A, B, 4, 16, 16, W, need - 1, S) == 4
-    assert lib.mmf_mlgru_proj(A, 0, B, C, D, E, A, B, 4, 16, 16, W + 16, need, S) == 4
+    assert lib.mmf_mlgru_proj(A, 0, B, C, D, E, A, B, 4, 16, 16, W, need - 1, S) == 6
+    assert lib.mmf_mlgru_proj(A, 0, B, C, D, E, A, B, 4, 16, 16, W + 16, need, S) == 6
     assert lib.mmf_mlgru_proj(None, 0, None, None, None, None, None, None, 0, 16, 16, None, 0, S) == 0
     assert lib.mmf_mlgru_proj_q(A, B, C, D, E, A, B, C, 4, 16, 24, S) == 2
     assert lib.mmf_mlgru_proj_q(A, B, None, D, E, A, B, C, 4, 16, 16, S) == 1
@@ -222,7 +227,7 @@ def test_mlgru_argument_checks(mmf):
     assert mmf.mmf_mlgru_scan_workspace_bytes(4, 16, 64) == 0
     need = mmf.mmf_mlgru_scan_workspace_bytes(1, 2048, 2048)
     assert need >= 3 * 2048 * 4 * 2 and need % 256 == 0
-    assert lib.mmf_mlgru_scan(A, B, C, D, 1, 2048, 2048, W, need - 1, S) == 4
+    assert lib.mmf_mlgru_scan(A, B, C, D, 1, 2048, 2048, W, need - 1, S) == 6
     # whole mixer
     assert lib.mmf_mlgru_fwd(A, 0, B, C, D, E, A, B, C, D, E, A, B, C, 1, 2, 24, None, 0, S) == 2
     assert lib.mmf_mlgru_fwd(A, 0, B, C, D, E, A, B, C, D, None, A, B, C, 1, 2, 32, None, 0, S) == 1
@@ -230,10 +235,10 @@ def test_mlgru_argument_checks(mmf):
     assert lib.mmf_mlgru_fwd(A, 0, B, C, D, E, A, B, C, D, E, A, B, None, 1, 2, 32, None, 0, S) == 1
     assert lib.mmf_mlgru_fwd(A, 0, B, C, D, E, A, BAD, C, D, E, A, B, C, 1, 2, 32, None, 0, S) == 3
     assert lib.mmf_mlgru_fwd(A, 0, B, C, D, E, A, B, C, D, E, A, BAD, C, 1, 2, 32, None, 0, S) == 3
-    assert lib.mmf_mlgru_fwd(A, 9, B, C, D, E, A, B, C, D, E, A, B, C, 1, 2, 32, None, 0, S) == 6
+    assert lib.mmf_mlgru_fwd(A, 9, B, C, D, E, A, B, C, D, E, A, B, C, 1, 2, 32, None, 0, S) == 4
     need = mmf.mmf_mlgru_workspace_bytes(1, 2, 32)
     assert need >= 2 * 32 * 16 and need % 256 == 0
-    assert lib.mmf_mlgru_fwd(A, 0, B, C, D, E, A, B, C, D, E, A, B, C, 1, 2, 32, W, need - 1, S) == 4
+    assert lib.mmf_mlgru_fwd(A, 0, B, C, D, E, A, B, C, D, E, A, B, C, 1, 2, 32, W, need - 1, S) == 6
     assert lib.mmf_mlgru_fwd(None, 0, None, None, None, None, None, None, None, None, None, None,
                              None, None, 0, 2, 32, None, 0, S) == 0
     assert mmf.mmf_mlgru_workspace_bytes(1, 2048, 2048) >= 2048 * 2048 * 16
@@ -250,10 +255,10 @@ def test_train_and_bwd_argument_checks(mmf):
     assert lib.mmf_bitlinear_train_fwd(A, 0, B, None, None, E, A, B, C, D, E, 4, 16, 8, None, 0, S) == 1
     assert lib.mmf_bitlinear_train_fwd(A, 0, B, C, None, E, A, B, None, D, E, 4, 16, 8, None, 0, S) == 1
     assert lib.mmf_bitlinear_train_fwd(A, 0, B, C, None, E, A, B, C, D, BAD, 4, 16, 8, None, 0, S) == 3
-    assert lib.mmf_bitlinear_train_fwd(A, 7, B, C, None, E, A, B, C, D, E, 4, 16, 8, None, 0, S) == 6
+    assert lib.mmf_bitlinear_train_fwd(A, 7, B, C, None, E, A, B, C, D, E, 4, 16, 8, None, 0, S) == 4
     need = mmf.mmf_bitlinear_train_workspace_bytes(4, 16, 8)
     assert need > 0 and need % 256 == 0
-    assert lib.mmf_bitlinear_train_fwd(A, 0, B, C, None, E, A, B, C, D, E, 4, 16, 8, W, need - 1, S) == 4
+    assert lib.mmf_bitlinear_train_fwd(A, 0, B, C, None, E, A, B, C, D, E, 4, 16, 8, W, need - 1, S) == 6
     assert lib.mmf_bitlinear_train_fwd(None, 0, None, None, None, None, None, None, None, None, None,
                                        0, 16, 8, None, 0, S) == 0
     # backward
@@ -262,9 +267,66 @@ def test_train_and_bwd_argument_checks(mmf):
     assert lib.mmf_bitlinear_bwd(A, B, 0, C, None, E, A, B, C, D, E, A, B, 4, 16, 8, None, 0, S) == 1
     assert lib.mmf_bitlinear_bwd(A, B, 0, C, D, E, A, B, C, D, None, A, B, 4, 16, 8, None, 0, S) == 1
     assert lib.mmf_bitlinear_bwd(A, B, 0, C, D, E, A, B, C, D, E, BAD, B, 4, 16, 8, None, 0, S) == 3
-    assert lib.mmf_bitlinear_bwd(A, B, 2, C, D, E, A, B, C, D, E, A, B, 4, 16, 8, None, 0, S) == 6
+    assert lib.mmf_bitlinear_bwd(A, B, 2, C, D, E, A, B, C, D, E, A, B, 4, 16, 8, None, 0, S) == 4
     need = mmf.mmf_bitlinear_bwd_workspace_bytes(4, 16, 8)
     assert need >= 16 * 8 * 2 + 4 * 16 * 6 and need % 256 == 0
-    assert lib.mmf_bitlinear_bwd(A, B, 0, C, D, E, A, B, C, D, E, A, B, 4, 16, 8, W, need - 1, S) == 4
+    assert lib.mmf_bitlinear_bwd(A, B, 0, C, D, E, A, B, C, D, E, A, B, 4, 16, 8, W, need - 1, S) == 6
     assert lib.mmf_bitlinear_bwd(None, None, 0, None, None, None, None, None, None, None, None, None,
                                  None, 0, 16, 8, None, 0, S) == 0
+
+
+def test_status_codes_follow_the_boundary():
+    """The numbering the boundary fixes: OK 0, NULL 1, SHAPE 2, ALIGN 3,
+    DTYPE 4, HIP 5 (then this library's WORKSPACE 6 and ARG 7)."""
+    text = open(HEADER).read()
+    codes = dict(re.findall(r"#define (MMF_[A-Z_0-9]+) (-?\d+)", text))
+    want = {"MMF_OK": "0", "MMF_ERR_NULL": "1", "MMF_ERR_SHAPE": "2", "MMF_ERR_ALIGN": "3",
+            "MMF_ERR_DTYPE": "4", "MMF_ERR_HIP": "5", "MMF_ERR_WORKSPACE": "6", "MMF_ERR_ARG": "7"}
+    for k, v in want.items():
+        assert codes.get(k) == v, (k, codes.get(k))
+
+
+def test_boundary_signatures():
+    """The three calls of the boundary keep their argument lists:
+    mmf_ternarize_weights(W, N, K, Wpacked, w_scale, stream),
+    mmf_bitlinear_fwd(x, gamma, Wpacked, w_scale, y, M, K, N, stream),
+    mmf_act_quant(x, gamma, q, a_scale, M, K, stream)."""
+    text = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+
+    def params(name):
+        m = re.search(r"\b" + name + r"\s*\(([^)]*)\)", text)
+        assert m, name
+        return [re.findall(r"(\w+)\s*$", p.strip())[0] for p in m.group(1).split(",")]
+
+    assert params("mmf_ternarize_weights") == ["W", "N", "K", "Wpacked", "w_scale", "stream"]
+    assert params("mmf_bitlinear_fwd") == ["x", "gamma", "Wpacked", "w_scale", "y", "M", "K", "N",
+                                           "stream"]
+    assert params("mmf_act_quant") == ["x", "gamma", "q", "a_scale", "M", "K", "stream"]
+    assert params("mmf_act_quant_f32") == ["x", "gamma", "q", "a_scale", "M", "K", "stream"]
+    assert params("mmf_ternary_gemm_i32") == ["q", "Wpacked", "acc", "M", "K", "N", "stream"]
+
+
+def test_shapes_past_the_kernel_offsets_are_rejected_up_front(mmf):
+    """Shapes the contraction kernel cannot address with its 32-bit offsets
+    return MMF_ERR_SHAPE from the host checks, before anything is enqueued
+    (the stand-in pointers are never dereferenced, so reaching a launch would
+    fault the test process instead)."""
+    lib = _c(mmf)
+    W = 0x100000
+    big_n = 1 << 21            # M = 41 takes the MFMA kernel: output row slices < 256 rows
+    huge = (1 << 27) + 16      # packed weights (K/16) * N * 4 >= 2^31 at K = 256
+    for M, K, N in ((41, 16, big_n), (4096, 256, huge), (41, 16, (1 << 24) + 4)):
+        assert lib.mmf_bitlinear_fwd(A, B, C, D, E, M, K, N, S) == 2
+        assert lib.mmf_bitlinear_fwd_f32(A, B, C, D, E, M, K, N, S) == 2
+        assert lib.mmf_bitlinear_fwd_ws(A, 0, B, C, D, E, M, K, N, W, 1 << 40, S) == 2
+        assert lib.mmf_ternary_gemm_dequant(A, B, C, D, E, A, M, K, N, S) == 2
+        assert lib.mmf_ternary_gemm_i32(A, B, C, M, K, N, S) == 2
+        assert lib.mmf_bitlinear_fwd_bias(A, 0, B, C, D, E, A, M, K, N, S) == 2
+        assert lib.mmf_bitlinear_train_fwd(A, 0, B, C, None, E, A, B, C, D, E, M, K, N, None, 0, S) == 2
+        assert lib.mmf_glu_fwd(A, B, C, D, E, M, K, N // 2, S) == 2
+        assert lib.mmf_ternary_gemm_glu(A, B, C, D, E, A, M, K, N // 2, S) == 2
+    # the MLGRU projection: 3d columns past the MFMA kernel's slice limit
+    d = 1 << 20
+    assert lib.mmf_mlgru_proj(A, 0, B, C, D, E, A, B, 41, 16, d, None, 0, S) == 2
+    assert lib.mmf_mlgru_proj_q(A, B, C, D, E, A, B, C, 41, 16, d, S) == 2
+
