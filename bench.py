@@ -131,7 +131,7 @@ CSRC = os.path.join(ROOT, "paper_2406_02528_amd", "csrc")
 # the files whose text decides what a kernel does; a recorded traffic figure
 # is used only while their digest is unchanged
 KERNEL_SOURCES = {
-    "decode_kernel": ("decode.hip", "mmf_device.h"),
+    "decode_kernel": ("decode_impl.h", "decode_bf16.hip", "mmf_device.h"),
     "gemm_kernel": ("gemm.hip", "mmf_device.h"),
 }
 CALIB_BYTES = 1 << 28          # bytes read and written by one calibration copy

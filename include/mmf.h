@@ -133,10 +133,9 @@ int mmf_act_quant_ex(const void *x, int x_is_f32, const float *gamma, int8_t *q,
  *   y[m][n] = a_scale[m] * w_scale * sum_k q[m][k] t[n][k]
  * with q, a_scale from the act-quant step above and t from Wpacked.  The
  * integer sum is exact; the product is fp32 (a_scale[m] * w_scale first).
- * Up to 40 tokens take the decode kernel in launches of at most 8 tokens
- * (VALU dot products for one token, 16x16x64 int8 MFMA for two to eight),
- * larger M the
- * int8 MFMA kernel.  Allocates its M*K + 8*M byte scratch stream-ordered
+ * Up to 64 tokens take the decode kernel in launches of at most 16 tokens
+ * (16x16x64 int8 MFMA over 16 columns by the token rows; weights streamed
+ * once per launch), larger M the int8 MFMA GEMM kernel.  Allocates its M*K + 8*M byte scratch stream-ordered
  * (hipMallocAsync); mmf_bitlinear_fwd_ws takes caller scratch instead.
  * x: [M][K] bf16 bits; gamma: [K] or NULL; Wpacked: [K/16][N]; w_scale: [1];
  * y: [M][N] float32 out.
@@ -213,9 +212,9 @@ int mmf_ternary_gemm_i32(const int8_t *q, const uint32_t *Wpacked,
  *
  * mmf_glu_fwd: x [M][K] bf16 bits (mmf_glu_fwd_f32: float32); gamma [K] or
  * NULL; Wgu_packed [K/16][2L] from mmf_glu_pack; w_scales [2] = gate, up;
- * p [M][L] float32 out.  Up to 40 tokens run the fused decode kernel with
- * the same SiLU(g) * u epilogue (launches of at most 8 tokens; the result is
- * bit-identical to the MFMA kernel's), larger M the int8 MFMA kernel.  Allocates the
+ * p [M][L] float32 out.  Up to 64 tokens run the fused decode kernel with
+ * the same SiLU(g) * u epilogue (launches of at most 16 tokens; the result is
+ * bit-identical to the GEMM kernel's), larger M the int8 MFMA GEMM kernel.  Allocates the
  * same stream-ordered scratch as mmf_bitlinear_fwd; mmf_glu_fwd_ws takes
  * caller scratch of mmf_bitlinear_workspace_bytes(M, K) bytes instead.
  */
@@ -285,8 +284,8 @@ int mmf_bitlinear_fwd_bias(const void *x, int x_is_f32, const float *gamma,
  * with s evaluated as for the GLU gate (hardware exp2 and reciprocal). The
  * recurrence's output gate o' = g * s(h) uses the same s.
  * x [M][K] bf16 bits or float32 (x_is_f32); bias [3d] or NULL; lb [d] or
- * NULL.  M <= 40 runs the fused decode kernel (launches of at most 8 tokens),
- * larger M the int8 MFMA kernel. */
+ * NULL.  M <= 64 runs the fused decode kernel (launches of at most 16
+ * tokens), larger M the int8 MFMA GEMM kernel. */
 size_t mmf_mlgru_proj_workspace_bytes(int64_t M, int64_t K, int64_t d);
 int mmf_mlgru_proj(const void *x, int x_is_f32, const float *gamma, const uint32_t *Wfcg,
                    const float *w_scales, const float *bias, const float *lb, float *fcg,
@@ -372,9 +371,10 @@ int mmf_bitlinear_bwd(const uint16_t *dO, const void *x, int x_is_f32, const flo
 
 /*
  * Kernel selection for the contraction: MMF_PATH_AUTO (decode kernel for
- * M <= 40, in launches of at most 8 tokens; MFMA kernel otherwise), MMF_PATH_GEMV or MMF_PATH_GEMM force one
- * kernel for every M (the decode kernel handles at most 8 tokens per launch
- * and is launched once per 8-token slice when forced).  Process-wide; returns
+ * M <= 64, in launches of at most 16 tokens; the GEMM kernel otherwise),
+ * MMF_PATH_GEMV or MMF_PATH_GEMM force one kernel for every M (the decode
+ * kernel handles at most 16 tokens per launch and is launched once per
+ * 16-token slice when forced).  Process-wide; returns
  * the previous setting, or -MMF_ERR_ARG for an unknown value.
  */
 #define MMF_PATH_AUTO 0

@@ -12,7 +12,7 @@ namespace {
 
 constexpr int64_t kMaxK = int64_t(1) << 20;
 constexpr int64_t kMaxMN = 0x7FFFFFFF;
-constexpr int kDecodeMaxTokens = 8;
+constexpr int kDecodeMaxTokens = mmf::kDecodeMaxTokens;
 constexpr size_t kScratchAlign = 256;
 
 std::atomic<int> g_path{MMF_PATH_AUTO};
@@ -43,15 +43,16 @@ FwdScratch fwd_scratch(int64_t M, int64_t K) {
 }
 
 // Automatic choice: up to kDecodeSliceMaxTokens tokens run as decode launches
-// of at most 8 tokens each, when the decode kernel takes such a slice (its
-// LDS holds q of 8 tokens up to K = 7680).  Measured (K = 2048, N = 2048 /
-// 6144 / 11264): the MFMA kernel takes >= 26 us at any small M (each output
-// tile's k loop runs on one CU), the decode slices ~5 us each, so the slices
-// win up to ~44 tokens (M = 16: 9.9 vs 26.3 us; M = 32: 19.5 vs 27.3;
-// M = 48: 29.2 vs 28.1).  MMF_PATH_GEMV forces the decode kernels for every
-// M (slices it cannot hold then go to the gemv kernel, which reads q from
-// global memory); MMF_PATH_GEMM forces the MFMA kernel.
-constexpr int64_t kDecodeSliceMaxTokens = 40;
+// of at most 16 tokens each, when the decode kernel takes such a slice (its
+// LDS holds q of 16 tokens up to K = 7680).  Measured at K = 2048, N = 6144:
+// the MFMA kernel takes >= 26 us at any small M (each output tile's k loop
+// runs on one CU, and 64 tokens fill few tiles), the decode launches 3.5 us
+// for one token, 6.2 us for 16, so M = 32: 12.4 us against 27.3; M = 40:
+// 17.3 against 27.3; M = 64: ~25 against 28.9.  MMF_PATH_GEMV forces the
+// decode kernels for every M (slices they cannot hold then go to the gemv
+// kernel, which reads q from global memory); MMF_PATH_GEMM forces the MFMA
+// kernel.
+constexpr int64_t kDecodeSliceMaxTokens = 64;
 bool use_decode(int64_t M, int64_t K, int64_t N, bool from_x, bool x_is_f32) {
   const int p = g_path.load(std::memory_order_relaxed);
   if (p == MMF_PATH_GEMV) return true;
@@ -61,7 +62,7 @@ bool use_decode(int64_t M, int64_t K, int64_t N, bool from_x, bool x_is_f32) {
                           x_is_f32);
 }
 
-// Contraction from quantised activations.  Decode-sized slices of at most 8
+// Contraction from quantised activations.  Decode-sized slices of at most 16
 // tokens keep q in LDS when it fits, else read it from global memory.
 hipError_t contract(const mmf::ContractArgs& a, hipStream_t stream) {
   if (!use_decode(a.M, a.K, a.N, false, false)) return mmf::launch_gemm(a, stream);
@@ -87,7 +88,7 @@ hipError_t contract(const mmf::ContractArgs& a, hipStream_t stream) {
 }
 
 // The whole forward runs as fused decode launches (no scratch) when every
-// slice of at most 8 tokens fits the fused kernel.
+// slice of at most 16 tokens fits the fused kernel.
 bool fused_decode(int64_t M, int64_t K, int64_t N, bool x_is_f32) {
   if (!use_decode(M, K, N, true, x_is_f32)) return false;
   const int64_t mt = M < kDecodeMaxTokens ? M : kDecodeMaxTokens;
@@ -263,7 +264,7 @@ int glu_alloc(const void* x, bool x_is_f32, const float* gamma, const uint32_t* 
 
 // ---- affine forward (bias and per-segment activations after the dequant) ----
 
-// Fused decode launches when every slice of at most 8 tokens fits the fused
+// Fused decode launches when every slice of at most 16 tokens fits the fused
 // kernel, else activation quantisation into `scratch` (fwd_scratch) and the
 // MFMA kernel for every M.
 int run_affine(const void* x, bool x_is_f32, const float* gamma, const uint32_t* Wpacked,

@@ -61,10 +61,12 @@ struct ContractArgs {
 // M <= 8 per launch (larger M is sliced).
 hipError_t launch_gemv(const ContractArgs& a, hipStream_t stream);
 
-// Fused decode forward: up to 8 tokens, q kept in LDS (M*K <= kDecodeMaxLdsQ).
-// With q == nullptr it normalises and quantises x itself (dequant epilogue
-// only); otherwise it contracts the given q / a_scale / q_rowsum.
-constexpr int kDecodeMaxLdsQ = 61440;
+// Fused decode forward: up to 16 tokens per launch, q kept in LDS (the q
+// region of M rows of K + 16 bytes, in whole KB, at most kDecodeMaxLdsQ).
+// With q == nullptr it normalises and quantises x itself; otherwise it
+// contracts the given q / a_scale / q_rowsum.
+constexpr int kDecodeMaxTokens = 16;
+constexpr int kDecodeMaxLdsQ = 131072;
 struct DecodeArgs {
   const void* x;            // [M][K] bf16 or f32 (q == nullptr)
   bool x_is_f32;
@@ -75,7 +77,7 @@ struct DecodeArgs {
   const uint32_t* Wpacked;  // [K/16][N]
   const float* w_scale;     // [1]
   void* out;                // [M][N]
-  int64_t M;                // 1..8
+  int64_t M;                // 1..kDecodeMaxTokens
   int K;
   int64_t N;
   Epilogue epilogue;

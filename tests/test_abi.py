@@ -313,9 +313,9 @@ def test_shapes_past_the_kernel_offsets_are_rejected_up_front(mmf):
     fault the test process instead)."""
     lib = _c(mmf)
     W = 0x100000
-    big_n = 1 << 21            # M = 41 takes the MFMA kernel: output row slices < 256 rows
+    big_n = 1 << 21            # M = 65 takes the MFMA kernel: output row slices < 256 rows
     huge = (1 << 27) + 16      # packed weights (K/16) * N * 4 >= 2^31 at K = 256
-    for M, K, N in ((41, 16, big_n), (4096, 256, huge), (41, 16, (1 << 24) + 4)):
+    for M, K, N in ((65, 16, big_n), (4096, 256, huge), (65, 16, (1 << 24) + 4)):
         assert lib.mmf_bitlinear_fwd(A, B, C, D, E, M, K, N, S) == 2
         assert lib.mmf_bitlinear_fwd_f32(A, B, C, D, E, M, K, N, S) == 2
         assert lib.mmf_bitlinear_fwd_ws(A, 0, B, C, D, E, M, K, N, W, 1 << 40, S) == 2
@@ -327,6 +327,6 @@ def test_shapes_past_the_kernel_offsets_are_rejected_up_front(mmf):
         assert lib.mmf_ternary_gemm_glu(A, B, C, D, E, A, M, K, N // 2, S) == 2
     # the MLGRU projection: 3d columns past the MFMA kernel's slice limit
     d = 1 << 20
-    assert lib.mmf_mlgru_proj(A, 0, B, C, D, E, A, B, 41, 16, d, None, 0, S) == 2
-    assert lib.mmf_mlgru_proj_q(A, B, C, D, E, A, B, C, 41, 16, d, S) == 2
+    assert lib.mmf_mlgru_proj(A, 0, B, C, D, E, A, B, 65, 16, d, None, 0, S) == 2
+    assert lib.mmf_mlgru_proj_q(A, B, C, D, E, A, B, C, 65, 16, d, S) == 2
 

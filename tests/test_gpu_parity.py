@@ -357,12 +357,12 @@ def test_decode_fallback_shapes(mmf, M, K, N):
 
 @pytest.mark.parametrize("M,K,N,f32", [(1, 4096, 324, False), (2, 4112, 1000, False), (1, 8192, 96, True),
                                        (2, 5120, 15360, False), (1, 4608, 4, True)])
-def test_decode_lds_weight_staging(mmf, M, K, N, f32):
-    """Decode shapes of at most two tokens with at least 256 word rows and
-    N % 4 == 0 stage each workgroup's weight block in LDS by LDS-DMA: ragged
-    column tails (N % 64 != 0), K/16 not a multiple of 4 (the last copy group
-    reads past the array: zeros), bf16 and fp32 activations, and through the
-    affine epilogue (a bias and the three MLGRU activations)."""
+def test_decode_large_blocks(mmf, M, K, N, f32):
+    """Decode shapes with many word rows per workgroup (eight weight loads in
+    flight per lane, or more in groups of eight): ragged column tails
+    (N % 64 != 0), K/16 not a multiple of 4 (the last step's missing word
+    rows read as zero), bf16 and fp32 activations, and through the affine
+    epilogue (a bias)."""
     rs = np.random.default_rng(M * 13 + K + N)
     bits, xf, g, W = workloads.random_case(rs, M, K, N)
     x_form = xf if f32 else bits
@@ -372,7 +372,7 @@ def test_decode_lds_weight_staging(mmf, M, K, N, f32):
     acc_ref = oracle.ternary_accumulate(case.q_ref, case.t)
     y_ref = oracle.dequant(acc_ref, case.a_ref, case.ws_ref)
     case.upload()
-    log(f"[lds weights] M={M} K={K} N={N} f32={f32}")
+    log(f"[decode large blocks] M={M} K={K} N={N} f32={f32}")
     Wp, ws = gpu_weights(mmf, case)
     check_weights(case, Wp, ws)
     q, a, r = gpu_act(mmf, case)
@@ -381,7 +381,7 @@ def test_decode_lds_weight_staging(mmf, M, K, N, f32):
     flip[flip_rows] = True
     y = run_forward(mmf, case, Wp, ws, "auto").cpu().numpy()
     compare_y(y, y_ref, acc_ref, flip)
-    # the same staging under the affine epilogue: y + b must equal the plain
+    # the same shape under the affine epilogue: y + b must equal the plain
     # forward plus b, rounded once more
     b = rs.uniform(-0.5, 0.5, N).astype(np.float32)
     yb = torch.empty((M, N), dtype=torch.float32, device=dev())
@@ -431,3 +431,36 @@ def test_decode_matrix_core_layouts(mmf, M, K, N, f32):
         torch.cuda.synchronize()
         expect = (y.astype(np.float32) + b).astype(np.float32)
         assert np.array_equal(yb.cpu().numpy(), expect)
+
+
+@pytest.mark.parametrize("M,K,N,f32", [(9, 2048, 6144, False), (15, 2064, 1000, False), (16, 2048, 6144, False),
+                                       (16, 1024, 520, True), (12, 4096, 640, False), (16, 7680, 192, False),
+                                       (33, 2048, 2048, False), (40, 1040, 96, True)])
+def test_decode_up_to_16_tokens_per_launch(mmf, M, K, N, f32):
+    """Nine to sixteen tokens run as one launch of the decode kernel (all 16
+    rows of the matrix-core operand carry tokens; rows past M read as zero):
+    9, 15 and 16 tokens fused from x; 12 x 4096 and 16 x 7680, whose rows
+    need more registers than the fused kernel holds, from act-quant's q
+    copied into LDS (16 x 7680 is the largest q region); 33 and 40 tokens as
+    launches of 16, 16 and the rest."""
+    rs = np.random.default_rng(M * 17 + K + N)
+    bits, xf, g, W = workloads.random_case(rs, M, K, N)
+    x_form = xf if f32 else bits
+    case = Case(x_form, xf, g, W, f"dec16 M{M}K{K}N{N}")
+    case.oracle_weights()
+    case.oracle_act()
+    acc_ref = oracle.ternary_accumulate(case.q_ref, case.t)
+    y_ref = oracle.dequant(acc_ref, case.a_ref, case.ws_ref)
+    case.upload()
+    log(f"[decode 16] M={M} K={K} N={N} f32={f32}")
+    Wp, ws = gpu_weights(mmf, case)
+    check_weights(case, Wp, ws)
+    q, a, r = gpu_act(mmf, case)
+    qn, flip_rows, _ = check_act(case, q, a, r)
+    flip = np.zeros(M, bool)
+    flip[flip_rows] = True
+    for path in ("auto", "gemv"):
+        acc = run_i32(mmf, torch.from_numpy(case.q_ref).to(dev()), Wp, M, N, path).cpu().numpy()
+        assert np.array_equal(acc, acc_ref), path
+        y = run_forward(mmf, case, Wp, ws, path).cpu().numpy()
+        compare_y(y, y_ref, acc_ref, flip)
