@@ -164,6 +164,28 @@ int mmf_bitlinear_fwd_ws(const void *x, int x_is_f32, const float *gamma,
                          hipStream_t stream);
 
 /*
+ * mmf_bitlinear_fwd for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same kernels and results as mmf_bitlinear_fwd_ws, with the
+ * scratch (q, a_scale, q_rowsum: mmf_bitlinear_workspace_bytes(M, K) bytes)
+ * in a static device array of mmf_bitlinear_noalloc_max_bytes() = 64 MiB
+ * that each GPU the library runs on holds until the process ends.  No call
+ * allocates or frees memory; the array's address is looked up once per
+ * device, on the first call there.  Calls that need more scratch than the
+ * array holds return MMF_ERR_WORKSPACE before anything is enqueued (up to 64
+ * tokens the fused decode kernel needs none).  Every call on a GPU shares that
+ * GPU's array: calls that overlap on one GPU (on different streams, or from
+ * different host threads) race; serialise them.  The array keeps the last
+ * call's contents, which every call overwrites before reading.
+ * x_is_f32: 0 = bf16 x, 1 = float32 x (MMF_ERR_DTYPE otherwise).
+ */
+size_t mmf_bitlinear_noalloc_max_bytes(void);
+int mmf_bitlinear_fwd_noalloc(const void *x, int x_is_f32, const float *gamma,
+                              const uint32_t *Wpacked, const float *w_scale,
+                              float *y, int64_t M, int64_t K, int64_t N,
+                              hipStream_t stream);
+
+/*
  * Ternary accumulation and dequantisation from already-quantised activations
  * (the contraction stage of the forward on its own; Sec. "MatMul-free Dense
  * Layers with Ternary Weights" and Algorithm 1):

@@ -52,6 +52,9 @@ _SIGNATURES = {
     "mmf_bitlinear_workspace_bytes": ([_I64, _I64], _SZ),
     "mmf_bitlinear_fwd_ws": ([_P, ctypes.c_int, _P, _P, _P, _P, _I64, _I64, _I64, _P, _SZ, _P],
                              ctypes.c_int),
+    "mmf_bitlinear_noalloc_max_bytes": ([], _SZ),
+    "mmf_bitlinear_fwd_noalloc": ([_P, ctypes.c_int, _P, _P, _P, _P, _I64, _I64, _I64, _P],
+                                  ctypes.c_int),
     "mmf_ternary_gemm_dequant": ([_P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _P], ctypes.c_int),
     "mmf_ternary_gemm_i32": ([_P, _P, _P, _I64, _I64, _I64, _P], ctypes.c_int),
     "mmf_set_path": ([ctypes.c_int], ctypes.c_int),
@@ -221,6 +224,26 @@ def mmf_bitlinear_fwd_ws(x: torch.Tensor, gamma: torch.Tensor | None, Wpacked: t
     _check(_lib.mmf_bitlinear_fwd_ws(_ptr(x), int(is_f32), _ptr(gamma), _ptr(Wpacked),
                                      _ptr(w_scale), _ptr(y), M, K, N, _ptr(workspace),
                                      workspace.numel(), _stream(stream)))
+
+
+def mmf_bitlinear_noalloc_max_bytes() -> int:
+    return int(_lib.mmf_bitlinear_noalloc_max_bytes())
+
+
+def mmf_bitlinear_fwd_noalloc(x: torch.Tensor, gamma: torch.Tensor | None, Wpacked: torch.Tensor,
+                              w_scale: torch.Tensor, y: torch.Tensor, stream=None) -> None:
+    """The fused forward with the library's static device scratch (allocates nothing)."""
+    M, K = x.shape
+    N = Wpacked.shape[1]
+    is_f32 = _x_kind(x)
+    _need(x, "x", x.dtype, (M, K))
+    if gamma is not None:
+        _need(gamma, "gamma", torch.float32, (K,))
+    _need(Wpacked, "Wpacked", torch.int32, (K // 16, N))
+    _need(w_scale, "w_scale", torch.float32, (1,))
+    _need(y, "y", torch.float32, (M, N))
+    _check(_lib.mmf_bitlinear_fwd_noalloc(_ptr(x), int(is_f32), _ptr(gamma), _ptr(Wpacked),
+                                          _ptr(w_scale), _ptr(y), M, K, N, _stream(stream)))
 
 
 def mmf_ternary_gemm_dequant(q: torch.Tensor, a_scale: torch.Tensor, q_rowsum: torch.Tensor,

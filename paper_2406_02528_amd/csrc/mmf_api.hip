@@ -4,6 +4,7 @@
 #include <atomic>
 #include <cstdint>
 #include <cstring>
+#include <mutex>
 
 #include "mmf.h"
 #include "mmf_launch.h"
@@ -377,6 +378,41 @@ BwdScratch bwd_scratch(int64_t M, int64_t K, int64_t N) {
   return s;
 }
 
+// ---- the forward without allocation (mmf_bitlinear_fwd_noalloc) ----
+//
+// Its scratch (q, a_scale, q_rowsum: fwd_scratch) lives in a file-scope
+// device array, one copy per GPU, held until the process ends.  Host code
+// never passes the array's name to a kernel (on the host that name is only a
+// stand-in, not a device address): the address of each device's copy comes
+// from hipGetSymbolAddress, taken once per device with that device current
+// (on the entry point's first call there), and is used everywhere after.
+constexpr size_t kNoAllocScratchBytes = size_t(64) << 20;
+__device__ __align__(256) char scratch[kNoAllocScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+char* g_scratch_ptr[kMaxDevices] = {};
+
+// The current device's copy of `scratch`, or nullptr (with *status set) when
+// the device cannot be determined or the address lookup fails.
+char* device_scratch(int* status) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+    *status = MMF_ERR_HIP;
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr) {
+      *status = MMF_ERR_HIP;
+      return nullptr;
+    }
+    g_scratch_ptr[dev] = static_cast<char*>(p);
+  }
+  return g_scratch_ptr[dev];
+}
+
 }  // namespace
 
 extern "C" {
@@ -463,6 +499,25 @@ int mmf_bitlinear_fwd_ws(const void* x, int x_is_f32, const float* gamma,
     return MMF_ERR_WORKSPACE;
   return run_fwd(x, x_is_f32 == 1, gamma, Wpacked, w_scale, y, M, K, N,
                  static_cast<char*>(workspace), stream);
+}
+
+size_t mmf_bitlinear_noalloc_max_bytes(void) { return kNoAllocScratchBytes; }
+
+int mmf_bitlinear_fwd_noalloc(const void* x, int x_is_f32, const float* gamma,
+                              const uint32_t* Wpacked, const float* w_scale, float* y, int64_t M,
+                              int64_t K, int64_t N, hipStream_t stream) {
+  if (int st = check_dtype(x_is_f32)) return st;
+  if (int st = check_fwd(x, x_is_f32 == 1, gamma, Wpacked, w_scale, y, M, K, N)) return st;
+  if (M == 0 || N == 0) return MMF_OK;
+  const bool f32 = x_is_f32 == 1;
+  // few tokens: fused decode launches, which use no scratch
+  if (fused_decode(M, K, N, f32))
+    return hip_status(run_fused_decode(x, f32, gamma, Wpacked, w_scale, y, M, K, N, stream));
+  if (fwd_scratch(M, K).total > kNoAllocScratchBytes) return MMF_ERR_WORKSPACE;
+  int st = MMF_OK;
+  char* ws = device_scratch(&st);
+  if (ws == nullptr) return st;
+  return run_fwd(x, f32, gamma, Wpacked, w_scale, y, M, K, N, ws, stream);
 }
 
 int mmf_ternary_gemm_dequant(const int8_t* q, const float* a_scale, const int32_t* q_rowsum,

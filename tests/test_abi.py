@@ -330,3 +330,20 @@ def test_shapes_past_the_kernel_offsets_are_rejected_up_front(mmf):
     assert lib.mmf_mlgru_proj(A, 0, B, C, D, E, A, B, 65, 16, d, None, 0, S) == 2
     assert lib.mmf_mlgru_proj_q(A, B, C, D, E, A, B, C, 65, 16, d, S) == 2
 
+
+def test_noalloc_argument_checks(mmf):
+    """The forward without allocation: the same checks as the forward, and
+    scratch needs past its static array rejected before anything is
+    enqueued."""
+    lib = _c(mmf)
+    assert mmf.mmf_bitlinear_noalloc_max_bytes() == 64 << 20
+    assert lib.mmf_bitlinear_fwd_noalloc(A, 0, B, C, D, E, 4, 24, 8, S) == 2
+    assert lib.mmf_bitlinear_fwd_noalloc(A, 2, B, C, D, E, 4, 16, 8, S) == 4
+    assert lib.mmf_bitlinear_fwd_noalloc(None, 0, B, C, D, E, 4, 16, 8, S) == 1
+    assert lib.mmf_bitlinear_fwd_noalloc(A, 0, B, C, BAD, E, 4, 16, 8, S) == 1 or \
+        lib.mmf_bitlinear_fwd_noalloc(A, 0, B, C, D, BAD, 4, 16, 8, S) == 3
+    assert lib.mmf_bitlinear_fwd_noalloc(A, 0, B, C, D, BAD, 4, 16, 8, S) == 3
+    assert lib.mmf_bitlinear_fwd_noalloc(None, 0, None, None, None, None, 0, 16, 8, S) == 0
+    # 65536 tokens of 1040 features: 68 MB of q, past the 64 MiB array
+    assert lib.mmf_bitlinear_fwd_noalloc(A, 0, B, C, D, E, 65536, 1040, 64, S) == 6
+    assert lib.mmf_bitlinear_fwd_noalloc(A, 0, B, C, D, E, 65, 16, 1 << 21, S) == 2
