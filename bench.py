@@ -695,9 +695,10 @@ def bench_train(torch, mmf, name, args):
         "value": w.ops / (ms_step * 1e-3) / 1e12, "unit": "TOPS", "ms_per_step": ms_step,
         "config": {"workload": name, "M": M, "K": K, "N": N, "x_dtype": "bf16", "dO_dtype": "bf16",
                    "fwd_us": ms_fwd * 1e3, "bwd_us": ms_bwd * 1e3},
-        "roofline": {"bound": "mfma", "kernel": "backward: the dY and dW bf16 GEMMs (rocBLAS, fp32 "
-                                                "accumulation) with their operand preparation, "
-                                                "RMSNorm backward and column sums, timed as one call",
+        "roofline": {"bound": "mfma", "kernel": "backward: the dY and dW bf16 MFMA kernels (fp32 "
+                                                "accumulation; codes and q expanded in the kernels) "
+                                                "with the code re-pack, the RMSNorm-backward finish "
+                                                "and the column sums, timed as one call",
                      "achieved": bwd_tflops, "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                      "frac": bwd_tflops / BF16_PEAK_TFLOPS, "traffic": None,
                      "flops_per_launch": 2 * mnk2, "avg_launch_us": ms_bwd * 1e3},

@@ -379,10 +379,16 @@ int mmf_bitlinear_train_fwd(const void *x, int x_is_f32, const float *gamma, con
  * [K] or NULL (ones); rstd, q, a_scale, Wpacked, w_scale from
  * mmf_bitlinear_train_fwd.  Outputs float32: dx [M][K], dW [N][K], db [N]
  * (NULL: not computed), dgamma [K] (NULL: not computed).  The two products
- * are bf16 GEMMs with fp32 accumulation on the matrix cores (rocBLAS); s, db
- * and dgamma are summed in fp64; when the dW product is long and narrow
- * (few output tiles) its contraction over tokens is split into up to 8
- * parts, added in fp64.  M == 0 or N == 0 is a no-op.  Workspace as above.
+ * run on the matrix cores with bf16 operands and fp32 accumulation: dY reads
+ * the packed codes (re-packed once per call with the contraction index
+ * inside the word) and expands them in registers, with gamma, rstd and the
+ * row sums of the RMSNorm backward in its epilogue; dW reads q and a_scale
+ * and forms Yq while staging them.  s, db and dgamma are summed in fp64;
+ * when the dW output has few tiles its contraction over tokens is split into
+ * parts added in fp64.  Shapes whose dO rows, re-packed codes or dW exceed
+ * 32-bit offsets ((N + 7) / 8 * 16 * 128 bytes of dO per 128 rows, K * 4 *
+ * ceil(N / 16) bytes of codes, N * K * 4 bytes of dW, each below 2^31)
+ * return MMF_ERR_SHAPE.  M == 0 or N == 0 is a no-op.  Workspace as above.
  */
 size_t mmf_bitlinear_bwd_workspace_bytes(int64_t M, int64_t K, int64_t N);
 int mmf_bitlinear_bwd(const uint16_t *dO, const void *x, int x_is_f32, const float *gamma,

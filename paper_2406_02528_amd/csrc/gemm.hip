@@ -42,41 +42,12 @@
 // own L2, so the linear workgroup id is remapped to give every XCD a
 // contiguous run of tiles, walked in groups of kGroupM tile rows; the tiles
 // an XCD works on at once then share A rows and B columns in its L2.
+#include "gemm_common.h"
 #include "mmf_device.h"
 #include "mmf_launch.h"
 
 namespace mmf {
 namespace {
-
-typedef int v4i __attribute__((ext_vector_type(4)));
-
-constexpr int kBufferFlags = 0x00020000;  // gfx9 buffer descriptor word 3
-constexpr int kXcds = 8;
-constexpr int kGroupM = 4;
-
-__device__ __forceinline__ void tile_coords(int64_t tiles_m, int64_t tiles_n, int64_t& tm,
-                                            int64_t& tn) {
-  const int64_t total = tiles_m * tiles_n;
-  const int64_t b = blockIdx.x;
-  // XCD-contiguous logical index: XCD x (= b % 8) takes tiles
-  // [x * per, (x + 1) * per); the tail beyond 8 * per keeps its order.
-  const int64_t per = total / kXcds;
-  int64_t L = b;
-  if (b < per * kXcds) L = (b % kXcds) * per + b / kXcds;
-  // grouped row-major walk: kGroupM tile rows at a time, columns inside
-  const int64_t group = L / (kGroupM * tiles_n);
-  const int64_t first_m = group * kGroupM;
-  const int64_t gm = (tiles_m - first_m) < kGroupM ? (tiles_m - first_m) : kGroupM;
-  const int64_t in_group = L - group * kGroupM * tiles_n;
-  tm = first_m + in_group % gm;
-  tn = in_group / gm;
-}
-
-// s_waitcnt immediates (gfx9 encoding): at most n vector memory operations
-// outstanding; with LGKM0 also every LDS operation completed, without it no
-// wait on LDS (lgkmcnt field at its maximum).
-#define MMF_WAIT_VM(n) (((n) & 0xF) | (0x7 << 4) | (0xF << 8) | ((((n) >> 4) & 3) << 14))
-#define MMF_WAIT_VM_LGKM0(n) (((n) & 0xF) | (0x7 << 4) | ((((n) >> 4) & 3) << 14))
 
 // BX4: B rows are copied 16 bytes per lane (one word row per instruction),
 // which needs N % 4 == 0 for aligned rows; otherwise 4 bytes per lane.
@@ -107,12 +78,6 @@ struct Tiling {
   static_assert(BK == 128, "A swizzle is for 8 chunks per row");
 };
 
-// Chunk swizzle of A rows (8 chunks of 16 bytes per row): row r stores logical
-// chunk c in slot c ^ swz(r).  Sixteen consecutive rows at one chunk then hit
-// distinct bank groups both when 8 lanes share 32 banks and when 16 lanes
-// share 64 banks; swz(r + 16) = swz(r).
-__device__ __forceinline__ int a_swz(int r) { return ((r >> 1) ^ (r << 2)) & 7; }
-
 template <int BM, int BN, int WM, int WN, int BK, int S, bool BX4, Epilogue EP>
 __global__ __launch_bounds__((Tiling<BM, BN, WM, WN, BK, S, BX4>::kThreads)) void gemm_kernel(
     const int8_t* __restrict__ q, const float* __restrict__ a_scale,
@@ -130,7 +95,7 @@ __global__ __launch_bounds__((Tiling<BM, BN, WM, WN, BK, S, BX4>::kThreads)) voi
   const int l16 = lane & 15;
   const int g = lane >> 4;  // k group of this lane inside one MFMA
   int64_t tm, tn;
-  tile_coords((M + BM - 1) / BM, (N + BN - 1) / BN, tm, tn);
+  tile_coords(blockIdx.x, (M + BM - 1) / BM, (N + BN - 1) / BN, tm, tn);
   const int m0 = static_cast<int>(tm) * BM;
   const int n0 = static_cast<int>(tn) * BN;
   const int J = K / 16;
@@ -326,7 +291,7 @@ __global__ __launch_bounds__((Tiling<BM, BN, WM, WN, BK, S, BX4>::kThreads)) voi
   const float ws = (EP == Epilogue::kDequantF32 || EP == Epilogue::kGluF32) ? w_scale[0] : 0.0f;
   const float ws_u = (EP == Epilogue::kGluF32) ? w_scale[1] : 0.0f;
   __syncthreads();
-  constexpr uint32_t kOut = 0x80000000u;
+  constexpr uint32_t kOut = kOutOfRange;
   if constexpr (EP == Epilogue::kGluF32) {
     // Blocks f = 2i (gate) and 2i + 1 (up) of a wave hold the same 16
     // channels: lane (g, l16) has channels 4 g .. 4 g + 3 of both, so the

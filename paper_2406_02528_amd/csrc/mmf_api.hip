@@ -362,20 +362,35 @@ TrainScratch train_scratch(int64_t M, int64_t K, int64_t N) {
 }
 
 struct BwdScratch {
-  size_t t_off, yq_off, dy_off, part_off, dw_off, total;
+  int64_t Np, S;
+  size_t wn_off, dop_off, spart_off, dgpart_off, colpart_off, dw_off, total;
 };
 BwdScratch bwd_scratch(int64_t M, int64_t K, int64_t N) {
   BwdScratch s;
-  s.t_off = 0;
-  s.yq_off = round_up(static_cast<size_t>(K) * static_cast<size_t>(N) * 2, kScratchAlign);
-  s.dy_off = s.yq_off + round_up(static_cast<size_t>(M) * static_cast<size_t>(K) * 2, kScratchAlign);
-  s.part_off = s.dy_off + round_up(static_cast<size_t>(M) * static_cast<size_t>(K) * 4, kScratchAlign);
-  const int64_t cols = N > K ? N : K;
-  s.dw_off = s.part_off + round_up(sizeof(double) * static_cast<size_t>(mmf::col_sum_partials(M) * cols),
-                                   kScratchAlign);
-  const int64_t S = mmf::dw_split(M, N, K);
-  s.total = s.dw_off + (S > 1 ? round_up(sizeof(float) * static_cast<size_t>(S * N * K), kScratchAlign) : 0);
+  s.Np = (N + 7) / 8 * 8;
+  s.S = mmf::bwd_dw_split(M, N, K, s.Np);
+  s.wn_off = 0;
+  s.dop_off = round_up(static_cast<size_t>(mmf::bwd_nmajor_words(N, K)) * 4, kScratchAlign);
+  const size_t dop = s.Np != N ? static_cast<size_t>(M) * static_cast<size_t>(s.Np) * 2 : 0;
+  s.spart_off = s.dop_off + round_up(dop, kScratchAlign);
+  s.dgpart_off = s.spart_off + round_up(sizeof(double) * static_cast<size_t>(mmf::bwd_dy_col_tiles(K) * M),
+                                        kScratchAlign);
+  s.colpart_off = s.dgpart_off + round_up(sizeof(double) * static_cast<size_t>(mmf::bwd_dy_row_tiles(M) * K),
+                                          kScratchAlign);
+  s.dw_off = s.colpart_off + round_up(sizeof(double) * static_cast<size_t>(mmf::col_sum_partials(M) * N),
+                                      kScratchAlign);
+  s.total = s.dw_off + (s.S > 1 ? round_up(sizeof(float) * static_cast<size_t>(s.S * N * K), kScratchAlign) : 0);
   return s;
+}
+
+// Shapes the backward's kernels address with 32-bit offsets: the n-major
+// codes and the dY launch's dO rows (bwd_dy_row_slice), dW [N][K] and the
+// token counts.
+int check_bwd_shape(int64_t M, int64_t K, int64_t N) {
+  const int64_t lim = (int64_t(1) << 31) - 1;
+  const int64_t Np = (N + 7) / 8 * 8;
+  if (mmf::bwd_dy_row_slice(Np, K) == 0 || N * K * 4 > lim || M > lim) return MMF_ERR_SHAPE;
+  return MMF_OK;
 }
 
 // ---- the forward without allocation (mmf_bitlinear_fwd_noalloc) ----
@@ -789,7 +804,7 @@ int mmf_bitlinear_train_fwd(const void* x, int x_is_f32, const float* gamma, con
 }
 
 size_t mmf_bitlinear_bwd_workspace_bytes(int64_t M, int64_t K, int64_t N) {
-  if (check_shape(M, K, N) != MMF_OK) return 0;
+  if (check_shape(M, K, N) != MMF_OK || check_bwd_shape(M, K, N) != MMF_OK) return 0;
   return bwd_scratch(M, K, N).total;
 }
 
@@ -799,6 +814,7 @@ int mmf_bitlinear_bwd(const uint16_t* dO, const void* x, int x_is_f32, const flo
                       int64_t K, int64_t N, void* workspace, size_t workspace_bytes, hipStream_t stream) {
   if (int st = check_dtype(x_is_f32)) return st;
   if (int st = check_shape(M, K, N)) return st;
+  if (int st = check_bwd_shape(M, K, N)) return st;
   if (M == 0 || N == 0) return MMF_OK;
   if (!dO || !x || !rstd || !q || !a_scale || !Wpacked || !w_scale || !dx || !dW) return MMF_ERR_NULL;
   if (!aligned16(dO) || !aligned16(x) || !aligned16(rstd) || !aligned16(q) || !aligned16(a_scale) ||
@@ -807,24 +823,32 @@ int mmf_bitlinear_bwd(const uint16_t* dO, const void* x, int x_is_f32, const flo
     return MMF_ERR_ALIGN;
   const BwdScratch s = bwd_scratch(M, K, N);
   return with_workspace(workspace, workspace_bytes, s.total, stream, [&](char* scratch) {
-    uint16_t* T = reinterpret_cast<uint16_t*>(scratch + s.t_off);
-    uint16_t* yq = reinterpret_cast<uint16_t*>(scratch + s.yq_off);
-    float* dYs = reinterpret_cast<float*>(scratch + s.dy_off);
-    double* parts = reinterpret_cast<double*>(scratch + s.part_off);
+    uint32_t* Wn = reinterpret_cast<uint32_t*>(scratch + s.wn_off);
+    double* s_part = reinterpret_cast<double*>(scratch + s.spart_off);
+    double* dg_part = dgamma ? reinterpret_cast<double*>(scratch + s.dgpart_off) : nullptr;
     const int Ki = static_cast<int>(K);
-    // dY (before the weight scale) = dO T^T with T the forward's codes as bf16
-    if (mmf::launch_expand_ternary(Wpacked, Ki, N, T, stream) != hipSuccess) return MMF_ERR_HIP;
-    if (mmf::gemm_bf16(false, true, M, K, N, dO, N, T, N, dYs, K, stream) != hipSuccess) return MMF_ERR_HIP;
-    if (mmf::launch_rms_norm_bwd(dYs, w_scale, x, x_is_f32 == 1, gamma, rstd, M, Ki, dx, stream) != hipSuccess)
-      return MMF_ERR_HIP;
-    // dW = dO^T Yq
-    if (mmf::launch_dequant_bf16(q, a_scale, M, Ki, yq, stream) != hipSuccess) return MMF_ERR_HIP;
-    if (mmf::gemm_bf16_dw(M, N, K, dO, yq, dW, reinterpret_cast<float*>(scratch + s.dw_off), stream) !=
+    const bool f32 = x_is_f32 == 1;
+    // dO rows in 16-byte chunks: zero-padded copy when N % 8 != 0
+    const uint16_t* dOp = dO;
+    if (s.Np != N) {
+      uint16_t* pad = reinterpret_cast<uint16_t*>(scratch + s.dop_off);
+      if (mmf::launch_pad_rows(dO, M, N, s.Np, pad, stream) != hipSuccess) return MMF_ERR_HIP;
+      dOp = pad;
+    }
+    // dY = dO Wt^T with r gamma dY into dx and the row / column partials,
+    // then dx and dgamma finished
+    if (mmf::launch_pack_nmajor(Wpacked, N, s.Np, Ki, Wn, stream) != hipSuccess) return MMF_ERR_HIP;
+    if (mmf::launch_dy(dOp, M, s.Np, Wn, w_scale, x, f32, gamma, rstd, Ki, dx, s_part, dg_part, stream) !=
         hipSuccess)
       return MMF_ERR_HIP;
-    if (db && mmf::launch_col_sum_bf16(dO, M, N, parts, db, stream) != hipSuccess) return MMF_ERR_HIP;
-    if (dgamma && mmf::launch_dgamma(dYs, w_scale, x, x_is_f32 == 1, rstd, M, Ki, parts, dgamma, stream) !=
-                      hipSuccess)
+    if (mmf::launch_dx_finish(dx, x, f32, rstd, s_part, M, Ki, stream) != hipSuccess) return MMF_ERR_HIP;
+    if (dgamma && mmf::launch_dgamma_finish(dg_part, M, Ki, dgamma, stream) != hipSuccess) return MMF_ERR_HIP;
+    // dW = dO^T Yq (token range split into parts when the output has few tiles)
+    float* dw_out = s.S > 1 ? reinterpret_cast<float*>(scratch + s.dw_off) : dW;
+    if (mmf::launch_dw(dOp, q, a_scale, M, s.Np, N, Ki, dw_out, s.S, stream) != hipSuccess) return MMF_ERR_HIP;
+    if (s.S > 1 && mmf::launch_sum_parts(dw_out, s.S, N * K, dW, stream) != hipSuccess) return MMF_ERR_HIP;
+    if (db && mmf::launch_col_sum_bf16(dO, M, N, reinterpret_cast<double*>(scratch + s.colpart_off), db,
+                                       stream) != hipSuccess)
       return MMF_ERR_HIP;
     return MMF_OK;
   });

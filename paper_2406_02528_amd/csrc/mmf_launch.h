@@ -121,40 +121,44 @@ int64_t mlgru_scan_ws_floats(int64_t B, int64_t T, int64_t d);
 hipError_t launch_mlgru_scan(const float* fcg, const float* h0, float* o, float* h_last, int64_t B,
                              int64_t T, int64_t d, float* ws, hipStream_t stream);
 
-// ---- backward (bwd.hip) ----
-// T [K][N] bf16 = the ternary codes of Wpacked [K/16][N] as -1, 0, +1.
-hipError_t launch_expand_ternary(const uint32_t* Wpacked, int K, int64_t N, uint16_t* T,
-                                 hipStream_t stream);
-// yq [M][K] bf16 = q * a_scale[m] (fp32 product, rounded to nearest even).
-hipError_t launch_dequant_bf16(const int8_t* q, const float* a_scale, int64_t M, int K, uint16_t* yq,
-                               hipStream_t stream);
-// RMSNorm backward per row: dY = w_scale * dYs, g = gamma dY,
-// s = sum g x (fp64), dx = r g - (r^3 s / K) x.
-hipError_t launch_rms_norm_bwd(const float* dYs, const float* w_scale, const void* x, bool x_is_f32,
-                               const float* gamma, const float* rstd, int64_t M, int K, float* dx,
-                               hipStream_t stream);
+// ---- backward (bwd.hip: column sums; bwd_gemm.hip: the two products) ----
 // Column sums over M rows, in fp64, in a fixed order: db[n] = sum_m dO[m][n]
-// (dO bf16 [M][N]) and dgamma[k] = sum_m (w_scale dYs[m][k]) x[m][k] r[m].
-// `partials` holds col_sum_partials(M) * cols doubles.
+// (dO bf16 [M][N]).  `partials` holds col_sum_partials(M) * N doubles.
 int64_t col_sum_partials(int64_t M);
 hipError_t launch_col_sum_bf16(const uint16_t* dO, int64_t M, int64_t N, double* partials, float* db,
                                hipStream_t stream);
-hipError_t launch_dgamma(const float* dYs, const float* w_scale, const void* x, bool x_is_f32,
-                         const float* rstd, int64_t M, int K, double* partials, float* dgamma,
-                         hipStream_t stream);
-// Dense bf16 x bf16 -> fp32 products on the matrix cores through rocBLAS,
-// row-major operands:  C[Mr][Nc] = A[Mr][Kc] * B[Kc][Nc] (transB: B given as
-// [Nc][Kc]); (transA: A given as [Kc][Mr]); `batch` products at the given
-// element strides.
-hipError_t gemm_bf16(bool transA, bool transB, int64_t Mr, int64_t Nc, int64_t Kc, const uint16_t* A,
-                     int64_t lda, const uint16_t* B, int64_t ldb, float* C, int64_t ldc, hipStream_t stream,
-                     int64_t batch = 1, int64_t strideA = 0, int64_t strideB = 0, int64_t strideC = 0);
-// dW [N][K] = dO^T yq (dO bf16 [M][N], yq bf16 [M][K]); long narrow products
-// are split over tokens into dw_split(M, N, K) parts summed in fp64 (`parts`
-// holds dw_split * N * K floats when the split is > 1).
-int64_t dw_split(int64_t M, int64_t N, int64_t K);
-hipError_t gemm_bf16_dw(int64_t M, int64_t N, int64_t K, const uint16_t* dO, const uint16_t* yq, float* dW,
-                        float* parts, hipStream_t stream);
+// out[c] = sum over p < nparts of partials[p * cols + c] (fp64, fixed order).
+hipError_t launch_col_final(const double* partials, int64_t nparts, int64_t cols, float* out, hipStream_t stream);
+// out[i] = sum over s < S of parts[s * n + i], in order, in fp64.
+hipError_t launch_sum_parts(const float* parts, int64_t S, int64_t n, float* out, hipStream_t stream);
+
+// Codes re-packed n-major: Wn [ceil(Np/16)][K] (bwd_nmajor_words(N, K)
+// words with Np = N rounded up to 8), codes of n >= N set to t = 0.
+int64_t bwd_nmajor_words(int64_t N, int64_t K);
+hipError_t launch_pack_nmajor(const uint32_t* Wpacked, int64_t N, int64_t Np, int K, uint32_t* Wn,
+                              hipStream_t stream);
+// dst [M][N8] = src [M][N] with zero columns N .. N8 - 1.
+hipError_t launch_pad_rows(const uint16_t* src, int64_t M, int64_t N, int64_t N8, uint16_t* dst,
+                           hipStream_t stream);
+// dY kernel: dO [M][Np] bf16 (Np % 8 == 0) against Wn; writes rg = r gamma dY
+// into rg [M][K], s_part [bwd_dy_col_tiles(K)][M] and (if not null) dg_part
+// [bwd_dy_row_tiles(M)][K].  bwd_dy_row_slice(Np, K) == 0: shape not
+// supported (32-bit offsets).
+int64_t bwd_dy_col_tiles(int64_t K);
+int64_t bwd_dy_row_tiles(int64_t M);
+int64_t bwd_dy_row_slice(int64_t Np, int64_t K);
+hipError_t launch_dy(const uint16_t* dO, int64_t M, int64_t Np, const uint32_t* Wn, const float* w_scale,
+                     const void* x, bool x_is_f32, const float* gamma, const float* rstd, int K, float* rg,
+                     double* s_part, double* dg_part, hipStream_t stream);
+// dx = rg - (r^3 s / K) x in place; dgamma from the row-tile partials.
+hipError_t launch_dx_finish(float* dx, const void* x, bool x_is_f32, const float* rstd, const double* s_part,
+                            int64_t M, int K, hipStream_t stream);
+hipError_t launch_dgamma_finish(const double* dg_part, int64_t M, int K, float* dgamma, hipStream_t stream);
+// dW kernel: out [S][N][K] (S = bwd_dw_split(M, N, K, Np) parts of the token
+// range; S == 1 writes dW itself).  N * K * 4 must stay below 2^31.
+int64_t bwd_dw_split(int64_t M, int64_t N, int64_t K, int64_t Np);
+hipError_t launch_dw(const uint16_t* dO, const int8_t* q, const float* a_scale, int64_t M, int64_t Np, int64_t N,
+                     int K, float* out, int64_t S, hipStream_t stream);
 
 hipError_t launch_glu_pack(const uint32_t* Wg, const uint32_t* Wu, int64_t L, int K, uint32_t* Wgu,
                            hipStream_t stream);
