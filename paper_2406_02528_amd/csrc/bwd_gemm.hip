@@ -71,22 +71,29 @@ constexpr int kBlock = 256;
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ int nmajor_bit(int e) { return 8 * (1 - (e >> 3)) + 2 * ((e >> 1) & 3) + 16 * (e & 1); }
 
+// Workgroup (x: jn, y: 256 columns k0 .. k0 + 255): the 16 x 16 input words of
+// rows k0 / 16 .. + 15 and columns n = 16 jn .. + 15 go through LDS, then
+// thread k assembles output word (jn, k0 + k) from the 16 words of its row.
 __global__ __launch_bounds__(kBlock) void pack_nmajor_kernel(const uint32_t* __restrict__ Wp, int64_t N, int K,
                                                              int64_t JN, uint32_t* __restrict__ Wn) {
-  const int64_t idx = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
-  if (idx >= JN * K) return;
-  const int64_t jn = idx / K;
-  const int k = static_cast<int>(idx % K);
-  const uint32_t* src = Wp + static_cast<int64_t>(k >> 4) * N;
+  __shared__ uint32_t tile[16][17];
+  const int t = threadIdx.x;
+  const int64_t jn = blockIdx.x;
+  const int k0 = blockIdx.y * kBlock;
+  {
+    const int j = t >> 4, e = t & 15;  // input word (k0 / 16 + j, 16 jn + e)
+    const int64_t n = 16 * jn + e;
+    const int jr = k0 / 16 + j;
+    tile[j][e] = (n < N && jr < K / 16) ? Wp[static_cast<int64_t>(jr) * N + n] : 0x55555555u;  // code 1 = zero
+  }
+  __syncthreads();
+  const int k = k0 + t;
+  if (k >= K) return;
   const int sh = 8 * (k & 3) + 2 * ((k >> 2) & 3);
   uint32_t w = 0;
 #pragma unroll
-  for (int e = 0; e < 16; ++e) {
-    const int64_t n = 16 * jn + e;
-    const uint32_t c = n < N ? (src[n] >> sh) & 3u : 1u;
-    w |= c << nmajor_bit(e);
-  }
-  Wn[idx] = w;
+  for (int e = 0; e < 16; ++e) w |= ((tile[t >> 4][e] >> sh) & 3u) << nmajor_bit(e);
+  Wn[jn * K + k] = w;
 }
 
 // dO rows padded with zeros to a multiple of 8 columns (16-byte chunks).
@@ -425,7 +432,7 @@ __device__ __forceinline__ void yq8(int2 qv, float a, uint32_t* out) {
 __global__ __launch_bounds__(dwk::kThreads) void dw_kernel(const uint16_t* __restrict__ dO,
                                                            const int8_t* __restrict__ q,
                                                            const float* __restrict__ a_scale, int T, int Np,
-                                                           int N, int K, int tiles, float* __restrict__ out_base) {
+                                                           int N, int K, DwPlan plan, float* __restrict__ out_base) {
   using namespace dwk;
   __shared__ __attribute__((aligned(16))) char smem[S * kStageBytes];
   const int tid = threadIdx.x;
@@ -434,16 +441,20 @@ __global__ __launch_bounds__(dwk::kThreads) void dw_kernel(const uint16_t* __res
   const int wn = wave / kWavesK, wk = wave % kWavesK;
   const int l16 = lane & 15;
   const int g = lane >> 4;
-  const int split = blockIdx.x / tiles;
+  // work unit -> tile and token range (see DwPlan)
+  const int u = blockIdx.x;
+  const int tile = static_cast<int>(u % plan.tiles);
+  const int split = static_cast<int>(u / plan.tiles);
+  const int nsplit = static_cast<int>(plan.split_all);
   int64_t tnn, tkk;
-  tile_coords(blockIdx.x % tiles, (N + BN - 1) / BN, (K + BK - 1) / BK, tnn, tkk);
+  tile_coords(tile, (N + BN - 1) / BN, (K + BK - 1) / BK, tnn, tkk);
   const int n0 = static_cast<int>(tnn) * BN;
   const int k0 = static_cast<int>(tkk) * BK;
   // this split's tokens
-  const int per = (T + gridDim.x / tiles - 1) / (gridDim.x / tiles);
+  const int per = (T + nsplit - 1) / nsplit;
   const int per64 = (per + BT - 1) / BT * BT;
-  const int t0 = split * per64;
-  const int t1 = t0 + per64 < T ? t0 + per64 : (T > t0 ? T : t0);
+  const int t0 = split * per64 < T ? split * per64 : T;
+  const int t1 = t0 + per64 < T ? t0 + per64 : T;
   float* out = out_base + static_cast<int64_t>(split) * N * K;
   const int KT = t1 > t0 ? (t1 - t0 + BT - 1) / BT : 0;
   const uint32_t rowb = 2u * static_cast<uint32_t>(Np);
@@ -513,17 +524,19 @@ __global__ __launch_bounds__(dwk::kThreads) void dw_kernel(const uint16_t* __res
                  : "n"(kDmaPerWave)
                  : "memory");
   };
-  auto write_yq = [&](int kt) {
+  // the Yq of chunk i of this thread's token row (quarter i of its q)
+  auto write_yq_chunk = [&](int kt, int i) {
     char* dst = smem + (kt % S) * kStageBytes + kTile + q_row * kRow;
-    const int2 qs[4] = {qv0, qv1, qv2, qv3};
+    const int2 qi = i == 0 ? qv0 : i == 1 ? qv1 : i == 2 ? qv2 : qv3;
+    uint32_t b[4];
+    yq8(qi, qa, b);
+    const int slot = (q_part + 8 * i) ^ q_sw;
+    *reinterpret_cast<v4i*>(dst + slot * 16) =
+        v4i{static_cast<int>(b[0]), static_cast<int>(b[1]), static_cast<int>(b[2]), static_cast<int>(b[3])};
+  };
+  auto write_yq = [&](int kt) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      uint32_t b[4];
-      yq8(qs[i], qa, b);
-      const int slot = (q_part + 8 * i) ^ q_sw;
-      *reinterpret_cast<v4i*>(dst + slot * 16) =
-          v4i{static_cast<int>(b[0]), static_cast<int>(b[1]), static_cast<int>(b[2]), static_cast<int>(b[3])};
-    }
+    for (int i = 0; i < 4; ++i) write_yq_chunk(kt, i);
   };
 
   // transpose-read offsets: lane (g, l16) names token row 8g + 4h + (l16 >> 2)
@@ -567,21 +580,18 @@ __global__ __launch_bounds__(dwk::kThreads) void dw_kernel(const uint16_t* __res
   // covers stage 0's copies and q loads issued before them.
   if (KT > 0) {
     v4i af[FM], b0[FN], b1[FN];
+    // one 32-token step: its MFMAs, with the next step's fragments read and
+    // (convert) a quarter of a stage's Yq formed behind every other group
     auto mma = [&](const v4i (&bc)[FN], v4i (&bn)[FN], int next_step, bool read_next, bool convert, int conv_kt) {
-      if (read_next) {
-#pragma unroll
-        for (int f = 0; f < FN; ++f) bn[f] = frag(next_step, offB[f]);
-      }
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int fm = 0; fm < FM; ++fm) {
 #pragma unroll
         for (int f = 0; f < FN; ++f) acc[fm][f] = mfma_bf16(bc[f], af[fm], acc[fm][f]);
         if (read_next) af[fm] = frag(next_step, offA[fm]);
-        if (fm == 1 && convert) {
-          wait_q();
-          write_yq(conv_kt);
-        }
+        if (read_next && fm < FN) bn[fm] = frag(next_step, offB[fm]);
+        if (convert && fm == 1) wait_q();
+        if (convert && (fm & 1)) write_yq_chunk(conv_kt, fm >> 1);
         __builtin_amdgcn_sched_barrier(0);
       }
     };
@@ -644,10 +654,9 @@ int64_t bwd_nmajor_words(int64_t N, int64_t K) { return ((N + 7) / 8 * 8 + 15) /
 hipError_t launch_pack_nmajor(const uint32_t* Wpacked, int64_t N, int64_t Np, int K, uint32_t* Wn,
                               hipStream_t stream) {
   const int64_t JN = (Np + 15) / 16;
-  const int64_t total = JN * K;
-  if (total == 0) return hipSuccess;
-  hipLaunchKernelGGL(pack_nmajor_kernel, dim3(static_cast<unsigned>((total + kBlock - 1) / kBlock)), dim3(kBlock), 0,
-                     stream, Wpacked, N, K, JN, Wn);
+  if (JN * K == 0) return hipSuccess;
+  hipLaunchKernelGGL(pack_nmajor_kernel, dim3(static_cast<unsigned>(JN), static_cast<unsigned>((K + kBlock - 1) / kBlock)),
+                     dim3(kBlock), 0, stream, Wpacked, N, K, JN, Wn);
   return hipGetLastError();
 }
 
@@ -712,28 +721,33 @@ hipError_t launch_dgamma_finish(const double* dg_part, int64_t M, int K, float* 
   return launch_col_final(dg_part, bwd_dy_row_tiles(M), K, dgamma, stream);
 }
 
-int64_t bwd_dw_split(int64_t M, int64_t N, int64_t K, int64_t Np) {
-  // split the token range while the output has too few tiles to fill the
-  // chip; every part keeps at least 512 tokens and, for 32-bit offsets,
-  // fewer than 2^31 bytes of dO rows and of q rows
-  const int64_t tiles = ((N + dwk::BN - 1) / dwk::BN) * ((K + dwk::BK - 1) / dwk::BK);
-  int64_t S = 1;
-  while (tiles * S < 200 && M / (2 * S) >= 512) S *= 2;
-  // (a part's rows, rounded up to whole stages, plus one stage of rows past
-  // its end, which read as zero)
+DwPlan bwd_dw_plan(int64_t M, int64_t N, int64_t K, int64_t Np, int cus) {
+  // Split the token range while the output has too few tiles to fill the
+  // chip (parts keep at least 512 tokens), and for 32-bit offsets: a part's
+  // rows, rounded up to whole stages, plus one stage of rows past its end
+  // (which read as zero) stay below 2^31 bytes of dO and of q.  (Splitting
+  // only a last, partial round of tiles measured slower than running it
+  // whole.)
+  DwPlan p;
+  p.tiles = ((N + dwk::BN - 1) / dwk::BN) * ((K + dwk::BK - 1) / dwk::BK);
   const int64_t lim = (int64_t(1) << 31) - 1;
-  auto rows = [&](int64_t s) { return (M + s - 1) / s + 2 * dwk::BT; };
-  while (rows(S) * 2 * Np > lim || rows(S) * K > lim) S *= 2;
-  return S;
+  auto fits = [&](int64_t s) {
+    const int64_t rows = (M + s - 1) / s + 2 * dwk::BT;
+    return rows * 2 * Np <= lim && rows * K <= lim;
+  };
+  int64_t S = 1;
+  while (p.tiles * S < (cus * 3) / 4 && M / (2 * S) >= 512) S *= 2;
+  while (!fits(S)) S *= 2;
+  p.split_all = S;
+  return p;
 }
 
 hipError_t launch_dw(const uint16_t* dO, const int8_t* q, const float* a_scale, int64_t M, int64_t Np, int64_t N,
-                     int K, float* out, int64_t S, hipStream_t stream) {
-  const int64_t tiles = ((N + dwk::BN - 1) / dwk::BN) * ((K + dwk::BK - 1) / dwk::BK);
+                     int K, float* out, const DwPlan& plan, hipStream_t stream) {
   if (N * K * 4 > (int64_t(1) << 31) - 1) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(dw_kernel, dim3(static_cast<unsigned>(tiles * S)), dim3(dwk::kThreads), 0, stream, dO, q,
-                     a_scale, static_cast<int>(M), static_cast<int>(Np), static_cast<int>(N), K,
-                     static_cast<int>(tiles), out);
+  hipLaunchKernelGGL(dw_kernel, dim3(static_cast<unsigned>(plan.tiles * plan.split_all)), dim3(dwk::kThreads), 0,
+                     stream, dO, q, a_scale, static_cast<int>(M), static_cast<int>(Np), static_cast<int>(N), K, plan,
+                     out);
   return hipGetLastError();
 }
 

@@ -361,14 +361,29 @@ TrainScratch train_scratch(int64_t M, int64_t K, int64_t N) {
   return s;
 }
 
+// Compute units of the current device (the dW kernel's work plan).
+int device_cus() {
+  static std::mutex mu;
+  static int cus[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  std::lock_guard<std::mutex> lock(mu);
+  if (cus[dev] == 0) {
+    int v = 0;
+    cus[dev] = (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && v > 0) ? v : 256;
+  }
+  return cus[dev];
+}
+
 struct BwdScratch {
-  int64_t Np, S;
+  int64_t Np;
+  mmf::DwPlan plan;
   size_t wn_off, dop_off, spart_off, dgpart_off, colpart_off, dw_off, total;
 };
 BwdScratch bwd_scratch(int64_t M, int64_t K, int64_t N) {
   BwdScratch s;
   s.Np = (N + 7) / 8 * 8;
-  s.S = mmf::bwd_dw_split(M, N, K, s.Np);
+  s.plan = mmf::bwd_dw_plan(M, N, K, s.Np, device_cus());
   s.wn_off = 0;
   s.dop_off = round_up(static_cast<size_t>(mmf::bwd_nmajor_words(N, K)) * 4, kScratchAlign);
   const size_t dop = s.Np != N ? static_cast<size_t>(M) * static_cast<size_t>(s.Np) * 2 : 0;
@@ -379,7 +394,8 @@ BwdScratch bwd_scratch(int64_t M, int64_t K, int64_t N) {
                                           kScratchAlign);
   s.dw_off = s.colpart_off + round_up(sizeof(double) * static_cast<size_t>(mmf::col_sum_partials(M) * N),
                                       kScratchAlign);
-  s.total = s.dw_off + (s.S > 1 ? round_up(sizeof(float) * static_cast<size_t>(s.S * N * K), kScratchAlign) : 0);
+  const int64_t S = s.plan.split_all;
+  s.total = s.dw_off + (S > 1 ? round_up(sizeof(float) * static_cast<size_t>(S * N * K), kScratchAlign) : 0);
   return s;
 }
 
@@ -844,9 +860,10 @@ int mmf_bitlinear_bwd(const uint16_t* dO, const void* x, int x_is_f32, const flo
     if (mmf::launch_dx_finish(dx, x, f32, rstd, s_part, M, Ki, stream) != hipSuccess) return MMF_ERR_HIP;
     if (dgamma && mmf::launch_dgamma_finish(dg_part, M, Ki, dgamma, stream) != hipSuccess) return MMF_ERR_HIP;
     // dW = dO^T Yq (token range split into parts when the output has few tiles)
-    float* dw_out = s.S > 1 ? reinterpret_cast<float*>(scratch + s.dw_off) : dW;
-    if (mmf::launch_dw(dOp, q, a_scale, M, s.Np, N, Ki, dw_out, s.S, stream) != hipSuccess) return MMF_ERR_HIP;
-    if (s.S > 1 && mmf::launch_sum_parts(dw_out, s.S, N * K, dW, stream) != hipSuccess) return MMF_ERR_HIP;
+    const int64_t S = s.plan.split_all;
+    float* dw_out = S > 1 ? reinterpret_cast<float*>(scratch + s.dw_off) : dW;
+    if (mmf::launch_dw(dOp, q, a_scale, M, s.Np, N, Ki, dw_out, s.plan, stream) != hipSuccess) return MMF_ERR_HIP;
+    if (S > 1 && mmf::launch_sum_parts(dw_out, S, N * K, dW, stream) != hipSuccess) return MMF_ERR_HIP;
     if (db && mmf::launch_col_sum_bf16(dO, M, N, reinterpret_cast<double*>(scratch + s.colpart_off), db,
                                        stream) != hipSuccess)
       return MMF_ERR_HIP;

@@ -154,11 +154,16 @@ hipError_t launch_dy(const uint16_t* dO, int64_t M, int64_t Np, const uint32_t* 
 hipError_t launch_dx_finish(float* dx, const void* x, bool x_is_f32, const float* rstd, const double* s_part,
                             int64_t M, int K, hipStream_t stream);
 hipError_t launch_dgamma_finish(const double* dg_part, int64_t M, int K, float* dgamma, hipStream_t stream);
-// dW kernel: out [S][N][K] (S = bwd_dw_split(M, N, K, Np) parts of the token
-// range; S == 1 writes dW itself).  N * K * 4 must stay below 2^31.
-int64_t bwd_dw_split(int64_t M, int64_t N, int64_t K, int64_t Np);
+// Work units of the dW kernel: every tile's token range is split into
+// split_all parts (1: none), written to out [split_all][N][K] and added by
+// launch_sum_parts when there is more than one.  N * K * 4 must stay below
+// 2^31.
+struct DwPlan {
+  int64_t tiles = 0, split_all = 1;
+};
+DwPlan bwd_dw_plan(int64_t M, int64_t N, int64_t K, int64_t Np, int cus);
 hipError_t launch_dw(const uint16_t* dO, const int8_t* q, const float* a_scale, int64_t M, int64_t Np, int64_t N,
-                     int K, float* out, int64_t S, hipStream_t stream);
+                     int K, float* out, const DwPlan& plan, hipStream_t stream);
 
 hipError_t launch_glu_pack(const uint32_t* Wg, const uint32_t* Wu, int64_t L, int K, uint32_t* Wgu,
                            hipStream_t stream);

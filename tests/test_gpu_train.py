@@ -186,14 +186,18 @@ def test_bwd_optional_outputs_and_workspace(mmf):
     assert torch.equal(dx1, dx2) and torch.equal(dW1, dW2)
 
 
-def test_train_workload_full_size_sampled(mmf):
+@pytest.mark.parametrize("name", ["train_d1024", "train_glu_up"])
+def test_train_workload_full_size_sampled(mmf, name):
     """The paper's training-efficiency setting (input size and sequence length
-    1024; 16 sequences, M = 16384, K = N = 1024): training forward and
-    backward at full size; dx rows and dW rows sampled from two oracle calls
-    (rows of tokens, then columns of outputs), db whole."""
-    w = workloads.TRAIN_WORKLOADS["train_d1024"]
+    1024; 16 sequences, M = 16384, K = N = 1024; its dW has 16 output tiles, so
+    every tile's token range is split) and the 1.3B model's GLU up-projection
+    over 8192 tokens (352 dW tiles: the last, partial round over the compute
+    units is split in two and added by the part finishing last): training
+    forward and backward at full size; dx rows and dW rows sampled from two
+    oracle calls (rows of tokens, then columns of outputs), db sampled."""
+    w = workloads.TRAIN_WORKLOADS[name]
     inp = workloads.make_train(w)
-    log(f"[train_d1024] M={w.M} K={w.K} N={w.N}")
+    log(f"[{name}] M={w.M} K={w.K} N={w.N}")
     x_d, g_d = to_dev_x(inp["x_bits"]), T_(inp["gamma"])
     fw = train_fwd_gpu(mmf, x_d, g_d, inp["W"], None)
     t, ws = oracle.weight_quant(inp["W"])
