@@ -132,7 +132,7 @@ CSRC = os.path.join(ROOT, "paper_2406_02528_amd", "csrc")
 # is used only while their digest is unchanged
 KERNEL_SOURCES = {
     "decode_kernel": ("decode_impl.h", "decode_bf16.hip", "mmf_device.h"),
-    "gemm_kernel": ("gemm.hip", "mmf_device.h"),
+    "gemm_kernel": ("gemm.hip", "gemm_common.h", "mmf_device.h"),
 }
 CALIB_BYTES = 1 << 28          # bytes read and written by one calibration copy
 
