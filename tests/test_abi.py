@@ -331,6 +331,18 @@ def test_shapes_past_the_kernel_offsets_are_rejected_up_front(mmf):
     assert lib.mmf_mlgru_proj_q(A, B, C, D, E, A, B, C, 65, 16, d, S) == 2
 
 
+def test_backward_shapes_past_its_offsets_are_rejected_up_front(mmf):
+    """The backward's 32-bit offsets: dW [N][K] of 2^31 bytes or more, the
+    re-packed codes, and dO rows too long for a 128-row slice return
+    MMF_ERR_SHAPE (and a zero workspace size) before anything is enqueued."""
+    lib = _c(mmf)
+    for M, K, N in ((64, 2048, 1 << 18), (64, 1 << 16, 1 << 15), (64, 16, (1 << 23) + 8)):
+        assert lib.mmf_bitlinear_bwd_workspace_bytes(M, K, N) == 0
+        assert lib.mmf_bitlinear_bwd(A, B, 0, None, C, D, E, A, B, C, D, None, None, M, K, N, None, 0, S) == 2
+    # just inside: dW of 2^31 - 2^13 bytes
+    assert lib.mmf_bitlinear_bwd_workspace_bytes(64, 2048, (1 << 18) - 1) > 0
+
+
 def test_noalloc_argument_checks(mmf):
     """The forward without allocation: the same checks as the forward, and
     scratch needs past its static array rejected before anything is

@@ -420,12 +420,12 @@ def test_mlgru_workloads(mmf, name):
                    a_rel(r["a_o"][rows], out["a_scale"]))
 
 
-@pytest.mark.parametrize("B,d", [(1, 2048), (5, 96), (11, 64)])
+@pytest.mark.parametrize("B,d", [(1, 2048), (5, 96), (21, 64)])
 def test_mlgru_decode_step_fused_equals_in_place(mmf, B, d):
     """A decode step (T = 1) whose new state goes to its own array runs the
     recurrence and output gate in the output projection's prologue; with the
     state updated in place it runs the recurrence kernel and the plain
-    projection.  Same arithmetic: the same bits (B = 11 spans two 8-token
+    projection.  Same arithmetic: the same bits (B = 21 spans two 16-token
     slices)."""
     rs = np.random.default_rng(7700 + B + d)
     bits, xf, gamma, W = workloads.random_case(rs, B, d, 3 * d)
