@@ -51,7 +51,13 @@
 // & 1) | 2 ((row >> 3) & 1))) so the rows one transpose read spans fall on
 // distinct bank groups, and so do the Yq stores of two consecutive rows.
 // When the output has few tiles the token range is split, and the parts are
-// added in fp64 in a fixed order.
+// added in fp64 in a fixed order; otherwise the tiles past the last whole
+// round of workgroups have their stages spread evenly over one more round of
+// units (each covering the end of one tile and the start of the next at
+// most), whose pieces a second kernel adds in token order.  The pieces meet
+// only through the kernel boundary: a last-arriver sum inside the kernel
+// needs a device-scope release per piece, which writes back the L2 and
+// measured slower than running those tiles unsplit.
 #include "gemm_common.h"
 #include "mmf_device.h"
 #include "mmf_launch.h"
@@ -427,12 +433,26 @@ __device__ __forceinline__ void yq8(int2 qv, float a, uint32_t* out) {
   }
 }
 
-// Token range [t_begin, t_end) of dO [*][Np] and q [*][K] (pointers at row
-// t_begin); out [N][K] (the split's part).
+// Output offset (bytes) of element 4 g of 16 x 16 block (fm, f) held by
+// thread tid of tile (n0, k0) in out [N][K], or kOutOfRange past N or K:
+// lane (g, l16) of wave (wn, wk) holds output feature n = l16 and input
+// features 4g .. 4g + 3 of each block (Yq was the MFMAs' first operand).
+__device__ __forceinline__ uint32_t dw_out_off(int n0, int k0, int tid, int fm, int f, int N, int K) {
+  using namespace dwk;
+  const int wave = tid >> 6, lane = tid & 63;
+  const int n = n0 + (wave / kWavesK) * WN + fm * 16 + (lane & 15);
+  const int k = k0 + (wave % kWavesK) * WK + f * 16 + 4 * (lane >> 4);
+  return (n < N && k < K) ? (static_cast<uint32_t>(n) * static_cast<uint32_t>(K) + static_cast<uint32_t>(k)) * 4u
+                          : kOutOfRange;
+}
+
+// dO [T][Np] and q [T][K] of T tokens; out [N][K], or [split_all][N][K]
+// parts when split_all > 1; parts: the tail pieces' slots (see DwPlan).
 __global__ __launch_bounds__(dwk::kThreads) void dw_kernel(const uint16_t* __restrict__ dO,
                                                            const int8_t* __restrict__ q,
                                                            const float* __restrict__ a_scale, int T, int Np,
-                                                           int N, int K, DwPlan plan, float* __restrict__ out_base) {
+                                                           int N, int K, DwPlan plan, float* __restrict__ out_base,
+                                                           float* __restrict__ parts) {
   using namespace dwk;
   __shared__ __attribute__((aligned(16))) char smem[S * kStageBytes];
   const int tid = threadIdx.x;
@@ -441,208 +461,289 @@ __global__ __launch_bounds__(dwk::kThreads) void dw_kernel(const uint16_t* __res
   const int wn = wave / kWavesK, wk = wave % kWavesK;
   const int l16 = lane & 15;
   const int g = lane >> 4;
-  // work unit -> tile and token range (see DwPlan)
+  // work unit -> one or two pieces (tile, token range [ta, tb), slot; slot
+  // -1: stored to out)
   const int u = blockIdx.x;
-  const int tile = static_cast<int>(u % plan.tiles);
-  const int split = static_cast<int>(u / plan.tiles);
-  const int nsplit = static_cast<int>(plan.split_all);
-  int64_t tnn, tkk;
-  tile_coords(tile, (N + BN - 1) / BN, (K + BK - 1) / BK, tnn, tkk);
-  const int n0 = static_cast<int>(tnn) * BN;
-  const int k0 = static_cast<int>(tkk) * BK;
-  // this split's tokens
-  const int per = (T + nsplit - 1) / nsplit;
-  const int per64 = (per + BT - 1) / BT * BT;
-  const int t0 = split * per64 < T ? split * per64 : T;
-  const int t1 = t0 + per64 < T ? t0 + per64 : T;
-  float* out = out_base + static_cast<int64_t>(split) * N * K;
-  const int KT = t1 > t0 ? (t1 - t0 + BT - 1) / BT : 0;
-  const uint32_t rowb = 2u * static_cast<uint32_t>(Np);
-  const v4i ddesc = buffer_desc(dO + static_cast<int64_t>(t0) * Np, static_cast<uint32_t>(t1 - t0) * rowb);
-  const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(smem));
-
-  // dO DMA: instruction i of the stage covers token rows 2i, 2i + 1; lane
-  // (row half, slot) copies logical chunk slot ^ sw(row)
-  uint32_t d_src[kDmaPerWave];
-#pragma unroll
-  for (int i = 0; i < kDmaPerWave; ++i) {
-    const int ins = wave * kDmaPerWave + i;
-    const int row = 2 * ins + (lane >> 5);
-    const int c = (lane & 31) ^ dw_swz(row);
-    const int n = n0 + c * 8;
-    d_src[i] = n < Np ? static_cast<uint32_t>(row) * rowb + 2u * static_cast<uint32_t>(n) : kOutOfRange;
-  }
-  // q staging: thread (row tid / 8, p = tid % 8) owns the 8-column chunks
-  // p + 8i (i = 0 .. 3) of its token row, so the 8 threads of a row write 8
-  // distinct bank groups per store and the next row (swizzle differing by
-  // 8) the other 8.
-  const int q_row = tid >> 3, q_part = tid & 7;
-  uint32_t q_src[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int k = k0 + 8 * (q_part + 8 * i);
-    q_src[i] = k < K ? static_cast<uint32_t>(q_row) * static_cast<uint32_t>(K) + static_cast<uint32_t>(k) : kOutOfRange;
-  }
-  const int q_sw = dw_swz(q_row);
-  auto issue_dma = [&](int kt) {
-    const uint32_t base = lds0 + static_cast<uint32_t>((kt % S) * kStageBytes);
-    const uint32_t tb = static_cast<uint32_t>(kt * BT) * rowb;
-    const bool live = kt < KT;
-#pragma unroll
-    for (int i = 0; i < kDmaPerWave; ++i) {
-      const uint32_t off = (d_src[i] == kOutOfRange || !live) ? kOutOfRange : d_src[i] + tb;
-      lds_dma16(__builtin_amdgcn_readfirstlane(base + (wave * kDmaPerWave + i) * 1024), off, ddesc);
+  int npiece = 1, tile_a, ta_a, tb_a, slot_a = -1, tile_b = 0, ta_b = 0, tb_b = 0, slot_b = -1;
+  float* out = out_base;
+  if (plan.split_all > 1) {
+    const int split = static_cast<int>(u / plan.tiles);
+    const int nsplit = static_cast<int>(plan.split_all);
+    const int per = (T + nsplit - 1) / nsplit;
+    const int per64 = (per + BT - 1) / BT * BT;
+    tile_a = static_cast<int>(u % plan.tiles);
+    ta_a = split * per64 < T ? split * per64 : T;
+    tb_a = ta_a + per64 < T ? ta_a + per64 : T;
+    out = out_base + static_cast<int64_t>(split) * N * K;
+  } else if (u < plan.full) {
+    tile_a = u;
+    ta_a = 0;
+    tb_a = T;
+  } else {
+    // tail unit v: stages [v I, v I + I) of the tail tiles' stages laid end
+    // to end (I = tail_steps <= a tile's stage count, so at most two tiles)
+    const int64_t kts = (T + BT - 1) / BT;
+    const int64_t v = u - plan.full;
+    const int64_t a = v * plan.tail_steps;
+    const int64_t b = a + plan.tail_steps < plan.tail_tiles * kts ? a + plan.tail_steps : plan.tail_tiles * kts;
+    const int64_t ia = a / kts, ib = (b - 1) / kts;
+    tile_a = static_cast<int>(plan.full + ia);
+    ta_a = static_cast<int>((a - ia * kts) * BT);
+    tb_a = static_cast<int>(((ia == ib ? b : (ia + 1) * kts) - ia * kts) * BT);
+    tb_a = tb_a < T ? tb_a : T;
+    slot_a = static_cast<int>(v + ia);
+    if (ib != ia) {
+      npiece = 2;
+      tile_b = static_cast<int>(plan.full + ib);
+      tb_b = static_cast<int>((b - ib * kts) * BT);
+      tb_b = tb_b < T ? tb_b : T;
+      slot_b = static_cast<int>(v + ib);
     }
-  };
-  // The thread's 32 q values and its token's a_scale (zero past the range)
-  // are loaded by inline assembly, so the compiler inserts no wait for them
-  // (its count of outstanding loads would not include the LDS-DMA copies
-  // issued behind them, and it would wait for those too); wait_q ties the
-  // registers to an explicit vmcnt wait.  Every load is issued and consumed
-  // within one loop iteration, so the registers never pass a loop back-edge.
-  const v4i qdesc = buffer_desc(q + static_cast<int64_t>(t0) * K, static_cast<uint32_t>(t1 - t0) * static_cast<uint32_t>(K));
-  const v4i adesc = buffer_desc(a_scale + t0, static_cast<uint32_t>(t1 - t0) * 4u);
-  int2 qv0, qv1, qv2, qv3;
-  float qa;
-  auto issue_q = [&](int kt) {
-    const uint32_t tb = static_cast<uint32_t>(kt * BT) * static_cast<uint32_t>(K);
-    const bool live = kt < KT;
-    uint32_t o[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) o[i] = (q_src[i] == kOutOfRange || !live) ? kOutOfRange : q_src[i] + tb;
-    const uint32_t oa = live ? 4u * static_cast<uint32_t>(kt * BT + q_row) : kOutOfRange;
-    asm volatile("buffer_load_dwordx2 %0, %1, %2, 0 offen" : "=v"(qv0) : "v"(o[0]), "s"(qdesc) : "memory");
-    asm volatile("buffer_load_dwordx2 %0, %1, %2, 0 offen" : "=v"(qv1) : "v"(o[1]), "s"(qdesc) : "memory");
-    asm volatile("buffer_load_dwordx2 %0, %1, %2, 0 offen" : "=v"(qv2) : "v"(o[2]), "s"(qdesc) : "memory");
-    asm volatile("buffer_load_dwordx2 %0, %1, %2, 0 offen" : "=v"(qv3) : "v"(o[3]), "s"(qdesc) : "memory");
-    asm volatile("buffer_load_dword %0, %1, %2, 0 offen" : "=v"(qa) : "v"(oa), "s"(adesc) : "memory");
-  };
-  // wait until only the kDmaPerWave copies issued behind the q loads remain
-  auto wait_q = [&]() {
-    asm volatile("s_waitcnt vmcnt(%5)"
-                 : "+v"(qv0), "+v"(qv1), "+v"(qv2), "+v"(qv3), "+v"(qa)
-                 : "n"(kDmaPerWave)
-                 : "memory");
-  };
-  // the Yq of chunk i of this thread's token row (quarter i of its q)
-  auto write_yq_chunk = [&](int kt, int i) {
-    char* dst = smem + (kt % S) * kStageBytes + kTile + q_row * kRow;
-    const int2 qi = i == 0 ? qv0 : i == 1 ? qv1 : i == 2 ? qv2 : qv3;
-    uint32_t b[4];
-    yq8(qi, qa, b);
-    const int slot = (q_part + 8 * i) ^ q_sw;
-    *reinterpret_cast<v4i*>(dst + slot * 16) =
-        v4i{static_cast<int>(b[0]), static_cast<int>(b[1]), static_cast<int>(b[2]), static_cast<int>(b[3])};
-  };
-  auto write_yq = [&](int kt) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) write_yq_chunk(kt, i);
-  };
-
-  // transpose-read offsets: lane (g, l16) names token row 8g + 4h + (l16 >> 2)
-  // and columns c0 + 4 (l16 & 3) .. + 3
-  const int tj = l16 & 3, te = l16 >> 2;
-  const int r_sw = dw_swz(8 * g + te);  // the same for both halves and steps
-  auto tr_off = [&](int c0) -> uint32_t {
-    const int chunk = (c0 >> 3) + (tj >> 1);
-    return static_cast<uint32_t>(((chunk ^ r_sw) << 4) + 8 * (tj & 1));
-  };
-  uint32_t offA[FM], offB[FN];
-#pragma unroll
-  for (int fm = 0; fm < FM; ++fm) offA[fm] = tr_off(wn * WN + fm * 16);
-#pragma unroll
-  for (int f = 0; f < FN; ++f) offB[f] = kTile + tr_off(wk * WK + f * 16);
-  const uint32_t row_base = static_cast<uint32_t>((8 * g + te) * kRow);
-  auto frag = [&](int s, uint32_t off) -> v4i {
-    const int kt = s / KS, ks = s % KS;
-    const char* base = smem + (kt % S) * kStageBytes + ks * 32 * kRow + row_base + off;
-    typedef __attribute__((address_space(3))) v4s lds_v4s;
-    const v4s lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s*)(base));
-    const v4s hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s*)(base + 4 * kRow));
-    const int2 l2 = __builtin_bit_cast(int2, lo), h2 = __builtin_bit_cast(int2, hi);
-    return v4i{l2.x, l2.y, h2.x, h2.y};
-  };
-
-  v4f acc[FM][FN];
-#pragma unroll
-  for (int a = 0; a < FM; ++a)
-#pragma unroll
-    for (int b = 0; b < FN; ++b) acc[a][b] = v4f{0.f, 0.f, 0.f, 0.f};
-
-  // Schedule (stage kt = steps 2kt, 2kt + 1; slot kt % 2).  Step 2kt turns
-  // stage kt + 1's q into Yq in the other slot; the first thing of step
-  // 2kt + 1 is the barrier that makes stage kt + 1 complete everywhere, after
-  // which stage kt + 2's q and dO copies go out (into the slot of stage kt,
-  // whose last reads were the read-ahead of step 2kt) and step 2kt + 1's
-  // MFMAs run with the read-ahead of step 2kt + 2.  Copies past the last
-  // stage read zero and are never used.  After the prologue's copies of
-  // stage 1 only those are waited for (vmcnt kDmaPerWave), which also
-  // covers stage 0's copies and q loads issued before them.
-  if (KT > 0) {
-    v4i af[FM], b0[FN], b1[FN];
-    // one 32-token step: its MFMAs, with the next step's fragments read and
-    // (convert) a quarter of a stage's Yq formed behind every other group
-    auto mma = [&](const v4i (&bc)[FN], v4i (&bn)[FN], int next_step, bool read_next, bool convert, int conv_kt) {
-      __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-      for (int fm = 0; fm < FM; ++fm) {
-#pragma unroll
-        for (int f = 0; f < FN; ++f) acc[fm][f] = mfma_bf16(bc[f], af[fm], acc[fm][f]);
-        if (read_next) af[fm] = frag(next_step, offA[fm]);
-        if (read_next && fm < FN) bn[fm] = frag(next_step, offB[fm]);
-        if (convert && fm == 1) wait_q();
-        if (convert && (fm & 1)) write_yq_chunk(conv_kt, fm >> 1);
-        __builtin_amdgcn_sched_barrier(0);
-      }
-    };
-    issue_q(0);
-    issue_dma(0);
-    wait_q();
-    write_yq(0);
-    const bool two = KT > 1;
-    if (two) issue_q(1);
-    issue_dma(1);
-    __builtin_amdgcn_s_waitcnt(MMF_WAIT_VM_LGKM0(kDmaPerWave));
-    __builtin_amdgcn_s_barrier();
-#pragma unroll
-    for (int fm = 0; fm < FM; ++fm) af[fm] = frag(0, offA[fm]);
-#pragma unroll
-    for (int f = 0; f < FN; ++f) b0[f] = frag(0, offB[f]);
-    // step 0: stage 1's Yq, MFMAs with the read-ahead of step 1
-    mma(b0, b1, 1, true, two, 1);
-    for (int kt = 0; kt < KT; ++kt) {
-      const bool next = kt + 1 < KT;
-      // step 2kt + 1
+  }
+  for (int pc = 0; pc < npiece; ++pc) {
+    const int tile = pc ? tile_b : tile_a;
+    const int t0 = pc ? ta_b : ta_a, t1 = pc ? tb_b : tb_a;
+    const int slot = pc ? slot_b : slot_a;
+    if (pc) {
+      // the first piece's LDS reads and stores are done everywhere before the
+      // second's copies go out
       __builtin_amdgcn_s_waitcnt(MMF_WAIT_VM_LGKM0(0));
       __builtin_amdgcn_s_barrier();
-      __builtin_amdgcn_sched_barrier(0);
-      // (q is loaded exactly when step 2kt + 2 converts it, under the same
-      // condition, so its registers stay live until their wait)
-      const bool q_next = kt + 2 < KT;
-      if (q_next) issue_q(kt + 2);
-      issue_dma(kt + 2);
-      mma(b1, b0, 2 * kt + 2, next, false, 0);
-      // step 2kt + 2 (the first step of stage kt + 1): stage kt + 2's Yq
-      if (next) mma(b0, b1, 2 * kt + 3, true, q_next, kt + 2);
     }
-    __builtin_amdgcn_s_waitcnt(MMF_WAIT_VM_LGKM0(0));
-  }
+    int64_t tnn, tkk;
+    tile_coords(tile, (N + BN - 1) / BN, (K + BK - 1) / BK, tnn, tkk);
+    const int n0 = static_cast<int>(tnn) * BN;
+    const int k0 = static_cast<int>(tkk) * BK;
+    const int KT = t1 > t0 ? (t1 - t0 + BT - 1) / BT : 0;
+    const uint32_t rowb = 2u * static_cast<uint32_t>(Np);
+    const v4i ddesc = buffer_desc(dO + static_cast<int64_t>(t0) * Np, static_cast<uint32_t>(t1 - t0) * rowb);
+    const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(smem));
 
-  // epilogue: lane (g, l16) holds output feature n = l16 and input features
-  // 4g .. 4g + 3 of each 16 x 16 block (Yq was the first operand)
-  const uint32_t out_bytes = static_cast<uint32_t>(N) * static_cast<uint32_t>(K) * 4u;
-  const __amdgpu_buffer_rsrc_t orsrc = __builtin_amdgcn_make_buffer_rsrc(out, 0, static_cast<int>(out_bytes), kBufferFlags);
+    // dO DMA: instruction i of the stage covers token rows 2i, 2i + 1; lane
+    // (row half, slot) copies logical chunk slot ^ sw(row)
+    uint32_t d_src[kDmaPerWave];
 #pragma unroll
-  for (int fm = 0; fm < FM; ++fm) {
-    const int n = n0 + wn * WN + fm * 16 + l16;
+    for (int i = 0; i < kDmaPerWave; ++i) {
+      const int ins = wave * kDmaPerWave + i;
+      const int row = 2 * ins + (lane >> 5);
+      const int c = (lane & 31) ^ dw_swz(row);
+      const int n = n0 + c * 8;
+      d_src[i] = n < Np ? static_cast<uint32_t>(row) * rowb + 2u * static_cast<uint32_t>(n) : kOutOfRange;
+    }
+    // q staging: thread (row tid / 8, p = tid % 8) owns the 8-column chunks
+    // p + 8i (i = 0 .. 3) of its token row, so the 8 threads of a row write 8
+    // distinct bank groups per store and the next row (swizzle differing by
+    // 8) the other 8.
+    const int q_row = tid >> 3, q_part = tid & 7;
+    uint32_t q_src[4];
 #pragma unroll
-    for (int f = 0; f < FN; ++f) {
-      const int k = k0 + wk * WK + f * 16 + 4 * g;
-      const uint32_t off = (n < N && k < K) ? (static_cast<uint32_t>(n) * static_cast<uint32_t>(K) + static_cast<uint32_t>(k)) * 4u
-                                            : kOutOfRange;
-      __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4i, acc[fm][f]), orsrc, off, 0, 0);
+    for (int i = 0; i < 4; ++i) {
+      const int k = k0 + 8 * (q_part + 8 * i);
+      q_src[i] = k < K ? static_cast<uint32_t>(q_row) * static_cast<uint32_t>(K) + static_cast<uint32_t>(k)
+                       : kOutOfRange;
+    }
+    const int q_sw = dw_swz(q_row);
+    auto issue_dma = [&](int kt) {
+      const uint32_t base = lds0 + static_cast<uint32_t>((kt % S) * kStageBytes);
+      const uint32_t tb = static_cast<uint32_t>(kt * BT) * rowb;
+      const bool live = kt < KT;
+#pragma unroll
+      for (int i = 0; i < kDmaPerWave; ++i) {
+        const uint32_t off = (d_src[i] == kOutOfRange || !live) ? kOutOfRange : d_src[i] + tb;
+        lds_dma16(__builtin_amdgcn_readfirstlane(base + (wave * kDmaPerWave + i) * 1024), off, ddesc);
+      }
+    };
+    // The thread's 32 q values and its token's a_scale (zero past the range)
+    // are loaded by inline assembly, so the compiler inserts no wait for them
+    // (its count of outstanding loads would not include the LDS-DMA copies
+    // issued behind them, and it would wait for those too); wait_q ties the
+    // registers to an explicit vmcnt wait.  Every load is issued and consumed
+    // within one loop iteration, so the registers never pass a loop back-edge.
+    const v4i qdesc =
+        buffer_desc(q + static_cast<int64_t>(t0) * K, static_cast<uint32_t>(t1 - t0) * static_cast<uint32_t>(K));
+    const v4i adesc = buffer_desc(a_scale + t0, static_cast<uint32_t>(t1 - t0) * 4u);
+    int2 qv0, qv1, qv2, qv3;
+    float qa;
+    auto issue_q = [&](int kt) {
+      const uint32_t tb = static_cast<uint32_t>(kt * BT) * static_cast<uint32_t>(K);
+      const bool live = kt < KT;
+      uint32_t o[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) o[i] = (q_src[i] == kOutOfRange || !live) ? kOutOfRange : q_src[i] + tb;
+      const uint32_t oa = live ? 4u * static_cast<uint32_t>(kt * BT + q_row) : kOutOfRange;
+      asm volatile("buffer_load_dwordx2 %0, %1, %2, 0 offen" : "=v"(qv0) : "v"(o[0]), "s"(qdesc) : "memory");
+      asm volatile("buffer_load_dwordx2 %0, %1, %2, 0 offen" : "=v"(qv1) : "v"(o[1]), "s"(qdesc) : "memory");
+      asm volatile("buffer_load_dwordx2 %0, %1, %2, 0 offen" : "=v"(qv2) : "v"(o[2]), "s"(qdesc) : "memory");
+      asm volatile("buffer_load_dwordx2 %0, %1, %2, 0 offen" : "=v"(qv3) : "v"(o[3]), "s"(qdesc) : "memory");
+      asm volatile("buffer_load_dword %0, %1, %2, 0 offen" : "=v"(qa) : "v"(oa), "s"(adesc) : "memory");
+    };
+    // wait until only the kDmaPerWave copies issued behind the q loads remain
+    auto wait_q = [&]() {
+      asm volatile("s_waitcnt vmcnt(%5)"
+                   : "+v"(qv0), "+v"(qv1), "+v"(qv2), "+v"(qv3), "+v"(qa)
+                   : "n"(kDmaPerWave)
+                   : "memory");
+    };
+    // the Yq of chunk i of this thread's token row (quarter i of its q)
+    auto write_yq_chunk = [&](int kt, int i) {
+      char* dst = smem + (kt % S) * kStageBytes + kTile + q_row * kRow;
+      const int2 qi = i == 0 ? qv0 : i == 1 ? qv1 : i == 2 ? qv2 : qv3;
+      uint32_t b[4];
+      yq8(qi, qa, b);
+      const int slot = (q_part + 8 * i) ^ q_sw;
+      *reinterpret_cast<v4i*>(dst + slot * 16) =
+          v4i{static_cast<int>(b[0]), static_cast<int>(b[1]), static_cast<int>(b[2]), static_cast<int>(b[3])};
+    };
+    auto write_yq = [&](int kt) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) write_yq_chunk(kt, i);
+    };
+
+    // transpose-read offsets: lane (g, l16) names token row 8g + 4h + (l16 >> 2)
+    // and columns c0 + 4 (l16 & 3) .. + 3
+    const int tj = l16 & 3, te = l16 >> 2;
+    const int r_sw = dw_swz(8 * g + te);  // the same for both halves and steps
+    auto tr_off = [&](int c0) -> uint32_t {
+      const int chunk = (c0 >> 3) + (tj >> 1);
+      return static_cast<uint32_t>(((chunk ^ r_sw) << 4) + 8 * (tj & 1));
+    };
+    uint32_t offA[FM], offB[FN];
+#pragma unroll
+    for (int fm = 0; fm < FM; ++fm) offA[fm] = tr_off(wn * WN + fm * 16);
+#pragma unroll
+    for (int f = 0; f < FN; ++f) offB[f] = kTile + tr_off(wk * WK + f * 16);
+    const uint32_t row_base = static_cast<uint32_t>((8 * g + te) * kRow);
+    auto frag = [&](int s, uint32_t off) -> v4i {
+      const int kt = s / KS, ks = s % KS;
+      const char* base = smem + (kt % S) * kStageBytes + ks * 32 * kRow + row_base + off;
+      typedef __attribute__((address_space(3))) v4s lds_v4s;
+      const v4s lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s*)(base));
+      const v4s hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s*)(base + 4 * kRow));
+      const int2 l2 = __builtin_bit_cast(int2, lo), h2 = __builtin_bit_cast(int2, hi);
+      return v4i{l2.x, l2.y, h2.x, h2.y};
+    };
+
+    v4f acc[FM][FN];
+#pragma unroll
+    for (int a = 0; a < FM; ++a)
+#pragma unroll
+      for (int b = 0; b < FN; ++b) acc[a][b] = v4f{0.f, 0.f, 0.f, 0.f};
+
+    // Schedule (stage kt = steps 2kt, 2kt + 1; slot kt % 2).  Step 2kt turns
+    // stage kt + 1's q into Yq in the other slot; the first thing of step
+    // 2kt + 1 is the barrier that makes stage kt + 1 complete everywhere, after
+    // which stage kt + 2's q and dO copies go out (into the slot of stage kt,
+    // whose last reads were the read-ahead of step 2kt) and step 2kt + 1's
+    // MFMAs run with the read-ahead of step 2kt + 2.  Copies past the last
+    // stage read zero and are never used.  After the prologue's copies of
+    // stage 1 only those are waited for (vmcnt kDmaPerWave), which also
+    // covers stage 0's copies and q loads issued before them.
+    if (KT > 0) {
+      v4i af[FM], b0[FN], b1[FN];
+      // one 32-token step: its MFMAs, with the next step's fragments read and
+      // (convert) a quarter of a stage's Yq formed behind every other group
+      auto mma = [&](const v4i (&bc)[FN], v4i (&bn)[FN], int next_step, bool read_next, bool convert, int conv_kt) {
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int fm = 0; fm < FM; ++fm) {
+#pragma unroll
+          for (int f = 0; f < FN; ++f) acc[fm][f] = mfma_bf16(bc[f], af[fm], acc[fm][f]);
+          if (read_next) af[fm] = frag(next_step, offA[fm]);
+          if (read_next && fm < FN) bn[fm] = frag(next_step, offB[fm]);
+          if (convert && fm == 1) wait_q();
+          if (convert && (fm & 1)) write_yq_chunk(conv_kt, fm >> 1);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      };
+      issue_q(0);
+      issue_dma(0);
+      wait_q();
+      write_yq(0);
+      const bool two = KT > 1;
+      if (two) issue_q(1);
+      issue_dma(1);
+      __builtin_amdgcn_s_waitcnt(MMF_WAIT_VM_LGKM0(kDmaPerWave));
+      __builtin_amdgcn_s_barrier();
+#pragma unroll
+      for (int fm = 0; fm < FM; ++fm) af[fm] = frag(0, offA[fm]);
+#pragma unroll
+      for (int f = 0; f < FN; ++f) b0[f] = frag(0, offB[f]);
+      // step 0: stage 1's Yq, MFMAs with the read-ahead of step 1
+      mma(b0, b1, 1, true, two, 1);
+      for (int kt = 0; kt < KT; ++kt) {
+        const bool next = kt + 1 < KT;
+        // step 2kt + 1
+        __builtin_amdgcn_s_waitcnt(MMF_WAIT_VM_LGKM0(0));
+        __builtin_amdgcn_s_barrier();
+        __builtin_amdgcn_sched_barrier(0);
+        // (q is loaded exactly when step 2kt + 2 converts it, under the same
+        // condition, so its registers stay live until their wait)
+        const bool q_next = kt + 2 < KT;
+        if (q_next) issue_q(kt + 2);
+        issue_dma(kt + 2);
+        mma(b1, b0, 2 * kt + 2, next, false, 0);
+        // step 2kt + 2 (the first step of stage kt + 1): stage kt + 2's Yq
+        if (next) mma(b0, b1, 2 * kt + 3, true, q_next, kt + 2);
+      }
+      __builtin_amdgcn_s_waitcnt(MMF_WAIT_VM_LGKM0(0));
+    }
+
+    if (slot >= 0) {
+      // a tail piece: its sums to the slot in register order, thread-minor
+      float* dst = parts + static_cast<int64_t>(slot) * (BN * BK) + 4 * tid;
+#pragma unroll
+      for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+        for (int f = 0; f < FN; ++f) *reinterpret_cast<v4f*>(dst + (fm * FN + f) * (4 * kThreads)) = acc[fm][f];
+    } else {
+      const uint32_t out_bytes = static_cast<uint32_t>(N) * static_cast<uint32_t>(K) * 4u;
+      const __amdgpu_buffer_rsrc_t orsrc =
+          __builtin_amdgcn_make_buffer_rsrc(out, 0, static_cast<int>(out_bytes), kBufferFlags);
+#pragma unroll
+      for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+        for (int f = 0; f < FN; ++f)
+          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4i, acc[fm][f]), orsrc,
+                                                 dw_out_off(n0, k0, tid, fm, f, N, K), 0, 0);
     }
   }
+}
+
+// The tail tiles of a DwPlan: blocks ti * kFixupSplit + j add blocks e of
+// tile full + ti held in registers e = j E .. j E + E - 1 (E = FM FN /
+// kFixupSplit), over the tile's pieces in token order (the units overlapping
+// its stages, slot = unit + ti), and store them like the kernel's epilogue.
+constexpr int kFixupSplit = 8;
+static_assert(dwk::FM * dwk::FN % kFixupSplit == 0, "fixup blocks take whole register groups");
+__global__ __launch_bounds__(dwk::kThreads) void dw_fixup_kernel(const float* __restrict__ parts, int T, int N,
+                                                                 int K, DwPlan plan, float* __restrict__ out) {
+  using namespace dwk;
+  constexpr int E = FM * FN / kFixupSplit;
+  const int tid = threadIdx.x;
+  const int64_t ti = blockIdx.x / kFixupSplit;
+  const int e0 = static_cast<int>(blockIdx.x % kFixupSplit) * E;
+  const int64_t kts = (T + BT - 1) / BT;
+  const int64_t v0 = ti * kts / plan.tail_steps, v1 = ((ti + 1) * kts - 1) / plan.tail_steps;
+  int64_t tnn, tkk;
+  tile_coords(plan.full + ti, (N + BN - 1) / BN, (K + BK - 1) / BK, tnn, tkk);
+  const int n0 = static_cast<int>(tnn) * BN;
+  const int k0 = static_cast<int>(tkk) * BK;
+  const float* src = parts + (v0 + ti) * (BN * BK) + 4 * tid;
+  v4f sum[E];
+#pragma unroll
+  for (int i = 0; i < E; ++i) sum[i] = *reinterpret_cast<const v4f*>(src + (e0 + i) * (4 * kThreads));
+  for (int64_t v = v0 + 1; v <= v1; ++v) {
+    const float* p = src + (v - v0) * (BN * BK);
+#pragma unroll
+    for (int i = 0; i < E; ++i) sum[i] += *reinterpret_cast<const v4f*>(p + (e0 + i) * (4 * kThreads));
+  }
+  const uint32_t out_bytes = static_cast<uint32_t>(N) * static_cast<uint32_t>(K) * 4u;
+  const __amdgpu_buffer_rsrc_t orsrc =
+      __builtin_amdgcn_make_buffer_rsrc(out, 0, static_cast<int>(out_bytes), kBufferFlags);
+#pragma unroll
+  for (int i = 0; i < E; ++i)
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4i, sum[i]), orsrc,
+                                           dw_out_off(n0, k0, tid, (e0 + i) / FN, (e0 + i) % FN, N, K), 0, 0);
 }
 
 }  // namespace
@@ -722,19 +823,36 @@ hipError_t launch_dgamma_finish(const double* dg_part, int64_t M, int K, float* 
 }
 
 DwPlan bwd_dw_plan(int64_t M, int64_t N, int64_t K, int64_t Np, int cus) {
-  // Split the token range while the output has too few tiles to fill the
-  // chip (parts keep at least 512 tokens), and for 32-bit offsets: a part's
-  // rows, rounded up to whole stages, plus one stage of rows past its end
-  // (which read as zero) stay below 2^31 bytes of dO and of q.  (Splitting
-  // only a last, partial round of tiles measured slower than running it
-  // whole.)
   DwPlan p;
   p.tiles = ((N + dwk::BN - 1) / dwk::BN) * ((K + dwk::BK - 1) / dwk::BK);
+  p.full = p.tiles;
   const int64_t lim = (int64_t(1) << 31) - 1;
+  // 32-bit offsets: a part's rows, rounded up to whole stages, plus one
+  // stage of rows past its end (which read as zero) stay below 2^31 bytes of
+  // dO and of q
   auto fits = [&](int64_t s) {
     const int64_t rows = (M + s - 1) / s + 2 * dwk::BT;
     return rows * 2 * Np <= lim && rows * K <= lim;
   };
+  const int64_t kts = (M + dwk::BT - 1) / dwk::BT;
+  if (p.tiles * 2 > cus && fits(1)) {
+    // whole tiles in full rounds; the last, partial round's stages spread
+    // over up to `cus` units of at least kDwMinTailSteps stages, when that
+    // saves an eighth of a tile's time or more
+    const int64_t r = p.tiles % cus;
+    if (r > 0 && kts > 0) {
+      int64_t steps = (r * kts + cus - 1) / cus;
+      if (steps < kDwMinTailSteps) steps = kDwMinTailSteps;
+      if (8 * steps <= 7 * kts) {
+        p.full = p.tiles - r;
+        p.tail_tiles = r;
+        p.tail_steps = steps;
+        p.tail_units = (r * kts + steps - 1) / steps;
+      }
+    }
+    return p;
+  }
+  // few tiles: split every tile's tokens while parts keep 512 tokens
   int64_t S = 1;
   while (p.tiles * S < (cus * 3) / 4 && M / (2 * S) >= 512) S *= 2;
   while (!fits(S)) S *= 2;
@@ -742,12 +860,22 @@ DwPlan bwd_dw_plan(int64_t M, int64_t N, int64_t K, int64_t Np, int cus) {
   return p;
 }
 
+size_t bwd_dw_parts_bytes(const DwPlan& p) {
+  return p.tail_units > 0 ? static_cast<size_t>(p.tail_units + p.tail_tiles) * dwk::BN * dwk::BK * sizeof(float) : 0;
+}
+
 hipError_t launch_dw(const uint16_t* dO, const int8_t* q, const float* a_scale, int64_t M, int64_t Np, int64_t N,
-                     int K, float* out, const DwPlan& plan, hipStream_t stream) {
+                     int K, float* out, float* parts, const DwPlan& plan, hipStream_t stream) {
   if (N * K * 4 > (int64_t(1) << 31) - 1) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(dw_kernel, dim3(static_cast<unsigned>(plan.tiles * plan.split_all)), dim3(dwk::kThreads), 0,
-                     stream, dO, q, a_scale, static_cast<int>(M), static_cast<int>(Np), static_cast<int>(N), K, plan,
-                     out);
+  if (plan.tail_units > 0 && parts == nullptr) return hipErrorInvalidValue;
+  const int64_t units = plan.split_all > 1 ? plan.tiles * plan.split_all : plan.full + plan.tail_units;
+  if (units == 0) return hipSuccess;
+  hipLaunchKernelGGL(dw_kernel, dim3(static_cast<unsigned>(units)), dim3(dwk::kThreads), 0, stream, dO, q, a_scale,
+                     static_cast<int>(M), static_cast<int>(Np), static_cast<int>(N), K, plan, out, parts);
+  if (plan.tail_units > 0)
+    hipLaunchKernelGGL(dw_fixup_kernel, dim3(static_cast<unsigned>(plan.tail_tiles * kFixupSplit)), dim3(dwk::kThreads),
+                       0, stream,
+                       parts, static_cast<int>(M), static_cast<int>(N), K, plan, out);
   return hipGetLastError();
 }
 

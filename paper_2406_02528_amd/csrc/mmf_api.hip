@@ -378,7 +378,7 @@ int device_cus() {
 struct BwdScratch {
   int64_t Np;
   mmf::DwPlan plan;
-  size_t wn_off, dop_off, spart_off, dgpart_off, colpart_off, dw_off, total;
+  size_t wn_off, dop_off, spart_off, dgpart_off, colpart_off, dw_off, parts_off, total;
 };
 BwdScratch bwd_scratch(int64_t M, int64_t K, int64_t N) {
   BwdScratch s;
@@ -395,7 +395,8 @@ BwdScratch bwd_scratch(int64_t M, int64_t K, int64_t N) {
   s.dw_off = s.colpart_off + round_up(sizeof(double) * static_cast<size_t>(mmf::col_sum_partials(M) * N),
                                       kScratchAlign);
   const int64_t S = s.plan.split_all;
-  s.total = s.dw_off + (S > 1 ? round_up(sizeof(float) * static_cast<size_t>(S * N * K), kScratchAlign) : 0);
+  s.parts_off = s.dw_off + (S > 1 ? round_up(sizeof(float) * static_cast<size_t>(S * N * K), kScratchAlign) : 0);
+  s.total = s.parts_off + round_up(mmf::bwd_dw_parts_bytes(s.plan), kScratchAlign);
   return s;
 }
 
@@ -859,10 +860,13 @@ int mmf_bitlinear_bwd(const uint16_t* dO, const void* x, int x_is_f32, const flo
       return MMF_ERR_HIP;
     if (mmf::launch_dx_finish(dx, x, f32, rstd, s_part, M, Ki, stream) != hipSuccess) return MMF_ERR_HIP;
     if (dgamma && mmf::launch_dgamma_finish(dg_part, M, Ki, dgamma, stream) != hipSuccess) return MMF_ERR_HIP;
-    // dW = dO^T Yq (token range split into parts when the output has few tiles)
+    // dW = dO^T Yq (token range split into parts when the output has few
+    // tiles; the last partial round of tiles spread over all CUs otherwise)
     const int64_t S = s.plan.split_all;
     float* dw_out = S > 1 ? reinterpret_cast<float*>(scratch + s.dw_off) : dW;
-    if (mmf::launch_dw(dOp, q, a_scale, M, s.Np, N, Ki, dw_out, s.plan, stream) != hipSuccess) return MMF_ERR_HIP;
+    float* parts = s.plan.tail_units > 0 ? reinterpret_cast<float*>(scratch + s.parts_off) : nullptr;
+    if (mmf::launch_dw(dOp, q, a_scale, M, s.Np, N, Ki, dw_out, parts, s.plan, stream) != hipSuccess)
+      return MMF_ERR_HIP;
     if (S > 1 && mmf::launch_sum_parts(dw_out, S, N * K, dW, stream) != hipSuccess) return MMF_ERR_HIP;
     if (db && mmf::launch_col_sum_bf16(dO, M, N, reinterpret_cast<double*>(scratch + s.colpart_off), db,
                                        stream) != hipSuccess)

@@ -154,16 +154,21 @@ hipError_t launch_dy(const uint16_t* dO, int64_t M, int64_t Np, const uint32_t* 
 hipError_t launch_dx_finish(float* dx, const void* x, bool x_is_f32, const float* rstd, const double* s_part,
                             int64_t M, int K, hipStream_t stream);
 hipError_t launch_dgamma_finish(const double* dg_part, int64_t M, int K, float* dgamma, hipStream_t stream);
-// Work units of the dW kernel: every tile's token range is split into
-// split_all parts (1: none), written to out [split_all][N][K] and added by
-// launch_sum_parts when there is more than one.  N * K * 4 must stay below
-// 2^31.
+// Work units of the dW kernel.  split_all > 1: every tile's token range is
+// split into split_all parts, written to out [split_all][N][K] and added by
+// launch_sum_parts.  Otherwise tiles [0, full) are whole units and the
+// stages (64 tokens each) of the tail_tiles tiles after them, laid end to
+// end, go to tail_units units of tail_steps stages; their pieces land in
+// bwd_dw_parts_bytes of slots that launch_dw adds into out by a second
+// kernel.  N * K * 4 must stay below 2^31.
 struct DwPlan {
-  int64_t tiles = 0, split_all = 1;
+  int64_t tiles = 0, split_all = 1, full = 0, tail_tiles = 0, tail_steps = 0, tail_units = 0;
 };
+constexpr int64_t kDwMinTailSteps = 8;
 DwPlan bwd_dw_plan(int64_t M, int64_t N, int64_t K, int64_t Np, int cus);
+size_t bwd_dw_parts_bytes(const DwPlan& plan);
 hipError_t launch_dw(const uint16_t* dO, const int8_t* q, const float* a_scale, int64_t M, int64_t Np, int64_t N,
-                     int K, float* out, const DwPlan& plan, hipStream_t stream);
+                     int K, float* out, float* parts, const DwPlan& plan, hipStream_t stream);
 
 hipError_t launch_glu_pack(const uint32_t* Wg, const uint32_t* Wu, int64_t L, int K, uint32_t* Wgu,
                            hipStream_t stream);

@@ -45,7 +45,7 @@ def compare_p(p_gpu, p_ref, acc_g, acc_u, flip_rows_mask):
     zero = (acc_g == 0) | (acc_u == 0)
     assert (p_gpu[ok][zero[ok]] == 0).all(), "nonzero p where a ternary sum is 0"
     bound = P_REL * np.abs(p_ref) + P_TAIL_ABS * rowmax
-    bad = (err > bound) & ok[:, None]
+    bad = ~(err <= bound) & ok[:, None]   # NaN counts as out of bound
     assert not bad.any(), f"{int(bad.sum())} p values out of bound, worst {float((err - bound).max()):.3e}"
     for m in np.nonzero(flip_rows_mask)[0]:
         assert err[m].max(initial=0.0) <= P_REL * rowmax[m, 0] + 1e-30

@@ -103,7 +103,7 @@ def check_gates(fcg_gpu, z_ref, bias, lb, flip_mask, ra):
               e_z[:, 2 * d:] + 1e-30]
     for s, name in enumerate("fcg"):
         seg = np.s_[s * d:(s + 1) * d]
-        bad = err[:, seg] > bounds[s]
+        bad = ~(err[:, seg] <= bounds[s])   # NaN counts as out of bound
         if bad.any():
             m, n = np.argwhere(bad)[0]
             n += s * d
@@ -138,7 +138,7 @@ def check_scan(o_gpu, h_gpu, fcg, B, T, h0):
     g = np.abs(fcg[:, 2 * d:].astype(np.float64))
     tol_o = g * (tol_h + U) / 4 + 6 * U * np.abs(o_ref.astype(np.float64)) + 1e-30
     err_o = np.abs(o_gpu.astype(np.float64) - o_ref)
-    bad = err_o > tol_o
+    bad = ~(err_o <= tol_o)
     assert not bad.any(), f"o': {int(bad.sum())} out of bound, worst excess {float((err_o - tol_o).max()):.3e}"
     if h_gpu is not None:
         last = tol_h.reshape(B, T, d)[:, -1]
@@ -153,7 +153,7 @@ def check_bias_out(y_gpu, y_ref, b, flip_mask, ra):
     tol = (3 * U + ra[:, None]) * np.abs(y) + 2 * U * np.abs(out) + 1e-30
     tol = tol + ROW_REL * np.abs(y).max(axis=1, keepdims=True) * flip_mask[:, None]
     err = np.abs(y_gpu.astype(np.float64) - out)
-    bad = err > tol
+    bad = ~(err <= tol)   # NaN counts as out of bound
     assert not bad.any(), f"{int(bad.sum())} outputs out of bound, worst excess {float((err - tol).max()):.3e}"
 
 

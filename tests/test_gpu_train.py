@@ -122,7 +122,7 @@ def bwd_bounds(dO, x, gamma, r, t, ws, yq, dY, exact_dy: bool):
 
 def check(name, got, ref, tol):
     err = np.abs(got.astype(np.float64) - ref.astype(np.float64))
-    bad = err > tol
+    bad = ~(err <= tol)   # NaN counts as out of bound
     if bad.any():
         i = np.unravel_index(np.argmax(err - tol), err.shape)
         raise AssertionError(f"{name}: {int(bad.sum())} out of bound; worst at {i}: got {got[i]!r} "
@@ -186,13 +186,53 @@ def test_bwd_optional_outputs_and_workspace(mmf):
     assert torch.equal(dx1, dx2) and torch.equal(dW1, dW2)
 
 
+@pytest.mark.parametrize("M,K,N", [(1000, 2288, 3998),    # 144 dW tiles: all of them spread over 256 units
+                                   (1000, 3840, 5120)])   # 300 tiles: 256 whole, 44 spread over 88 units
+def test_bwd_dw_tail_pieces(mmf, M, K, N):
+    """dW with more output tiles than half the compute units (256 on MI355X):
+    whole tiles take the full rounds of workgroups and the stages of the
+    remaining tiles are spread evenly over one more round, in pieces that a
+    unit may take from two tiles and that a second kernel adds.  dW is checked
+    against the oracle on every output row of the first and the last (ragged)
+    256-row tile and on one row of every other, so each tile is covered;
+    dx on sampled token rows; db on the sampled columns."""
+    log(f"[bwd tail] M={M} K={K} N={N}")
+    rs = np.random.default_rng(9300 + N)
+    bits, xf, gamma, W = workloads.random_case(rs, M, K, N)
+    x_d, g_d = to_dev_x(bits), T_(gamma)
+    fw = train_fwd_gpu(mmf, x_d, g_d, W, None)
+    t, ws = oracle.weight_quant(W)
+    assert np.array_equal(packed_to_np(fw["Wp"]), oracle.pack(t))
+    dO_bits = workloads.f32_to_bf16_bits(rs.standard_normal((M, N)).astype(np.float32))
+    dO_f = workloads.bf16_bits_to_f32(dO_bits)
+    dx = torch.full((M, K), float("nan"), dtype=torch.float32, device=dev())
+    dW = torch.full((N, K), float("nan"), dtype=torch.float32, device=dev())
+    db = torch.full((N,), float("nan"), dtype=torch.float32, device=dev())
+    mmf.mmf_bitlinear_bwd(bf16_tensor(dO_bits), x_d, g_d, fw["r"], fw["q"], fw["a"], fw["Wp"], fw["ws"],
+                          dx, dW, db, None)
+    torch.cuda.synchronize()
+    q, a, r = fw["q"].cpu().numpy(), fw["a"].cpu().numpy(), fw["r"].cpu().numpy()
+    rows = np.unique(np.concatenate([rs.integers(0, M, 40), [0, M - 1]]))
+    ref = oracle.bitlinear_bwd(dO_f[rows], xf[rows], gamma, r[rows], q[rows], a[rows], t, ws)
+    tdx, _, _, _ = bwd_bounds(dO_f[rows], xf[rows], gamma, r[rows], t, ws, ref["yq"], ref["dY"], False)
+    check("dx (sampled rows)", dx.cpu().numpy()[rows], ref["dx"], tdx)
+    last = (N - 1) // 256 * 256
+    one_per_tile = [rs.integers(n0, min(n0 + 256, N)) for n0 in range(256, last, 256)]
+    cols = np.unique(np.concatenate([np.arange(0, 256), one_per_tile, np.arange(last, N)]))
+    ref = oracle.bitlinear_bwd(dO_f[:, cols], xf, gamma, r, q, a, t[cols], ws)
+    _, tdW, tdb, _ = bwd_bounds(dO_f[:, cols], xf, gamma, r, t[cols], ws, ref["yq"], ref["dY"], False)
+    check("dW (output rows)", dW.cpu().numpy()[cols], ref["dW"], tdW)
+    check("db (sampled)", db.cpu().numpy()[cols], ref["db"], tdb)
+
+
 @pytest.mark.parametrize("name", ["train_d1024", "train_glu_up"])
 def test_train_workload_full_size_sampled(mmf, name):
     """The paper's training-efficiency setting (input size and sequence length
     1024; 16 sequences, M = 16384, K = N = 1024; its dW has 16 output tiles, so
     every tile's token range is split) and the 1.3B model's GLU up-projection
-    over 8192 tokens (352 dW tiles: the last, partial round over the compute
-    units is split in two and added by the part finishing last): training
+    over 8192 tokens (352 dW tiles: 256 whole, the stages of the other 96
+    spread evenly over 256 more units and their pieces added by a second
+    kernel): training
     forward and backward at full size; dx rows and dW rows sampled from two
     oracle calls (rows of tokens, then columns of outputs), db sampled."""
     w = workloads.TRAIN_WORKLOADS[name]
