@@ -133,9 +133,10 @@ int mmf_act_quant_ex(const void *x, int x_is_f32, const float *gamma, int8_t *q,
  *   y[m][n] = a_scale[m] * w_scale * sum_k q[m][k] t[n][k]
  * with q, a_scale from the act-quant step above and t from Wpacked.  The
  * integer sum is exact; the product is fp32 (a_scale[m] * w_scale first).
- * Up to 64 tokens take the decode kernel in launches of at most 16 tokens
- * (16x16x64 int8 MFMA over 16 columns by the token rows; weights streamed
- * once per launch), larger M the int8 MFMA GEMM kernel.  Allocates its M*K + 8*M byte scratch stream-ordered
+ * Up to 32 tokens (K <= 2048) or 64 (larger K) take the decode kernel in
+ * launches of at most 16 tokens (16x16x64 int8 MFMA over 16 columns by the
+ * token rows; weights streamed once per launch), larger M the int8 MFMA GEMM
+ * kernel.  Allocates its M*K + 8*M byte scratch stream-ordered
  * (hipMallocAsync); mmf_bitlinear_fwd_ws takes caller scratch instead.
  * x: [M][K] bf16 bits; gamma: [K] or NULL; Wpacked: [K/16][N]; w_scale: [1];
  * y: [M][N] float32 out.
@@ -172,8 +173,9 @@ int mmf_bitlinear_fwd_ws(const void *x, int x_is_f32, const float *gamma,
  * that each GPU the library runs on holds until the process ends.  No call
  * allocates or frees memory; the array's address is looked up once per
  * device, on the first call there.  Calls that need more scratch than the
- * array holds return MMF_ERR_WORKSPACE before anything is enqueued (up to 64
- * tokens the fused decode kernel needs none).  Every call on a GPU shares that
+ * array holds return MMF_ERR_WORKSPACE before anything is enqueued (the
+ * fused decode kernel, up to 32 tokens at K <= 2048 and 64 beyond, needs
+ * none).  Every call on a GPU shares that
  * GPU's array: calls that overlap on one GPU (on different streams, or from
  * different host threads) race; serialise them.  The array keeps the last
  * call's contents, which every call overwrites before reading.
@@ -234,9 +236,10 @@ int mmf_ternary_gemm_i32(const int8_t *q, const uint32_t *Wpacked,
  *
  * mmf_glu_fwd: x [M][K] bf16 bits (mmf_glu_fwd_f32: float32); gamma [K] or
  * NULL; Wgu_packed [K/16][2L] from mmf_glu_pack; w_scales [2] = gate, up;
- * p [M][L] float32 out.  Up to 64 tokens run the fused decode kernel with
- * the same SiLU(g) * u epilogue (launches of at most 16 tokens; the result is
- * bit-identical to the GEMM kernel's), larger M the int8 MFMA GEMM kernel.  Allocates the
+ * p [M][L] float32 out.  Up to 32 tokens (K <= 2048) or 64 (larger K) run
+ * the fused decode kernel with the same SiLU(g) * u epilogue (launches of at
+ * most 16 tokens; the result is bit-identical to the GEMM kernel's), larger M
+ * the int8 MFMA GEMM kernel.  Allocates the
  * same stream-ordered scratch as mmf_bitlinear_fwd; mmf_glu_fwd_ws takes
  * caller scratch of mmf_bitlinear_workspace_bytes(M, K) bytes instead.
  */
@@ -306,8 +309,8 @@ int mmf_bitlinear_fwd_bias(const void *x, int x_is_f32, const float *gamma,
  * with s evaluated as for the GLU gate (hardware exp2 and reciprocal). The
  * recurrence's output gate o' = g * s(h) uses the same s.
  * x [M][K] bf16 bits or float32 (x_is_f32); bias [3d] or NULL; lb [d] or
- * NULL.  M <= 64 runs the fused decode kernel (launches of at most 16
- * tokens), larger M the int8 MFMA GEMM kernel. */
+ * NULL.  M <= 32 (K <= 2048) or 64 (larger K) runs the fused decode kernel
+ * (launches of at most 16 tokens), larger M the int8 MFMA GEMM kernel. */
 size_t mmf_mlgru_proj_workspace_bytes(int64_t M, int64_t K, int64_t d);
 int mmf_mlgru_proj(const void *x, int x_is_f32, const float *gamma, const uint32_t *Wfcg,
                    const float *w_scales, const float *bias, const float *lb, float *fcg,
@@ -399,7 +402,8 @@ int mmf_bitlinear_bwd(const uint16_t *dO, const void *x, int x_is_f32, const flo
 
 /*
  * Kernel selection for the contraction: MMF_PATH_AUTO (decode kernel for
- * M <= 64, in launches of at most 16 tokens; the GEMM kernel otherwise),
+ * M <= 32 at K <= 2048 and M <= 64 beyond, in launches of at most 16
+ * tokens; the GEMM kernel otherwise),
  * MMF_PATH_GEMV or MMF_PATH_GEMM force one kernel for every M (the decode
  * kernel handles at most 16 tokens per launch and is launched once per
  * 16-token slice when forced).  Process-wide; returns

@@ -15,6 +15,10 @@
 // square one (the int8 rows of q are the heavy operand, the 2-bit weight
 // columns the light one): 32 KB per 128-deep stage for 128 x 512 against
 // 40 KB for 256 x 256, and the global->LDS copies are what limits the loop.
+// A problem with few such tiles (a short M, a narrow N) runs on 64 x 512 or
+// 64 x 256 tiles instead (waves of 64 x 64 or 32 x 64), whichever finishes
+// first by the rule of gemm_tile_choice: a lone tile's k loop is latency-
+// bound, so more, smaller tiles on more CUs beat a few wide ones.
 //
 // Operands and pipeline:
 //  - The operands of one BK = 128 deep k stage stream through a 3-slot LDS
@@ -73,7 +77,7 @@ struct Tiling {
   static constexpr int kStageBytes = kABytes + kBBytes;
   static_assert(kAInstr % kWaves == 0 && kBInstr % kWaves == 0, "loads must split evenly");
   static_assert(S == 3, "the stage waits below assume a 3-slot ring");
-  static_assert(FN == 4 && FM >= 2 * FN, "expansion schedule: four words, one per late fragment");
+  static_assert(FN == 4 && FM >= 2, "expansion schedule: four words behind the fragment groups");
   static_assert(kLoadsPerStage <= FM, "one stage load per fragment group");
   static_assert(BK == 128, "A swizzle is for 8 chunks per row");
 };
@@ -206,6 +210,14 @@ __global__ __launch_bounds__((Tiling<BM, BN, WM, WN, BK, S, BX4>::kThreads)) voi
     const uint32_t* Bs = reinterpret_cast<const uint32_t*>(smem + (kt % S) * T::kStageBytes + T::kABytes);
     return Bs[(ks * 4 + g) * T::kBRow + wn * WN + f * 16 + l16];
   };
+  constexpr auto exp_lo = [](int fm) constexpr -> int {
+    if constexpr (FM >= 2 * FN) return fm >= FM - FN ? fm - (FM - FN) : 0;
+    else return fm == 0 ? 0 : ((fm - 1) * FN) / (FM - 1);
+  };
+  constexpr auto exp_hi = [](int fm) constexpr -> int {
+    if constexpr (FM >= 2 * FN) return fm >= FM - FN ? fm - (FM - FN) + 1 : 0;
+    else return fm == 0 ? 0 : (fm * FN) / (FM - 1);
+  };
   auto expand = [](uint32_t x) -> v4i {
     return v4i{static_cast<int>(codes4(x, 0)), static_cast<int>(codes4(x, 1)),
                static_cast<int>(codes4(x, 2)), static_cast<int>(codes4(x, 3))};
@@ -270,7 +282,11 @@ __global__ __launch_bounds__((Tiling<BM, BN, WM, WN, BK, S, BX4>::kThreads)) voi
         acc[fm][f] = __builtin_amdgcn_mfma_i32_16x16x64_i8(bc[f], af[fm], acc[fm][f], 0, 0, 0);
       af[fm] = a_read(s + 1, fm);
       if (refill && fm < T::kLoadsPerStage) issue_one(kt + S - 1, fm);
-      if (fm >= FM - FN) bn[fm - (FM - FN)] = expand(bw[fm - (FM - FN)]);
+      // the next step's words, expanded behind this step's groups: one in
+      // each of the last FN groups when there are at least 2 FN groups, else
+      // spread over groups 1 .. FM - 1 (group 0 leaves their LDS reads time)
+#pragma unroll
+      for (int f = exp_lo(fm); f < exp_hi(fm); ++f) bn[f] = expand(bw[f]);
       __builtin_amdgcn_sched_barrier(0);
     }
   };
@@ -418,6 +434,30 @@ hipError_t launch_cfg(const ContractArgs& a, int64_t m_begin, int64_t m_rows, hi
 
 }  // namespace
 
+int gemm_tile_choice(int64_t rows, int64_t N, int cus) {
+  // Estimated time = rounds of workgroups over the CUs x the time of one
+  // tile's k loop when it runs alone, measured relative to each other at
+  // K = 2048 (128 x 512 : 64 x 512 : 64 x 256 = 29.5 : 18.6 : 14.0 us, i.e.
+  // 21 : 13 : 10).  The widest tile has the most reuse per operand byte and
+  // wins once a problem fills the CUs; a problem with few such tiles (short
+  // M, or narrow N) finishes sooner with more, smaller tiles.  Ties keep the
+  // wider tile.
+  struct Shape { int64_t bm, bn, cost; };
+  constexpr Shape kShapes[] = {{128, 512, 21}, {64, 512, 13}, {64, 256, 10}};
+  const int64_t c = cus > 0 ? cus : 256;
+  int best = 0;
+  int64_t best_t = -1;
+  for (int i = 0; i < 3; ++i) {
+    const int64_t tiles = ((rows + kShapes[i].bm - 1) / kShapes[i].bm) * ((N + kShapes[i].bn - 1) / kShapes[i].bn);
+    const int64_t t = (tiles + c - 1) / c * kShapes[i].cost;
+    if (best_t < 0 || t < best_t) {
+      best = i;
+      best_t = t;
+    }
+  }
+  return best;
+}
+
 hipError_t launch_gemm(const ContractArgs& a, hipStream_t stream) {
   // 32-bit buffer offsets: a launch covers at most 2^31 - 1 bytes of q, of
   // packed weights and of output; taller problems run in row slices.  The
@@ -425,10 +465,14 @@ hipError_t launch_gemm(const ContractArgs& a, hipStream_t stream) {
   const int64_t slice = gemm_row_slice(a.K, a.N);
   if (slice == 0) return hipErrorInvalidValue;
   const bool bx4 = (a.N % 4) == 0;
+  const int cus = device_cus();
   for (int64_t m0 = 0; m0 < a.M; m0 += slice) {
     const int64_t rows = a.M - m0 < slice ? a.M - m0 : slice;
-    const hipError_t e = bx4 ? launch_cfg<128, 512, 128, 64, 128, 3, true>(a, m0, rows, stream)
-                             : launch_cfg<256, 256, 128, 64, 128, 3, false>(a, m0, rows, stream);
+    const int choice = bx4 ? gemm_tile_choice(rows, a.N, cus) : -1;
+    const hipError_t e = choice < 0  ? launch_cfg<256, 256, 128, 64, 128, 3, false>(a, m0, rows, stream)
+                         : choice == 1 ? launch_cfg<64, 512, 64, 64, 128, 3, true>(a, m0, rows, stream)
+                         : choice == 2 ? launch_cfg<64, 256, 32, 64, 128, 3, true>(a, m0, rows, stream)
+                                       : launch_cfg<128, 512, 128, 64, 128, 3, true>(a, m0, rows, stream);
     if (e != hipSuccess) return e;
   }
   return hipSuccess;

@@ -43,22 +43,25 @@ FwdScratch fwd_scratch(int64_t M, int64_t K) {
   return s;
 }
 
-// Automatic choice: up to kDecodeSliceMaxTokens tokens run as decode launches
+// Automatic choice: up to decode_max_tokens(K) tokens run as decode launches
 // of at most 16 tokens each, when the decode kernel takes such a slice (its
-// LDS holds q of 16 tokens up to K = 7680).  Measured at K = 2048, N = 6144:
-// the MFMA kernel takes >= 26 us at any small M (each output tile's k loop
-// runs on one CU, and 64 tokens fill few tiles), the decode launches 3.5 us
-// for one token, 6.2 us for 16, so M = 32: 12.4 us against 27.3; M = 40:
-// 17.3 against 27.3; M = 64: ~25 against 28.9.  MMF_PATH_GEMV forces the
-// decode kernels for every M (slices they cannot hold then go to the gemv
-// kernel, which reads q from global memory); MMF_PATH_GEMM forces the MFMA
-// kernel.
-constexpr int64_t kDecodeSliceMaxTokens = 64;
+// LDS holds q of 16 tokens up to K = 7680); more go to the MFMA kernel, whose
+// time at a small M is one tile's k loop (latency-bound, ~0.6-0.9 us per 128
+// of K).  Measured forward calls from x, decode slices at 16 / 32 / 48 / 64
+// tokens against the MFMA kernel at 16-128 tokens: K = 1024, N = 4096: 5.0 /
+// 9.5 / 13.9 / 18.1 us against 10.2-11.8; K = 2048, N = 6144: 6.7 / 12.7 /
+// 18.6 / 24.5 against 15.2-17.2; K = 4096, N = 11008: 9.2 / 14.1 / 18.8 /
+// 23.6 against 24.0-26.4; K = 5120, N = 15360: 11.5 / 16.7 / 21.6 / 26.8
+// against 35.2-37.3.  So 32 tokens at K <= 2048, 64 beyond.  MMF_PATH_GEMV
+// forces the decode kernels for every M (slices they cannot hold then go to
+// the gemv kernel, which reads q from global memory); MMF_PATH_GEMM forces
+// the MFMA kernel.
+int64_t decode_max_tokens(int64_t K) { return K <= 2048 ? 32 : 64; }
 bool use_decode(int64_t M, int64_t K, int64_t N, bool from_x, bool x_is_f32) {
   const int p = g_path.load(std::memory_order_relaxed);
   if (p == MMF_PATH_GEMV) return true;
   if (p == MMF_PATH_GEMM) return false;
-  if (M > kDecodeSliceMaxTokens) return false;
+  if (M > decode_max_tokens(K)) return false;
   return mmf::decode_fits(M < kDecodeMaxTokens ? M : kDecodeMaxTokens, static_cast<int>(K), N, from_x,
                           x_is_f32);
 }
@@ -361,19 +364,6 @@ TrainScratch train_scratch(int64_t M, int64_t K, int64_t N) {
   return s;
 }
 
-// Compute units of the current device (the dW kernel's work plan).
-int device_cus() {
-  static std::mutex mu;
-  static int cus[64] = {};
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-  std::lock_guard<std::mutex> lock(mu);
-  if (cus[dev] == 0) {
-    int v = 0;
-    cus[dev] = (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && v > 0) ? v : 256;
-  }
-  return cus[dev];
-}
 
 struct BwdScratch {
   int64_t Np;
@@ -383,7 +373,7 @@ struct BwdScratch {
 BwdScratch bwd_scratch(int64_t M, int64_t K, int64_t N) {
   BwdScratch s;
   s.Np = (N + 7) / 8 * 8;
-  s.plan = mmf::bwd_dw_plan(M, N, K, s.Np, device_cus());
+  s.plan = mmf::bwd_dw_plan(M, N, K, s.Np, mmf::device_cus());
   s.wn_off = 0;
   s.dop_off = round_up(static_cast<size_t>(mmf::bwd_nmajor_words(N, K)) * 4, kScratchAlign);
   const size_t dop = s.Np != N ? static_cast<size_t>(M) * static_cast<size_t>(s.Np) * 2 : 0;
@@ -446,6 +436,21 @@ char* device_scratch(int* status) {
 }
 
 }  // namespace
+
+// Compute units of the current device, cached per device (the work plans of
+// the dW kernel and the tile choice of the MFMA contraction).
+int mmf::device_cus() {
+  static std::mutex mu;
+  static int cus[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  std::lock_guard<std::mutex> lock(mu);
+  if (cus[dev] == 0) {
+    int v = 0;
+    cus[dev] = (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && v > 0) ? v : 256;
+  }
+  return cus[dev];
+}
 
 extern "C" {
 

@@ -92,8 +92,15 @@ struct DecodeArgs {
 };
 bool decode_fits(int64_t mt, int K, int64_t N, bool from_x, bool x_is_f32);
 hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream);
-// Prefill kernel: int8 MFMA, any M.
+// Compute units of the current device (cached per device).
+int device_cus();
+// Prefill kernel: int8 MFMA, any M.  The workgroup tile is 128 x 512, or
+// 64 x 512 / 64 x 256 when those finish a problem with few 128 x 512 tiles
+// sooner (gemm_tile_choice); 256 x 256 when N % 4 != 0.
 hipError_t launch_gemm(const ContractArgs& a, hipStream_t stream);
+// Index of the tile shape launch_gemm uses for `rows` x N on `cus` compute
+// units (N % 4 == 0): 0 for 128 x 512, 1 for 64 x 512, 2 for 64 x 256.
+int gemm_tile_choice(int64_t rows, int64_t N, int cus);
 // Rows per launch of the MFMA kernel for K in-features and N out-features,
 // or 0 when the shape is beyond its 32-bit buffer offsets: the packed weights
 // must stay below 2^31 bytes, N at most 2^24, and a launch covers a slice of

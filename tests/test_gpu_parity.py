@@ -178,31 +178,52 @@ SWEEP_K = [16, 48, 64, 256, 2064]
 SWEEP_N = [1, 16, 64, 257, 1024]
 
 
+def check_shape(mmf, rs, M, K, N, paths, tag="sweep"):
+    """One random case: weights and act-quant against the oracle, then the
+    exact int32 sums and the forward through each of `paths`."""
+    bits, xf, g, W = workloads.random_case(rs, M, K, N)
+    case = Case(bits, xf, g, W, f"M{M}K{K}N{N}")
+    case.oracle_weights()
+    case.oracle_act()
+    acc_ref = oracle.ternary_accumulate(case.q_ref, case.t)
+    y_ref = oracle.dequant(acc_ref, case.a_ref, case.ws_ref)
+    case.upload()
+    log(f"[{tag}] M={M} K={K} N={N}")
+    Wp, ws = gpu_weights(mmf, case)
+    check_weights(case, Wp, ws)
+    q, a, r = gpu_act(mmf, case)
+    qn, flip_rows, _ = check_act(case, q, a, r)
+    flip = np.zeros(M, bool)
+    flip[flip_rows] = True
+    q_ref_d = torch.from_numpy(case.q_ref).to(dev())
+    for path in paths:
+        acc = run_i32(mmf, q_ref_d, Wp, M, N, path).cpu().numpy()
+        assert np.array_equal(acc, acc_ref), (path, M, K, N)
+        y = run_forward(mmf, case, Wp, ws, path).cpu().numpy()
+        assert not np.isnan(y).any(), ("forward left outputs unwritten", path, M, K, N)
+        compare_y(y, y_ref, acc_ref, flip)
+
+
 @pytest.mark.parametrize("M", SWEEP_M)
 def test_random_shapes(mmf, M):
     rs = np.random.default_rng(1000 + M)
     for K in SWEEP_K:
         for N in SWEEP_N:
-            bits, xf, g, W = workloads.random_case(rs, M, K, N)
-            case = Case(bits, xf, g, W, f"M{M}K{K}N{N}")
-            case.oracle_weights()
-            case.oracle_act()
-            acc_ref = oracle.ternary_accumulate(case.q_ref, case.t)
-            y_ref = oracle.dequant(acc_ref, case.a_ref, case.ws_ref)
-            case.upload()
-            log(f"[sweep] M={M} K={K} N={N}")
-            Wp, ws = gpu_weights(mmf, case)
-            check_weights(case, Wp, ws)
-            q, a, r = gpu_act(mmf, case)
-            qn, flip_rows, _ = check_act(case, q, a, r)
-            flip = np.zeros(M, bool)
-            flip[flip_rows] = True
-            q_ref_d = torch.from_numpy(case.q_ref).to(dev())
-            for path in PATHS:
-                acc = run_i32(mmf, q_ref_d, Wp, M, N, path).cpu().numpy()
-                assert np.array_equal(acc, acc_ref), (path, M, K, N)
-                y = run_forward(mmf, case, Wp, ws, path).cpu().numpy()
-                compare_y(y, y_ref, acc_ref, flip)
+            check_shape(mmf, rs, M, K, N, PATHS)
+
+
+# The MFMA kernel's tile shape follows the problem (on 256 compute units):
+# 64 x 256 tiles for a short M or a narrow N, 64 x 512 in between, 128 x 512
+# once the wide tiles fill the CUs (the full-size workloads above).  Ragged
+# in every dimension (a partial last stage of K, partial row and column
+# tiles).  The automatic path sends 33-64 tokens to the MFMA kernel at
+# K <= 2048 and to decode launches of 16 tokens beyond.
+@pytest.mark.parametrize("M,K,N", [(300, 1040, 2000),    # 64 x 256: 40 tiles
+                                   (1000, 336, 6000),    # 64 x 512: 192 tiles
+                                   (40, 2048, 1000),     # auto: MFMA kernel (64 x 256)
+                                   (57, 2064, 1000)])    # auto: four decode launches
+def test_gemm_tile_shapes(mmf, M, K, N):
+    check_shape(mmf, np.random.default_rng(1100 + M + K), M, K, N, PATHS + ("auto",), tag="tiles")
 
 
 # ---------------------------------------------------------------------------
