@@ -134,6 +134,8 @@ static_assert(kAInstr % kWaves == 0 && kBInstr % kWaves == 0, "loads must split 
 static_assert(kLoadsPerStage <= FM, "one stage load per fragment group");
 static_assert(FN == 4 && FM >= 2 * FN, "expansion schedule: four words, one per late fragment");
 static_assert(S * kStageBytes >= kWaves * 4 * BM * 8, "row-sum reduction reuses the ring");
+constexpr int kDbRedBytes = kWaves * kWave * 8;        // per-wave fp64 scratch of the db column sums
+static_assert(BK == 128 && kWaves == 8 && BM == 128, "db duty: wave w sums chunk w of every row");
 }  // namespace dyk
 
 // Expanded code fragment of one lane: 8 bf16 values t / 2 (see the file head).
@@ -172,15 +174,23 @@ template <> struct X4<float> {
 
 // dO [M][Np] bf16 (Np % 8 == 0, zero columns past N), Wn [ceil(Np/16)][K].
 // rg [M][K] (the dx buffer), s_part [ceil(K/BN)][ld_s] (row m at column m),
-// dg_part [ceil(M/BM)][K] or null.
+// dg_part [ceil(M/BM)][K] or null, db_part [ceil(M/BM)][N] or null.
+//
+// db duty: the column tiles of a row tile read the same dO rows, so each
+// 64-column stage of dO is summed over the row tile's 128 rows by one of them
+// (stage kt by column tile kt % ntn) while the stage is in LDS: wave w sums
+// the 8 columns of chunk w, lane (row group g8 = lane / 8, column lane % 8)
+// the 16 rows g8 + 8 i in fp64 (bf16 values are exact in fp64), then the 8
+// row groups are added in order through the wave's own LDS scratch and the
+// sum goes to db_part[tm][n].
 template <typename XT>
 __global__ __launch_bounds__(dyk::kThreads) void dy_kernel(
     const uint16_t* __restrict__ dO, const uint32_t* __restrict__ Wn, const float* __restrict__ w_scale,
     const XT* __restrict__ x, const float* __restrict__ gamma, const float* __restrict__ rstd,
-    float* __restrict__ rg, double* __restrict__ s_part, int64_t ld_s, double* __restrict__ dg_part, int M,
-    int Np, int K) {
+    float* __restrict__ rg, double* __restrict__ s_part, int64_t ld_s, double* __restrict__ dg_part,
+    double* __restrict__ db_part, int M, int N, int Np, int K) {
   using namespace dyk;
-  __shared__ __attribute__((aligned(16))) char smem[S * kStageBytes];
+  __shared__ __attribute__((aligned(16))) char smem[S * kStageBytes + kDbRedBytes];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wn = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -263,9 +273,34 @@ __global__ __launch_bounds__(dyk::kThreads) void dy_kernel(
 #pragma unroll
   for (int f = 0; f < FN; ++f) be[0][f] = expand_bf16_half(bw[f], rot);
 
+  // db duty of stage kt (see above); its slot stays intact until the barrier
+  // of stage kt + 1's last step, and every read here is consumed before it
+  const int ntn = (K + BN - 1) / BN;
+  double* db_red = reinterpret_cast<double*>(smem + S * kStageBytes) + wn * kWave;
+  auto db_stage = [&](int kt) {
+    const char* st = smem + (kt % S) * kStageBytes;
+    const int dc = lane & 7, g8 = lane >> 3;
+    double sum = 0.0;
+#pragma unroll
+    for (int i = 0; i < BM / 8; ++i) {
+      const int r = g8 + 8 * i;
+      const uint32_t v = *reinterpret_cast<const uint16_t*>(st + r * BK + ((wn ^ a_swz(r)) << 4) + 2 * dc);
+      sum += static_cast<double>(__uint_as_float(v << 16));
+    }
+    db_red[lane] = sum;
+    if (lane < 8) {
+      double t = 0.0;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) t += db_red[8 * j + lane];
+      const int n = kt * (BK / 2) + wn * 8 + lane;
+      if (n < N) db_part[tm * N + n] = t;
+    }
+  };
+
   // one 32-value step s: its MFMAs, the fragment reads of step s + 1 and
   // the expansion of its words; the last step of a stage waits for the next
-  // stage's loads and passes a barrier, then refills the retired slot
+  // stage's loads and passes a barrier, then refills the retired slot (and,
+  // on its db duty, sums the stage's columns)
   auto step = [&](int s, v4i (&bc)[FN], v4i (&bn)[FN]) {
     const int kt = s / KS, ks = s % KS;
     const bool refill = (ks == KS - 1);
@@ -286,6 +321,7 @@ __global__ __launch_bounds__(dyk::kThreads) void dy_kernel(
       if (fm >= FM - FN) bn[fm - (FM - FN)] = expand_bf16_half(bw[fm - (FM - FN)], rot);
       __builtin_amdgcn_sched_barrier(0);
     }
+    if (refill && db_part != nullptr && kt % ntn == tn) db_stage(kt);
   };
   const int steps = KT * KS;
   int s = 0;
@@ -782,23 +818,24 @@ int64_t bwd_dy_row_slice(int64_t Np, int64_t K) {
   return rows;
 }
 
-hipError_t launch_dy(const uint16_t* dO, int64_t M, int64_t Np, const uint32_t* Wn, const float* w_scale,
-                     const void* x, bool x_is_f32, const float* gamma, const float* rstd, int K, float* rg,
-                     double* s_part, double* dg_part, hipStream_t stream) {
+hipError_t launch_dy(const uint16_t* dO, int64_t M, int64_t N, int64_t Np, const uint32_t* Wn,
+                     const float* w_scale, const void* x, bool x_is_f32, const float* gamma, const float* rstd,
+                     int K, float* rg, double* s_part, double* dg_part, double* db_part, hipStream_t stream) {
   const int64_t slice = bwd_dy_row_slice(Np, K);
   if (slice == 0) return hipErrorInvalidValue;
   for (int64_t mb = 0; mb < M; mb += slice) {
     const int64_t rows = M - mb < slice ? M - mb : slice;
     const dim3 grid(static_cast<unsigned>(bwd_dy_row_tiles(rows) * bwd_dy_col_tiles(K)));
     double* dgp = dg_part ? dg_part + (mb / dyk::BM) * K : nullptr;
+    double* dbp = db_part ? db_part + (mb / dyk::BM) * N : nullptr;
     if (x_is_f32)
       hipLaunchKernelGGL(dy_kernel<float>, grid, dim3(dyk::kThreads), 0, stream, dO + mb * Np, Wn, w_scale,
                          static_cast<const float*>(x) + mb * K, gamma, rstd + mb, rg + mb * K, s_part + mb, M,
-                         dgp, static_cast<int>(rows), static_cast<int>(Np), K);
+                         dgp, dbp, static_cast<int>(rows), static_cast<int>(N), static_cast<int>(Np), K);
     else
       hipLaunchKernelGGL(dy_kernel<uint16_t>, grid, dim3(dyk::kThreads), 0, stream, dO + mb * Np, Wn, w_scale,
                          static_cast<const uint16_t*>(x) + mb * K, gamma, rstd + mb, rg + mb * K, s_part + mb, M,
-                         dgp, static_cast<int>(rows), static_cast<int>(Np), K);
+                         dgp, dbp, static_cast<int>(rows), static_cast<int>(N), static_cast<int>(Np), K);
   }
   return hipGetLastError();
 }
@@ -820,6 +857,10 @@ hipError_t launch_dx_finish(float* dx, const void* x, bool x_is_f32, const float
 
 hipError_t launch_dgamma_finish(const double* dg_part, int64_t M, int K, float* dgamma, hipStream_t stream) {
   return launch_col_final(dg_part, bwd_dy_row_tiles(M), K, dgamma, stream);
+}
+
+hipError_t launch_db_finish(const double* db_part, int64_t M, int64_t N, float* db, hipStream_t stream) {
+  return launch_col_final(db_part, bwd_dy_row_tiles(M), N, db, stream);
 }
 
 DwPlan bwd_dw_plan(int64_t M, int64_t N, int64_t K, int64_t Np, int cus) {

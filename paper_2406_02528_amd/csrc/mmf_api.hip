@@ -368,7 +368,7 @@ TrainScratch train_scratch(int64_t M, int64_t K, int64_t N) {
 struct BwdScratch {
   int64_t Np;
   mmf::DwPlan plan;
-  size_t wn_off, dop_off, spart_off, dgpart_off, colpart_off, dw_off, parts_off, total;
+  size_t wn_off, dop_off, spart_off, dgpart_off, dbpart_off, dw_off, parts_off, total;
 };
 BwdScratch bwd_scratch(int64_t M, int64_t K, int64_t N) {
   BwdScratch s;
@@ -380,9 +380,9 @@ BwdScratch bwd_scratch(int64_t M, int64_t K, int64_t N) {
   s.spart_off = s.dop_off + round_up(dop, kScratchAlign);
   s.dgpart_off = s.spart_off + round_up(sizeof(double) * static_cast<size_t>(mmf::bwd_dy_col_tiles(K) * M),
                                         kScratchAlign);
-  s.colpart_off = s.dgpart_off + round_up(sizeof(double) * static_cast<size_t>(mmf::bwd_dy_row_tiles(M) * K),
+  s.dbpart_off = s.dgpart_off + round_up(sizeof(double) * static_cast<size_t>(mmf::bwd_dy_row_tiles(M) * K),
                                           kScratchAlign);
-  s.dw_off = s.colpart_off + round_up(sizeof(double) * static_cast<size_t>(mmf::col_sum_partials(M) * N),
+  s.dw_off = s.dbpart_off + round_up(sizeof(double) * static_cast<size_t>(mmf::bwd_dy_row_tiles(M) * N),
                                       kScratchAlign);
   const int64_t S = s.plan.split_all;
   s.parts_off = s.dw_off + (S > 1 ? round_up(sizeof(float) * static_cast<size_t>(S * N * K), kScratchAlign) : 0);
@@ -860,8 +860,9 @@ int mmf_bitlinear_bwd(const uint16_t* dO, const void* x, int x_is_f32, const flo
     // dY = dO Wt^T with r gamma dY into dx and the row / column partials,
     // then dx and dgamma finished
     if (mmf::launch_pack_nmajor(Wpacked, N, s.Np, Ki, Wn, stream) != hipSuccess) return MMF_ERR_HIP;
-    if (mmf::launch_dy(dOp, M, s.Np, Wn, w_scale, x, f32, gamma, rstd, Ki, dx, s_part, dg_part, stream) !=
-        hipSuccess)
+    double* db_part = db ? reinterpret_cast<double*>(scratch + s.dbpart_off) : nullptr;
+    if (mmf::launch_dy(dOp, M, N, s.Np, Wn, w_scale, x, f32, gamma, rstd, Ki, dx, s_part, dg_part, db_part,
+                       stream) != hipSuccess)
       return MMF_ERR_HIP;
     if (mmf::launch_dx_finish(dx, x, f32, rstd, s_part, M, Ki, stream) != hipSuccess) return MMF_ERR_HIP;
     if (dgamma && mmf::launch_dgamma_finish(dg_part, M, Ki, dgamma, stream) != hipSuccess) return MMF_ERR_HIP;
@@ -873,9 +874,7 @@ int mmf_bitlinear_bwd(const uint16_t* dO, const void* x, int x_is_f32, const flo
     if (mmf::launch_dw(dOp, q, a_scale, M, s.Np, N, Ki, dw_out, parts, s.plan, stream) != hipSuccess)
       return MMF_ERR_HIP;
     if (S > 1 && mmf::launch_sum_parts(dw_out, S, N * K, dW, stream) != hipSuccess) return MMF_ERR_HIP;
-    if (db && mmf::launch_col_sum_bf16(dO, M, N, reinterpret_cast<double*>(scratch + s.colpart_off), db,
-                                       stream) != hipSuccess)
-      return MMF_ERR_HIP;
+    if (db && mmf::launch_db_finish(db_part, M, N, db, stream) != hipSuccess) return MMF_ERR_HIP;
     return MMF_OK;
   });
 }

@@ -128,12 +128,7 @@ int64_t mlgru_scan_ws_floats(int64_t B, int64_t T, int64_t d);
 hipError_t launch_mlgru_scan(const float* fcg, const float* h0, float* o, float* h_last, int64_t B,
                              int64_t T, int64_t d, float* ws, hipStream_t stream);
 
-// ---- backward (bwd.hip: column sums; bwd_gemm.hip: the two products) ----
-// Column sums over M rows, in fp64, in a fixed order: db[n] = sum_m dO[m][n]
-// (dO bf16 [M][N]).  `partials` holds col_sum_partials(M) * N doubles.
-int64_t col_sum_partials(int64_t M);
-hipError_t launch_col_sum_bf16(const uint16_t* dO, int64_t M, int64_t N, double* partials, float* db,
-                               hipStream_t stream);
+// ---- backward (bwd.hip: final sums; bwd_gemm.hip: the two products) ----
 // out[c] = sum over p < nparts of partials[p * cols + c] (fp64, fixed order).
 hipError_t launch_col_final(const double* partials, int64_t nparts, int64_t cols, float* out, hipStream_t stream);
 // out[i] = sum over s < S of parts[s * n + i], in order, in fp64.
@@ -149,18 +144,21 @@ hipError_t launch_pad_rows(const uint16_t* src, int64_t M, int64_t N, int64_t N8
                            hipStream_t stream);
 // dY kernel: dO [M][Np] bf16 (Np % 8 == 0) against Wn; writes rg = r gamma dY
 // into rg [M][K], s_part [bwd_dy_col_tiles(K)][M] and (if not null) dg_part
-// [bwd_dy_row_tiles(M)][K].  bwd_dy_row_slice(Np, K) == 0: shape not
+// [bwd_dy_row_tiles(M)][K] and db_part [bwd_dy_row_tiles(M)][N] (the column
+// sums of dO per row tile, for db).  bwd_dy_row_slice(Np, K) == 0: shape not
 // supported (32-bit offsets).
 int64_t bwd_dy_col_tiles(int64_t K);
 int64_t bwd_dy_row_tiles(int64_t M);
 int64_t bwd_dy_row_slice(int64_t Np, int64_t K);
-hipError_t launch_dy(const uint16_t* dO, int64_t M, int64_t Np, const uint32_t* Wn, const float* w_scale,
-                     const void* x, bool x_is_f32, const float* gamma, const float* rstd, int K, float* rg,
-                     double* s_part, double* dg_part, hipStream_t stream);
+hipError_t launch_dy(const uint16_t* dO, int64_t M, int64_t N, int64_t Np, const uint32_t* Wn,
+                     const float* w_scale, const void* x, bool x_is_f32, const float* gamma, const float* rstd,
+                     int K, float* rg, double* s_part, double* dg_part, double* db_part, hipStream_t stream);
 // dx = rg - (r^3 s / K) x in place; dgamma from the row-tile partials.
 hipError_t launch_dx_finish(float* dx, const void* x, bool x_is_f32, const float* rstd, const double* s_part,
                             int64_t M, int K, hipStream_t stream);
 hipError_t launch_dgamma_finish(const double* dg_part, int64_t M, int K, float* dgamma, hipStream_t stream);
+// db[n] = sum over the row tiles of db_part (fp64, tile order).
+hipError_t launch_db_finish(const double* db_part, int64_t M, int64_t N, float* db, hipStream_t stream);
 // Work units of the dW kernel.  split_all > 1: every tile's token range is
 // split into split_all parts, written to out [split_all][N][K] and added by
 // launch_sum_parts.  Otherwise tiles [0, full) are whole units and the

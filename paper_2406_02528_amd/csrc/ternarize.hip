@@ -33,16 +33,33 @@ __global__ __launch_bounds__(kSumThreads) void sum_abs_kernel(
   __shared__ double red[kSumThreads];
   const int64_t begin = static_cast<int64_t>(blockIdx.x) * chunk;
   const int64_t end = min(begin + chunk, count);
-  double acc = 0.0;
-  // count and chunk are multiples of 4, W is 16-byte aligned
-  for (int64_t i = begin + 4 * threadIdx.x; i < end; i += 4 * kSumThreads) {
-    const float4 v = *reinterpret_cast<const float4*>(W + i);
-    acc += static_cast<double>(fabsf(v.x));
-    acc += static_cast<double>(fabsf(v.y));
-    acc += static_cast<double>(fabsf(v.z));
-    acc += static_cast<double>(fabsf(v.w));
+  // count and chunk are multiples of 4, W is 16-byte aligned.  Four loads
+  // per thread go out together and feed four independent fp64 sums (one
+  // chain of dependent adds per load would hold each thread to one load in
+  // flight).
+  constexpr int64_t kStride = 4 * kSumThreads;
+  double acc[4] = {0.0, 0.0, 0.0, 0.0};
+  int64_t i = begin + 4 * threadIdx.x;
+  for (; i + 3 * kStride < end; i += 4 * kStride) {
+    float4 v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) v[u] = *reinterpret_cast<const float4*>(W + i + u * kStride);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      acc[u] += static_cast<double>(fabsf(v[u].x));
+      acc[u] += static_cast<double>(fabsf(v[u].y));
+      acc[u] += static_cast<double>(fabsf(v[u].z));
+      acc[u] += static_cast<double>(fabsf(v[u].w));
+    }
   }
-  const double total = block_sum_f64(acc, red);
+  for (; i < end; i += kStride) {
+    const float4 v = *reinterpret_cast<const float4*>(W + i);
+    acc[0] += static_cast<double>(fabsf(v.x));
+    acc[0] += static_cast<double>(fabsf(v.y));
+    acc[0] += static_cast<double>(fabsf(v.z));
+    acc[0] += static_cast<double>(fabsf(v.w));
+  }
+  const double total = block_sum_f64((acc[0] + acc[1]) + (acc[2] + acc[3]), red);
   if (threadIdx.x == 0) partials[blockIdx.x] = total;
 }
 
