@@ -463,7 +463,8 @@ def test_decode_up_to_16_tokens_per_launch(mmf, M, K, N, f32):
     9, 15 and 16 tokens fused from x; 12 x 4096 and 16 x 7680, whose rows
     need more registers than the fused kernel holds, from act-quant's q
     copied into LDS (16 x 7680 is the largest q region); 33 and 40 tokens as
-    launches of 16, 16 and the rest."""
+    launches of 16, 16 and the rest on the forced decode path (the automatic
+    path sends more than 32 tokens at K <= 2048 to the MFMA kernel)."""
     rs = np.random.default_rng(M * 17 + K + N)
     bits, xf, g, W = workloads.random_case(rs, M, K, N)
     x_form = xf if f32 else bits
