@@ -158,8 +158,8 @@ __global__ __launch_bounds__((Tiling<BM, BN, WM, WN, BK, S, BX4>::kThreads)) voi
   // them itself with explicit vmcnt waits before its barriers.  Offsets at or
   // past the end of a buffer (rows past M, chunks past K, word rows past
   // K/16, stages past the last) read zero without touching memory.
-  auto issue_one = [&](int kt, int i) {
-    const uint32_t base = lds0 + static_cast<uint32_t>((kt % S) * T::kStageBytes);
+  auto issue_one = [&](int kt, int slot, int i) {
+    const uint32_t base = lds0 + static_cast<uint32_t>(slot * T::kStageBytes);
     const int k0 = kt * BK;
     if (i < T::kAPerWave) {
       const uint32_t off = (k0 + a_chunk[i] < K) ? a_src[i] + static_cast<uint32_t>(k0) : 0x80000000u;
@@ -198,16 +198,14 @@ __global__ __launch_bounds__((Tiling<BM, BN, WM, WN, BK, S, BX4>::kThreads)) voi
   v4i af[FM];
   uint32_t bw[FN];
   v4i be[2][FN];
-  auto a_read = [&](int s, int fm) -> v4i {
-    const int kt = s / KS, ks = s % KS;
-    const char* st = smem + (kt % S) * T::kStageBytes;
+  auto a_read = [&](int slot, int ks, int fm) -> v4i {
+    const char* st = smem + slot * T::kStageBytes;
     const int row = wm * WM + fm * 16 + l16;
     const int c = (ks * 4 + g) ^ a_swz(row);
     return *reinterpret_cast<const v4i*>(st + row * BK + c * 16);
   };
-  auto b_read = [&](int s, int f) -> uint32_t {
-    const int kt = s / KS, ks = s % KS;
-    const uint32_t* Bs = reinterpret_cast<const uint32_t*>(smem + (kt % S) * T::kStageBytes + T::kABytes);
+  auto b_read = [&](int slot, int ks, int f) -> uint32_t {
+    const uint32_t* Bs = reinterpret_cast<const uint32_t*>(smem + slot * T::kStageBytes + T::kABytes);
     return Bs[(ks * 4 + g) * T::kBRow + wn * WN + f * 16 + l16];
   };
   constexpr auto exp_lo = [](int fm) constexpr -> int {
@@ -247,41 +245,42 @@ __global__ __launch_bounds__((Tiling<BM, BN, WM, WN, BK, S, BX4>::kThreads)) voi
 #pragma unroll
   for (int p = 0; p < S - 1; ++p)
 #pragma unroll
-    for (int i = 0; i < T::kLoadsPerStage; ++i) issue_one(p, i);
+    for (int i = 0; i < T::kLoadsPerStage; ++i) issue_one(p, p, i);
   __builtin_amdgcn_s_waitcnt(MMF_WAIT_VM((S - 2) * T::kLoadsPerStage));
   __builtin_amdgcn_s_barrier();
 #pragma unroll
-  for (int fm = 0; fm < FM; ++fm) af[fm] = a_read(0, fm);
+  for (int fm = 0; fm < FM; ++fm) af[fm] = a_read(0, 0, fm);
 #pragma unroll
-  for (int f = 0; f < FN; ++f) bw[f] = b_read(0, f);
+  for (int f = 0; f < FN; ++f) bw[f] = b_read(0, 0, f);
 #pragma unroll
   for (int f = 0; f < FN; ++f) be[0][f] = expand(bw[f]);
 
-  // One k64 step s (stage kt = s / KS): the MFMAs of step s, the fragment
-  // reads of step s + 1 and the expansion of its words.  The last step of a
-  // stage reads the next stage: it first waits for its own loads of that
-  // stage (with S = 3 nothing younger is in flight) and passes a barrier,
-  // which makes every wave's loads visible and certifies that every wave has
-  // consumed the oldest slot (its data fed MFMAs of earlier steps); that
-  // slot is then refilled with stage kt + S - 1, one load per fragment group.
-  auto step = [&](int s, v4i (&bc)[FN], v4i (&bn)[FN]) {
-    const int kt = s / KS, ks = s % KS;
+  // One k64 step (ks of stage kt, in ring slot `slot`; the next stage in
+  // `slot_next`): the MFMAs of the step, the fragment reads of the next step
+  // and the expansion of its words.  The last step of a stage reads the next
+  // stage: it first waits for its own loads of that stage (with S = 3
+  // nothing younger is in flight) and passes a barrier, which makes every
+  // wave's loads visible and certifies that every wave has consumed the
+  // oldest slot (its data fed MFMAs of earlier steps); that slot is then
+  // refilled with stage kt + S - 1, one load per fragment group.
+  auto step = [&](int kt, int ks, int slot, int slot_next, v4i (&bc)[FN], v4i (&bn)[FN]) {
     const bool refill = (ks == KS - 1);
+    const int rslot = refill ? slot_next : slot, rks = refill ? 0 : ks + 1;
     __builtin_amdgcn_sched_barrier(0);
     if (refill) {
       __builtin_amdgcn_s_waitcnt(MMF_WAIT_VM((S - 3) * T::kLoadsPerStage));
       __builtin_amdgcn_s_barrier();
     }
 #pragma unroll
-    for (int f = 0; f < FN; ++f) bw[f] = b_read(s + 1, f);
+    for (int f = 0; f < FN; ++f) bw[f] = b_read(rslot, rks, f);
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int fm = 0; fm < FM; ++fm) {
 #pragma unroll
       for (int f = 0; f < FN; ++f)
         acc[fm][f] = __builtin_amdgcn_mfma_i32_16x16x64_i8(bc[f], af[fm], acc[fm][f], 0, 0, 0);
-      af[fm] = a_read(s + 1, fm);
-      if (refill && fm < T::kLoadsPerStage) issue_one(kt + S - 1, fm);
+      af[fm] = a_read(rslot, rks, fm);
+      if (refill && fm < T::kLoadsPerStage) issue_one(kt + S - 1, (slot + S - 1) % S, fm);
       // the next step's words, expanded behind this step's groups: one in
       // each of the last FN groups when there are at least 2 FN groups, else
       // spread over groups 1 .. FM - 1 (group 0 leaves their LDS reads time)
@@ -290,13 +289,24 @@ __global__ __launch_bounds__((Tiling<BM, BN, WM, WN, BK, S, BX4>::kThreads)) voi
       __builtin_amdgcn_sched_barrier(0);
     }
   };
-  const int steps = KT * KS;
-  int s = 0;
-  for (; s + 1 < steps; s += 2) {
-    step(s, be[0], be[1]);
-    step(s + 1, be[1], be[0]);
+  // Whole periods of the ring (S stages) with every slot a compile-time
+  // constant, so that LDS addresses are base + immediate and the loop's
+  // back-edge, where the compiler's count of LDS reads in flight starts
+  // over, comes once per S stages; then the remaining stages.  KS is even,
+  // so a step's parity (which expanded-word buffer it reads) is ks's.
+  static_assert(KS % 2 == 0, "step parity");
+  int kt = 0;
+  for (; kt + S <= KT; kt += S) {
+#pragma unroll
+    for (int j = 0; j < S; ++j)
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) step(kt + j, ks, j, (j + 1) % S, be[ks % 2], be[(ks + 1) % 2]);
   }
-  if (s < steps) step(s, be[0], be[1]);
+  for (; kt < KT; ++kt) {
+    const int slot = kt % S;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) step(kt, ks, slot, (slot + 1) % S, be[ks % 2], be[(ks + 1) % 2]);
+  }
   // no LDS-DMA write may still be in flight when the workgroup's LDS is freed
   __builtin_amdgcn_s_waitcnt(MMF_WAIT_VM_LGKM0(0));
 
