@@ -318,44 +318,6 @@ __global__ __launch_bounds__((Tiling<BM, BN, WM, WN, BK, S, BX4>::kThreads)) voi
   const float ws_u = (EP == Epilogue::kGluF32) ? w_scale[1] : 0.0f;
   __syncthreads();
   constexpr uint32_t kOut = kOutOfRange;
-  if constexpr (EP == Epilogue::kGluF32) {
-    // Blocks f = 2i (gate) and 2i + 1 (up) of a wave hold the same 16
-    // channels: lane (g, l16) has channels 4 g .. 4 g + 3 of both, so the
-    // gate p = SiLU(g) * u is formed in registers and stored 16 bytes at a
-    // time into the L = N / 2 wide output.
-    static_assert(BX4 && FN % 2 == 0, "GLU output needs whole 16-column block pairs");
-    const int L = N / 2;
-    const uint32_t out_bytes = static_cast<uint32_t>(M) * static_cast<uint32_t>(L) * 4u;
-    const __amdgpu_buffer_rsrc_t orsrc =
-        __builtin_amdgcn_make_buffer_rsrc(out, 0, static_cast<int>(out_bytes), kBufferFlags);
-#pragma unroll
-    for (int fm = 0; fm < FM; ++fm) {
-      const int lr = wm * WM + fm * 16 + l16;
-      const bool row_ok = m0 + lr < M;
-      const int rs = s_rsum[lr];
-      const float sg = s_scale[lr] * ws, su = s_scale[lr] * ws_u;
-      const uint32_t row_bytes = static_cast<uint32_t>(m0 + lr) * static_cast<uint32_t>(L) * 4u;
-#pragma unroll
-      for (int pi = 0; pi < FN / 2; ++pi) {
-        const int ch = (n0 + wn * WN) / 2 + pi * 16 + 4 * g;
-        v4i v;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const float gv = static_cast<float>(acc[fm][2 * pi][r] - rs) * sg;
-          const float uv = static_cast<float>(acc[fm][2 * pi + 1][r] - rs) * su;
-          v[r] = __float_as_int(gv * sigmoid_hw(gv) * uv);
-        }
-        const uint32_t off = (row_ok && ch < L) ? row_bytes + 4u * static_cast<uint32_t>(ch) : kOut;
-        __builtin_amdgcn_raw_buffer_store_b128(v, orsrc, off, 0, 0);
-      }
-    }
-    return;
-  }
-  // Range-checked buffer stores: rows past M fall outside the output's
-  // range, columns past N are sent there explicitly; no branches.
-  const uint32_t out_bytes = static_cast<uint32_t>(M) * static_cast<uint32_t>(N) * 4u;
-  const __amdgpu_buffer_rsrc_t orsrc =
-      __builtin_amdgcn_make_buffer_rsrc(out, 0, static_cast<int>(out_bytes), kBufferFlags);
   // affine epilogue: bias, lower bound, scale and activation of the lane's
   // four columns in each 16-column block (N % 16 == 0, one segment per block)
   ColAffine4 cf[FN];
@@ -367,17 +329,23 @@ __global__ __launch_bounds__((Tiling<BM, BN, WM, WN, BK, S, BX4>::kThreads)) voi
       cf[f] = load_col_affine4(aff, w_scale, static_cast<uint32_t>(N), n < N ? static_cast<uint32_t>(n) : 0u);
     }
   }
-#pragma unroll
-  for (int fm = 0; fm < FM; ++fm) {
+  // The lane's four outputs of block (fm, f) (for the GLU, f is the gate/up
+  // pair index: blocks 2f and 2f + 1 hold the same 16 channels, and lane
+  // (g, l16) has channels 4 g .. 4 g + 3 of both).
+  auto outputs = [&](int fm, int f) -> v4i {
     const int lr = wm * WM + fm * 16 + l16;
-    const bool row_ok = m0 + lr < M;
     const int rs = s_rsum[lr];
-    const float sc = s_scale[lr] * ws;
-    const uint32_t row_bytes = static_cast<uint32_t>(m0 + lr) * static_cast<uint32_t>(N) * 4u;
+    v4i v;
+    if constexpr (EP == Epilogue::kGluF32) {
+      const float sg = s_scale[lr] * ws, su = s_scale[lr] * ws_u;
 #pragma unroll
-    for (int f = 0; f < FN; ++f) {
-      const int n = n0 + wn * WN + f * 16 + 4 * g;
-      v4i v;
+      for (int r = 0; r < 4; ++r) {
+        const float gv = static_cast<float>(acc[fm][2 * f][r] - rs) * sg;
+        const float uv = static_cast<float>(acc[fm][2 * f + 1][r] - rs) * su;
+        v[r] = __float_as_int(gv * sigmoid_hw(gv) * uv);
+      }
+    } else {
+      const float sc = s_scale[lr] * ws;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int d = acc[fm][f][r] - rs;
@@ -388,16 +356,85 @@ __global__ __launch_bounds__((Tiling<BM, BN, WM, WN, BK, S, BX4>::kThreads)) voi
           v[r] = (EP == Epilogue::kDequantF32) ? __float_as_int(static_cast<float>(d) * sc) : d;
         }
       }
-      if constexpr (BX4) {
-        // N % 4 == 0: the four columns are all inside or all past N
-        const uint32_t off = (row_ok && n < N) ? row_bytes + 4u * static_cast<uint32_t>(n) : kOut;
-        __builtin_amdgcn_raw_buffer_store_b128(v, orsrc, off, 0, 0);
-      } else {
+    }
+    return v;
+  };
+  constexpr bool kGlu = EP == Epilogue::kGluF32;
+  // Plain outputs (dequantised or raw int32) leave through LDS as whole row
+  // segments (below); the GLU and affine epilogues, whose output rows are
+  // half as wide or whose launches are a single round, measured faster with
+  // direct 16-byte stores, and N % 4 != 0 takes per-element stores.
+  constexpr bool kStaged = BX4 && (EP == Epilogue::kDequantF32 || EP == Epilogue::kRawI32);
+  if constexpr (!kStaged) {
+    const int ow = kGlu ? N / 2 : N;  // output row length
+    const uint32_t out_bytes = static_cast<uint32_t>(M) * static_cast<uint32_t>(ow) * 4u;
+    const __amdgpu_buffer_rsrc_t orsrc =
+        __builtin_amdgcn_make_buffer_rsrc(out, 0, static_cast<int>(out_bytes), kBufferFlags);
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const uint32_t off = (row_ok && n + r < N) ? row_bytes + 4u * static_cast<uint32_t>(n + r) : kOut;
-          __builtin_amdgcn_raw_buffer_store_b32(static_cast<uint32_t>(v[r]), orsrc, off, 0, 0);
+    for (int fm = 0; fm < FM; ++fm) {
+      const int lr = wm * WM + fm * 16 + l16;
+      const bool row_ok = m0 + lr < M;
+      const uint32_t row_bytes = static_cast<uint32_t>(m0 + lr) * static_cast<uint32_t>(ow) * 4u;
+#pragma unroll
+      for (int f = 0; f < (kGlu ? FN / 2 : FN); ++f) {
+        const int n = (kGlu ? (n0 + wn * WN) / 2 : n0 + wn * WN) + f * 16 + 4 * g;
+        const v4i v = outputs(fm, f);
+        if constexpr (BX4) {
+          // N % 4 == 0 (and L % 16 == 0): the four columns are all inside or all past the row
+          const uint32_t off = (row_ok && n < ow) ? row_bytes + 4u * static_cast<uint32_t>(n) : kOut;
+          __builtin_amdgcn_raw_buffer_store_b128(v, orsrc, off, 0, 0);
+        } else {
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const uint32_t off = (row_ok && n + r < N) ? row_bytes + 4u * static_cast<uint32_t>(n + r) : kOut;
+            __builtin_amdgcn_raw_buffer_store_b32(static_cast<uint32_t>(v[r]), orsrc, off, 0, 0);
+          }
         }
+      }
+    }
+  } else {
+    // The tile leaves through LDS (the ring is free now) in chunks of 16
+    // rows, two chunk buffers in turn: the waves holding the chunk's rows
+    // write their outputs there, and after an LDS-only barrier every thread
+    // stores 16-byte pieces of whole rows, so one store instruction of a wave
+    // covers 1 KB of a row instead of 16 rows x 64 bytes.  Rows past M and
+    // columns past N fall outside the buffer's range or are sent there
+    // explicitly.
+    constexpr int OW = kGlu ? BN / 2 : BN;   // output columns of the tile
+    constexpr int OF = kGlu ? FN / 2 : FN;   // 16-column output blocks of a wave
+    constexpr int kRowB = OW * 4 + 16;       // staged row, padded by 16 bytes
+    constexpr int kChunkB = 16 * kRowB;
+    constexpr int kPieces = 16 * OW / 4;     // 16-byte pieces per chunk
+    static_assert(!kGlu || FN % 2 == 0, "GLU output needs whole 16-column block pairs");
+    static_assert(2 * kChunkB <= S * T::kStageBytes, "two staged chunks fit the ring");
+    static_assert(kPieces % T::kThreads == 0, "whole pieces per thread");
+    const int ow = kGlu ? N / 2 : N;         // output row length
+    const int c0 = kGlu ? n0 / 2 : n0;       // the tile's first output column
+    const uint32_t out_bytes = static_cast<uint32_t>(M) * static_cast<uint32_t>(ow) * 4u;
+    const __amdgpu_buffer_rsrc_t orsrc =
+        __builtin_amdgcn_make_buffer_rsrc(out, 0, static_cast<int>(out_bytes), kBufferFlags);
+#pragma unroll
+    for (int c = 0; c < BM / 16; ++c) {
+      char* buf = smem + (c & 1) * kChunkB;
+      if (wm == c / FM) {  // wave-uniform: this wave holds the chunk's rows
+#pragma unroll
+        for (int f = 0; f < OF; ++f)
+          *reinterpret_cast<v4i*>(buf + l16 * kRowB + (wn * (WN / (FN / OF)) + f * 16 + 4 * g) * 4) =
+              outputs(c % FM, f);
+      }
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+      __builtin_amdgcn_s_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+#pragma unroll
+      for (int i = 0; i < kPieces / T::kThreads; ++i) {
+        const int p = i * T::kThreads + tid;
+        const int r = p / (OW / 4), q4 = p % (OW / 4);
+        const v4i v = *reinterpret_cast<const v4i*>(buf + r * kRowB + q4 * 16);
+        const int m = m0 + c * 16 + r, n = c0 + 4 * q4;
+        const uint32_t off =
+            (m < M && n < ow) ? (static_cast<uint32_t>(m) * static_cast<uint32_t>(ow) + static_cast<uint32_t>(n)) * 4u
+                              : kOut;
+        __builtin_amdgcn_raw_buffer_store_b128(v, orsrc, off, 0, 0);
       }
     }
   }
