@@ -244,11 +244,28 @@ def calib_copy(torch):
 # ---------------------------------------------------------------------------
 
 class Timer:
+    """HIP-event timing of `steps` calls after `warmup` untimed ones.  Before
+    the warm-up the same work runs for SETTLE_S seconds of wall time: after
+    an idle spell the chip's clocks take ~20 launches of the largest GEMM
+    (2.1 -> 1.6 ms each, ~35 ms) to reach their sustained level, which a few
+    warm-up steps do not cover."""
+    SETTLE_S = 0.25
+
     def __init__(self, torch):
         self.torch = torch
 
     def time(self, fn, steps, warmup):
+        import time as _time
         torch = self.torch
+        t0 = _time.perf_counter()
+        n = 0
+        while True:
+            fn()
+            n += 1
+            if n % 4 == 0:
+                torch.cuda.synchronize()
+                if _time.perf_counter() - t0 >= self.SETTLE_S:
+                    break
         for _ in range(warmup):
             fn()
         torch.cuda.synchronize()
