@@ -248,8 +248,10 @@ class Timer:
     the warm-up the same work runs for SETTLE_S seconds of wall time: after
     an idle spell the chip's clocks take ~20 launches of the largest GEMM
     (2.1 -> 1.6 ms each, ~35 ms) to reach their sustained level, which a few
-    warm-up steps do not cover."""
-    SETTLE_S = 0.25
+    warm-up steps do not cover.  (BENCH_SETTLE_S overrides the 0.25 s, e.g.
+    0 for counter-collection runs, whose per-dispatch counts do not depend on
+    the clock.)"""
+    SETTLE_S = float(os.environ.get("BENCH_SETTLE_S", "0.25"))
 
     def __init__(self, torch):
         self.torch = torch
