@@ -362,8 +362,9 @@ __global__ __launch_bounds__((Tiling<BM, BN, WM, WN, BK, S, BX4>::kThreads)) voi
   constexpr bool kGlu = EP == Epilogue::kGluF32;
   // Plain outputs (dequantised or raw int32) leave through LDS as whole row
   // segments (below); the GLU and affine epilogues, whose output rows are
-  // half as wide or whose launches are a single round, measured faster with
-  // direct 16-byte stores, and N % 4 != 0 takes per-element stores.
+  // half as wide or whose launches are a single round, measured no faster
+  // that way and keep direct 16-byte stores, and N % 4 != 0 takes
+  // per-element stores.
   constexpr bool kStaged = BX4 && (EP == Epilogue::kDequantF32 || EP == Epilogue::kRawI32);
   if constexpr (!kStaged) {
     const int ow = kGlu ? N / 2 : N;  // output row length
@@ -393,44 +394,40 @@ __global__ __launch_bounds__((Tiling<BM, BN, WM, WN, BK, S, BX4>::kThreads)) voi
       }
     }
   } else {
-    // The tile leaves through LDS (the ring is free now) in chunks of 16
-    // rows, two chunk buffers in turn: the waves holding the chunk's rows
-    // write their outputs there, and after an LDS-only barrier every thread
-    // stores 16-byte pieces of whole rows, so one store instruction of a wave
-    // covers 1 KB of a row instead of 16 rows x 64 bytes.  Rows past M and
-    // columns past N fall outside the buffer's range or are sent there
-    // explicitly.
-    constexpr int OW = kGlu ? BN / 2 : BN;   // output columns of the tile
-    constexpr int OF = kGlu ? FN / 2 : FN;   // 16-column output blocks of a wave
-    constexpr int kRowB = OW * 4 + 16;       // staged row, padded by 16 bytes
-    constexpr int kChunkB = 16 * kRowB;
-    constexpr int kPieces = 16 * OW / 4;     // 16-byte pieces per chunk
-    static_assert(!kGlu || FN % 2 == 0, "GLU output needs whole 16-column block pairs");
-    static_assert(2 * kChunkB <= S * T::kStageBytes, "two staged chunks fit the ring");
-    static_assert(kPieces % T::kThreads == 0, "whole pieces per thread");
-    const int ow = kGlu ? N / 2 : N;         // output row length
-    const int c0 = kGlu ? n0 / 2 : n0;       // the tile's first output column
+    // Each wave's outputs leave through a private LDS buffer (the ring is
+    // free now), 16 rows at a time: the wave writes its 16 x WN block as it
+    // holds it (lane (g, l16): row l16, four columns of each 16-column block)
+    // and reads it back as four store instructions of 4 rows x WN columns,
+    // each row a contiguous 4 WN-byte segment.  Only the wave itself touches
+    // its buffer, so no workgroup barrier is needed, and one buffer serves
+    // every group of 16 rows: a wave's LDS operations are processed in issue
+    // order, so the next group's writes land after this group's reads.  Rows
+    // past M and columns past N fall outside the buffer's range or are sent
+    // there explicitly.
+    static_assert(WN == 64 && FN == 4, "a wave's row segment is 64 columns");
+    constexpr int kRowB = WN * 4 + 16;       // staged row, padded by 16 bytes
+    constexpr int kBufB = 16 * kRowB;
+    static_assert(kBufB * T::kWaves <= S * T::kStageBytes, "a buffer per wave fits the ring");
+    const int ow = N;
     const uint32_t out_bytes = static_cast<uint32_t>(M) * static_cast<uint32_t>(ow) * 4u;
     const __amdgpu_buffer_rsrc_t orsrc =
         __builtin_amdgcn_make_buffer_rsrc(out, 0, static_cast<int>(out_bytes), kBufferFlags);
+    char* const buf = smem + wave * kBufB;
+    const int rr = lane >> 4, qq = lane & 15;  // read-back lane: row rr of 4, column quad qq
+    const int n = n0 + wn * WN + 4 * qq;
 #pragma unroll
-    for (int c = 0; c < BM / 16; ++c) {
-      char* buf = smem + (c & 1) * kChunkB;
-      if (wm == c / FM) {  // wave-uniform: this wave holds the chunk's rows
+    for (int fm = 0; fm < FM; ++fm) {
 #pragma unroll
-        for (int f = 0; f < OF; ++f)
-          *reinterpret_cast<v4i*>(buf + l16 * kRowB + (wn * (WN / (FN / OF)) + f * 16 + 4 * g) * 4) =
-              outputs(c % FM, f);
-      }
-      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
-      __builtin_amdgcn_s_barrier();
-      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+      for (int f = 0; f < FN; ++f)
+        *reinterpret_cast<v4i*>(buf + l16 * kRowB + (f * 16 + 4 * g) * 4) = outputs(fm, f);
+      // the wave's own writes, complete before it reads them back
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront", "local");
+      __builtin_amdgcn_s_waitcnt(MMF_WAIT_LGKM0);
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront", "local");
 #pragma unroll
-      for (int i = 0; i < kPieces / T::kThreads; ++i) {
-        const int p = i * T::kThreads + tid;
-        const int r = p / (OW / 4), q4 = p % (OW / 4);
-        const v4i v = *reinterpret_cast<const v4i*>(buf + r * kRowB + q4 * 16);
-        const int m = m0 + c * 16 + r, n = c0 + 4 * q4;
+      for (int i = 0; i < 4; ++i) {
+        const v4i v = *reinterpret_cast<const v4i*>(buf + (4 * i + rr) * kRowB + qq * 16);
+        const int m = m0 + wm * WM + fm * 16 + 4 * i + rr;
         const uint32_t off =
             (m < M && n < ow) ? (static_cast<uint32_t>(m) * static_cast<uint32_t>(ow) + static_cast<uint32_t>(n)) * 4u
                               : kOut;

@@ -41,6 +41,8 @@ __device__ __forceinline__ void tile_coords(int64_t b, int64_t tiles_m, int64_t 
 // wait on LDS (lgkmcnt field at its maximum).
 #define MMF_WAIT_VM(n) (((n) & 0xF) | (0x7 << 4) | (0xF << 8) | ((((n) >> 4) & 3) << 14))
 #define MMF_WAIT_VM_LGKM0(n) (((n) & 0xF) | (0x7 << 4) | ((((n) >> 4) & 3) << 14))
+// LDS / scalar memory counter only (vmcnt and expcnt at their maxima)
+#define MMF_WAIT_LGKM0 (0xF | (0x7 << 4) | (0x3 << 14))
 
 // Chunk swizzle of 128-byte LDS rows (8 chunks of 16 bytes per row): row r
 // stores logical chunk c in slot c ^ swz(r).  Sixteen consecutive rows at one
