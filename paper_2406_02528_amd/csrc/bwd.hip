@@ -13,22 +13,26 @@ constexpr int kBlock = 256;
 
 unsigned blocks_for(int64_t threads) { return static_cast<unsigned>((threads + kBlock - 1) / kBlock); }
 
-// out[c] = sum of partials [nparts][cols] over p: 32 columns per workgroup,
-// 8 lanes per column over the partials, then the lanes in a fixed order.
+// out[c] = sum of partials [nparts][cols] over p: 8 columns per workgroup,
+// 32 lanes per column, lane l taking the partials l, l + 32, ... (their loads
+// issued together), then the 32 lane sums of a column added in lane order.
+// Both orders are fixed, so the result is the same bits on every call.
 __global__ __launch_bounds__(kBlock) void col_final_kernel(const double* partials, int64_t nparts, int64_t cols,
                                                            float* out) {
-  constexpr int kCols = 32, kLanes = kBlock / kCols;
-  __shared__ double red[kLanes][kCols];
+  constexpr int kCols = 8, kLanes = kBlock / kCols;
+  __shared__ double red[kCols][kLanes + 1];
   const int c = threadIdx.x % kCols, l = threadIdx.x / kCols;
   const int64_t col = static_cast<int64_t>(blockIdx.x) * kCols + c;
   double acc = 0.0;
-  if (col < cols)
+  if (col < cols) {
+#pragma unroll 4
     for (int64_t p = l; p < nparts; p += kLanes) acc += partials[p * cols + col];
-  red[l][c] = acc;
+  }
+  red[c][l] = acc;
   __syncthreads();
   if (l == 0 && col < cols) {
     double s = 0.0;
-    for (int i = 0; i < kLanes; ++i) s += red[i][c];
+    for (int i = 0; i < kLanes; ++i) s += red[c][i];
     out[col] = static_cast<float>(s);
   }
 }
@@ -46,7 +50,7 @@ __global__ __launch_bounds__(kBlock) void sum_parts_kernel(const float* parts, i
 
 hipError_t launch_col_final(const double* partials, int64_t nparts, int64_t cols, float* out, hipStream_t stream) {
   if (cols == 0) return hipSuccess;
-  hipLaunchKernelGGL(col_final_kernel, dim3(static_cast<unsigned>((cols + 31) / 32)), dim3(kBlock), 0, stream,
+  hipLaunchKernelGGL(col_final_kernel, dim3(static_cast<unsigned>((cols + 7) / 8)), dim3(kBlock), 0, stream,
                      partials, nparts, cols, out);
   return hipGetLastError();
 }
