@@ -349,6 +349,16 @@ __global__ __launch_bounds__(dyk::kThreads) void dy_kernel(
 #pragma unroll
     for (int e = 0; e < 4; ++e) dgp[f][e] = 0.0;
   double* red = reinterpret_cast<double*>(smem);  // [kWaves][4][BM]
+  // r g leaves through a private LDS buffer per wave after the row sums'
+  // region, 16 rows at a time: written as the lane holds it (row l16, four
+  // columns of each 16-column block), read back as four store instructions
+  // of 4 rows x 256 contiguous bytes (one wave's LDS operations complete in
+  // issue order, so no barrier and one buffer for every row group)
+  constexpr int kRgRow = WN * 4 + 16;
+  static_assert(kWaves * 4 * BM * 8 + kWaves * 16 * kRgRow <= S * kStageBytes, "row sums and staging fit the ring");
+  char* const sbuf = smem + kWaves * 4 * BM * 8 + wn * 16 * kRgRow;
+  const int rr = lane >> 4, qq = lane & 15;
+  const int kq = k0 + wn * WN + 4 * qq;  // read-back lane's four columns
 #pragma unroll
   for (int fm = 0; fm < FM; ++fm) {
     const int lr = fm * 16 + l16;
@@ -360,10 +370,10 @@ __global__ __launch_bounds__(dyk::kThreads) void dy_kernel(
 #pragma unroll
     for (int f = 0; f < FN; ++f) {
       const int k = k0 + wn * WN + f * 16 + 4 * g;
+      float o[4] = {0.0f, 0.0f, 0.0f, 0.0f};
       if (row_ok && k < K) {
         float xv[4];
         X4<XT>::load(x + static_cast<int64_t>(m) * K + k, xv);
-        float o[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const float dy = w2 * acc[fm][f][e];
@@ -372,10 +382,20 @@ __global__ __launch_bounds__(dyk::kThreads) void dy_kernel(
           sp += static_cast<double>(gk) * static_cast<double>(xv[e]);
           dgp[f][e] += static_cast<double>(dy) * static_cast<double>(xv[e]) * rd;
         }
-        *reinterpret_cast<float4*>(rg + static_cast<int64_t>(m) * K + k) = make_float4(o[0], o[1], o[2], o[3]);
       }
+      *reinterpret_cast<float4*>(sbuf + l16 * kRgRow + (f * 16 + 4 * g) * 4) = make_float4(o[0], o[1], o[2], o[3]);
     }
     red[(wn * 4 + g) * BM + lr] = sp;
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront", "local");
+    __builtin_amdgcn_s_waitcnt(MMF_WAIT_LGKM0);
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront", "local");
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int row = 4 * i + rr;
+      const float4 v = *reinterpret_cast<const float4*>(sbuf + row * kRgRow + qq * 16);
+      const int mr = m0 + fm * 16 + row;
+      if (mr < M && kq < K) *reinterpret_cast<float4*>(rg + static_cast<int64_t>(mr) * K + kq) = v;
+    }
   }
   if (dg_part != nullptr) {
 #pragma unroll
