@@ -752,15 +752,39 @@ __global__ __launch_bounds__(dwk::kThreads) void dw_kernel(const uint16_t* __res
 #pragma unroll
         for (int f = 0; f < FN; ++f) *reinterpret_cast<v4f*>(dst + (fm * FN + f) * (4 * kThreads)) = acc[fm][f];
     } else {
+      // the tile leaves through a private LDS buffer per wave in the ring
+      // (every wave is past the ring's last stage after the barrier), 16
+      // output features at a time: written as the lane holds them (feature
+      // l16, four input features of each 16-wide block), read back as four
+      // store instructions of 4 features x 256 contiguous bytes (one wave's
+      // LDS operations complete in issue order: no further barrier)
+      constexpr int kRow = WK * 4 + 16;
+      static_assert(kWaves * 16 * kRow <= S * kStageBytes, "the staging buffers fit the ring");
+      __builtin_amdgcn_s_barrier();
+      char* const sbuf = smem + wave * 16 * kRow;
       const uint32_t out_bytes = static_cast<uint32_t>(N) * static_cast<uint32_t>(K) * 4u;
       const __amdgpu_buffer_rsrc_t orsrc =
           __builtin_amdgcn_make_buffer_rsrc(out, 0, static_cast<int>(out_bytes), kBufferFlags);
+      const int rr = lane >> 4, qq = lane & 15;
+      const int kq = k0 + wk * WK + 4 * qq;
 #pragma unroll
-      for (int fm = 0; fm < FM; ++fm)
+      for (int fm = 0; fm < FM; ++fm) {
 #pragma unroll
         for (int f = 0; f < FN; ++f)
-          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4i, acc[fm][f]), orsrc,
-                                                 dw_out_off(n0, k0, tid, fm, f, N, K), 0, 0);
+          *reinterpret_cast<v4f*>(sbuf + l16 * kRow + (f * 16 + 4 * g) * 4) = acc[fm][f];
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront", "local");
+        __builtin_amdgcn_s_waitcnt(MMF_WAIT_LGKM0);
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront", "local");
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const v4i v = *reinterpret_cast<const v4i*>(sbuf + (4 * i + rr) * kRow + qq * 16);
+          const int n = n0 + wn * WN + fm * 16 + 4 * i + rr;
+          const uint32_t off = (n < N && kq < K)
+                                   ? (static_cast<uint32_t>(n) * static_cast<uint32_t>(K) + static_cast<uint32_t>(kq)) * 4u
+                                   : kOutOfRange;
+          __builtin_amdgcn_raw_buffer_store_b128(v, orsrc, off, 0, 0);
+        }
+      }
     }
   }
 }
