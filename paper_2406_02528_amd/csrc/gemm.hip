@@ -19,6 +19,13 @@
 // 64 x 256 tiles instead (waves of 64 x 64 or 32 x 64), whichever finishes
 // first by the rule of gemm_tile_choice: a lone tile's k loop is latency-
 // bound, so more, smaller tiles on more CUs beat a few wide ones.
+// Where the wide tile is chosen, K <= 4096 and the epilogue is not the
+// affine one, the same area is covered by two 128 x 256 workgroups of 4
+// waves per CU instead (75 KB of LDS each, the same 128 x 64 per wave): a
+// tile's output stores, which otherwise run after its k loop with the matrix
+// cores idle, then overlap the other workgroup's k loop.  The narrower tile moves 1.5x the operand bytes per MAC, a cost
+// that grows with K while the store time it hides does not, so at larger K
+// the single wide tile stays ahead.
 //
 // Operands and pipeline:
 //  - The operands of one BK = 128 deep k stage stream through a 3-slot LDS
@@ -82,8 +89,12 @@ struct Tiling {
   static_assert(BK == 128, "A swizzle is for 8 chunks per row");
 };
 
+// Two waves per SIMD whatever the workgroup size: a 4-wave workgroup left to
+// itself would take up to 512 registers per lane and keep a second workgroup
+// off its CU.
 template <int BM, int BN, int WM, int WN, int BK, int S, bool BX4, Epilogue EP>
-__global__ __launch_bounds__((Tiling<BM, BN, WM, WN, BK, S, BX4>::kThreads)) void gemm_kernel(
+__global__ __launch_bounds__((Tiling<BM, BN, WM, WN, BK, S, BX4>::kThreads))
+__attribute__((amdgpu_waves_per_eu(2))) void gemm_kernel(
     const int8_t* __restrict__ q, const float* __restrict__ a_scale,
     const int32_t* __restrict__ q_rowsum, const uint32_t* __restrict__ Wp,
     const float* __restrict__ w_scale, void* __restrict__ out, int M, int K, int N, const Affine aff) {
@@ -107,12 +118,18 @@ __global__ __launch_bounds__((Tiling<BM, BN, WM, WN, BK, S, BX4>::kThreads)) voi
 
   // Per-lane source offsets of this wave's LDS-DMA loads (k0 added per stage).
   // A instruction i covers rows 8 (wave * kAPerWave + i) .. + 7; the lane's
-  // LDS slot s holds the row's logical chunk s ^ swz(row).
+  // LDS slot s holds the row's logical chunk s ^ swz(row).  Instruction i + 2
+  // reads the rows 16 below instruction i's, and the swizzle repeats every 16
+  // rows, so only the first two instructions' offsets are kept (16 K is added
+  // per pair after them): with four A loads per wave, four kept offsets push
+  // the register count past 256 and spill inside the k loop.
   constexpr int kRowsPerInstr = 1024 / BK;
-  uint32_t a_src[T::kAPerWave];
-  int a_chunk[T::kAPerWave];
+  static_assert(kRowsPerInstr == 8, "two A loads per 16-row swizzle period");
+  constexpr int kA2 = T::kAPerWave < 2 ? T::kAPerWave : 2;
+  uint32_t a_src[kA2];
+  int a_chunk[kA2];
 #pragma unroll
-  for (int i = 0; i < T::kAPerWave; ++i) {
+  for (int i = 0; i < kA2; ++i) {
     const int r = (wave * T::kAPerWave + i) * kRowsPerInstr + lane / T::kChunks;
     const int c = (lane % T::kChunks) ^ a_swz(r);
     a_chunk[i] = c * 16;
@@ -162,7 +179,10 @@ __global__ __launch_bounds__((Tiling<BM, BN, WM, WN, BK, S, BX4>::kThreads)) voi
     const uint32_t base = lds0 + static_cast<uint32_t>(slot * T::kStageBytes);
     const int k0 = kt * BK;
     if (i < T::kAPerWave) {
-      const uint32_t off = (k0 + a_chunk[i] < K) ? a_src[i] + static_cast<uint32_t>(k0) : 0x80000000u;
+      const uint32_t off = (k0 + a_chunk[i & 1] < K)
+                               ? a_src[i & 1] + static_cast<uint32_t>(k0) +
+                                     static_cast<uint32_t>((i >> 1) * 16) * static_cast<uint32_t>(K)
+                               : 0x80000000u;
       const uint32_t dst = __builtin_amdgcn_readfirstlane(base + (wave * T::kAPerWave + i) * 1024);
       asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
                    :
@@ -453,7 +473,9 @@ hipError_t launch_cfg(const ContractArgs& a, int64_t m_begin, int64_t m_rows, hi
                        static_cast<void*>(static_cast<float*>(a.out) + m_begin * a.N),
                        static_cast<int>(m_rows), a.K, static_cast<int>(a.N), a.affine);
   else if (a.epilogue == Epilogue::kAffineF32) {
-    if constexpr (BX4)
+    // not built for the paired 128 x 256 tile, which launch_gemm does not use
+    // for this epilogue
+    if constexpr (BX4 && T::kWaves == 8)
       hipLaunchKernelGGL((gemm_kernel<BM, BN, WM, WN, BK, S, true, Epilogue::kAffineF32>), grid, block, 0,
                          stream, q, as, rs, a.Wpacked, a.w_scale,
                          static_cast<void*>(static_cast<float*>(a.out) + m_begin * a.N),
@@ -477,6 +499,14 @@ hipError_t launch_cfg(const ContractArgs& a, int64_t m_begin, int64_t m_rows, hi
 }
 
 }  // namespace
+
+// The wide tile's area as two 128 x 256 workgroups per CU up to this depth
+// (measured at M = 8192-16384: level or faster at K = 1024-4096 with the
+// dequantising and GLU epilogues, up to 1 % slower at K = 5120 with large N).
+// The affine epilogue keeps the wide tile: its paired form needs more than
+// 256 registers inside the k loop and measured 3 % slower on the MLGRU gate
+// projection (2048 x 2048 x 6144).
+constexpr int kPairedTileMaxK = 4096;
 
 int gemm_tile_choice(int64_t rows, int64_t N, int cus) {
   // Estimated time = rounds of workgroups over the CUs x the time of one
@@ -516,7 +546,9 @@ hipError_t launch_gemm(const ContractArgs& a, hipStream_t stream) {
     const hipError_t e = choice < 0  ? launch_cfg<256, 256, 128, 64, 128, 3, false>(a, m0, rows, stream)
                          : choice == 1 ? launch_cfg<64, 512, 64, 64, 128, 3, true>(a, m0, rows, stream)
                          : choice == 2 ? launch_cfg<64, 256, 32, 64, 128, 3, true>(a, m0, rows, stream)
-                                       : launch_cfg<128, 512, 128, 64, 128, 3, true>(a, m0, rows, stream);
+                         : (a.K <= kPairedTileMaxK && a.epilogue != Epilogue::kAffineF32)
+                             ? launch_cfg<128, 256, 128, 64, 128, 3, true>(a, m0, rows, stream)
+                             : launch_cfg<128, 512, 128, 64, 128, 3, true>(a, m0, rows, stream);
     if (e != hipSuccess) return e;
   }
   return hipSuccess;
