@@ -62,6 +62,15 @@ namespace {
 
 // BX4: B rows are copied 16 bytes per lane (one word row per instruction),
 // which needs N % 4 == 0 for aligned rows; otherwise 4 bytes per lane.
+// The lane's index in its wave, computed afresh and hidden from the
+// optimiser: values derived from it after a k loop that takes every register
+// are then recomputed there instead of being kept (spilled) across the loop.
+__device__ __forceinline__ int fresh_lane_id() {
+  int l = static_cast<int>(__builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u)));
+  asm volatile("" : "+v"(l));
+  return l;
+}
+
 template <int BM, int BN, int WM, int WN, int BK, int S, bool BX4>
 struct Tiling {
   static constexpr int kWavesM = BM / WM, kWavesN = BN / WN;
@@ -128,33 +137,64 @@ __attribute__((amdgpu_waves_per_eu(2))) void gemm_kernel(
   constexpr int kA2 = T::kAPerWave < 2 ? T::kAPerWave : 2;
   uint32_t a_src[kA2];
   int a_chunk[kA2];
-#pragma unroll
-  for (int i = 0; i < kA2; ++i) {
-    const int r = (wave * T::kAPerWave + i) * kRowsPerInstr + lane / T::kChunks;
-    const int c = (lane % T::kChunks) ^ a_swz(r);
-    a_chunk[i] = c * 16;
-    a_src[i] = static_cast<uint32_t>(m0 + r) * static_cast<uint32_t>(K) + static_cast<uint32_t>(c * 16);
-  }
   // B instruction i: word row jj, a 256-word (BX4) or 64-word chunk of this
   // tile's columns.  Columns past N read the next word row or zero; their
   // outputs are dropped.
   uint32_t b_src[T::kBPerWave];
   int b_jj[T::kBPerWave], b_dst[T::kBPerWave];
+  // The 4-wave tile's k loop takes all 256 registers.  There the offsets are
+  // set from the lane index by set_offsets, again from a fresh lane index for
+  // the stages after the last whole period, and the epilogue derives its
+  // lane coordinates afresh too, so that nothing lane-derived is kept
+  // (spilled) across the loop.  The 8-wave tiles set the same offsets inline
+  // once, the form the register allocator handles best for them (through
+  // set_offsets, without the second call, they spill).
+  constexpr bool kFreshLane = T::kWaves == 4;
+  static_assert(!kFreshLane || BX4, "the 4-wave tile copies B 16 bytes per lane");
+  auto set_offsets = [&](int ln) {
 #pragma unroll
-  for (int i = 0; i < T::kBPerWave; ++i) {
-    const int idx = wave * T::kBPerWave + i;
-    if constexpr (BX4) {
+    for (int i = 0; i < kA2; ++i) {
+      const int r = (wave * T::kAPerWave + i) * kRowsPerInstr + ln / T::kChunks;
+      const int c = (ln % T::kChunks) ^ a_swz(r);
+      a_chunk[i] = c * 16;
+      a_src[i] = static_cast<uint32_t>(m0 + r) * static_cast<uint32_t>(K) + static_cast<uint32_t>(c * 16);
+    }
+#pragma unroll
+    for (int i = 0; i < T::kBPerWave; ++i) {
+      const int idx = wave * T::kBPerWave + i;
       const int jj = idx / (BN / 256), q256 = idx % (BN / 256);
       b_jj[i] = jj;
       b_dst[i] = jj * T::kBRow * 4 + q256 * 1024;
       b_src[i] = 4u * (static_cast<uint32_t>(jj) * static_cast<uint32_t>(N) +
-                       static_cast<uint32_t>(n0 + q256 * 256 + 4 * lane));
-    } else {
-      const int jj = idx / (BN / 64), q64 = idx % (BN / 64);
-      b_jj[i] = jj;
-      b_dst[i] = jj * T::kBRow * 4 + q64 * 256;
-      b_src[i] = 4u * (static_cast<uint32_t>(jj) * static_cast<uint32_t>(N) +
-                       static_cast<uint32_t>(n0 + q64 * 64 + lane));
+                       static_cast<uint32_t>(n0 + q256 * 256 + 4 * ln));
+    }
+  };
+  if constexpr (kFreshLane) {
+    set_offsets(lane);
+  } else {
+#pragma unroll
+    for (int i = 0; i < kA2; ++i) {
+      const int r = (wave * T::kAPerWave + i) * kRowsPerInstr + lane / T::kChunks;
+      const int c = (lane % T::kChunks) ^ a_swz(r);
+      a_chunk[i] = c * 16;
+      a_src[i] = static_cast<uint32_t>(m0 + r) * static_cast<uint32_t>(K) + static_cast<uint32_t>(c * 16);
+    }
+#pragma unroll
+    for (int i = 0; i < T::kBPerWave; ++i) {
+      const int idx = wave * T::kBPerWave + i;
+      if constexpr (BX4) {
+        const int jj = idx / (BN / 256), q256 = idx % (BN / 256);
+        b_jj[i] = jj;
+        b_dst[i] = jj * T::kBRow * 4 + q256 * 1024;
+        b_src[i] = 4u * (static_cast<uint32_t>(jj) * static_cast<uint32_t>(N) +
+                         static_cast<uint32_t>(n0 + q256 * 256 + 4 * lane));
+      } else {
+        const int jj = idx / (BN / 64), q64 = idx % (BN / 64);
+        b_jj[i] = jj;
+        b_dst[i] = jj * T::kBRow * 4 + q64 * 256;
+        b_src[i] = 4u * (static_cast<uint32_t>(jj) * static_cast<uint32_t>(N) +
+                         static_cast<uint32_t>(n0 + q64 * 64 + lane));
+      }
     }
   }
   const uint32_t b_row = 4u * static_cast<uint32_t>(N);
@@ -322,6 +362,9 @@ __attribute__((amdgpu_waves_per_eu(2))) void gemm_kernel(
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) step(kt + j, ks, j, (j + 1) % S, be[ks % 2], be[(ks + 1) % 2]);
   }
+  if constexpr (kFreshLane) {
+    if (kt < KT) set_offsets(fresh_lane_id());
+  }
   for (; kt < KT; ++kt) {
     const int slot = kt % S;
 #pragma unroll
@@ -332,6 +375,8 @@ __attribute__((amdgpu_waves_per_eu(2))) void gemm_kernel(
 
   // ---- epilogue: the MFMA computed the transposed product, so lane
   // (g, l16) holds row l16 and columns 4 g .. 4 g + 3 of each 16 x 16 block ----
+  const int elane = kFreshLane ? fresh_lane_id() : lane;
+  const int el16 = elane & 15, eg = elane >> 4;
   const int* s_rsum = reinterpret_cast<const int*>(smem + S * T::kStageBytes);
   const float* s_scale = reinterpret_cast<const float*>(smem + S * T::kStageBytes + 4 * BM);
   const float ws = (EP == Epilogue::kDequantF32 || EP == Epilogue::kGluF32) ? w_scale[0] : 0.0f;
@@ -345,7 +390,7 @@ __attribute__((amdgpu_waves_per_eu(2))) void gemm_kernel(
     static_assert(BX4, "affine output needs N % 4 == 0");
 #pragma unroll
     for (int f = 0; f < FN; ++f) {
-      const int n = n0 + wn * WN + f * 16 + 4 * g;
+      const int n = n0 + wn * WN + f * 16 + 4 * eg;
       cf[f] = load_col_affine4(aff, w_scale, static_cast<uint32_t>(N), n < N ? static_cast<uint32_t>(n) : 0u);
     }
   }
@@ -353,7 +398,7 @@ __attribute__((amdgpu_waves_per_eu(2))) void gemm_kernel(
   // pair index: blocks 2f and 2f + 1 hold the same 16 channels, and lane
   // (g, l16) has channels 4 g .. 4 g + 3 of both).
   auto outputs = [&](int fm, int f) -> v4i {
-    const int lr = wm * WM + fm * 16 + l16;
+    const int lr = wm * WM + fm * 16 + el16;
     const int rs = s_rsum[lr];
     v4i v;
     if constexpr (EP == Epilogue::kGluF32) {
@@ -393,12 +438,12 @@ __attribute__((amdgpu_waves_per_eu(2))) void gemm_kernel(
         __builtin_amdgcn_make_buffer_rsrc(out, 0, static_cast<int>(out_bytes), kBufferFlags);
 #pragma unroll
     for (int fm = 0; fm < FM; ++fm) {
-      const int lr = wm * WM + fm * 16 + l16;
+      const int lr = wm * WM + fm * 16 + el16;
       const bool row_ok = m0 + lr < M;
       const uint32_t row_bytes = static_cast<uint32_t>(m0 + lr) * static_cast<uint32_t>(ow) * 4u;
 #pragma unroll
       for (int f = 0; f < (kGlu ? FN / 2 : FN); ++f) {
-        const int n = (kGlu ? (n0 + wn * WN) / 2 : n0 + wn * WN) + f * 16 + 4 * g;
+        const int n = (kGlu ? (n0 + wn * WN) / 2 : n0 + wn * WN) + f * 16 + 4 * eg;
         const v4i v = outputs(fm, f);
         if constexpr (BX4) {
           // N % 4 == 0 (and L % 16 == 0): the four columns are all inside or all past the row
@@ -433,13 +478,13 @@ __attribute__((amdgpu_waves_per_eu(2))) void gemm_kernel(
     const __amdgpu_buffer_rsrc_t orsrc =
         __builtin_amdgcn_make_buffer_rsrc(out, 0, static_cast<int>(out_bytes), kBufferFlags);
     char* const buf = smem + wave * kBufB;
-    const int rr = lane >> 4, qq = lane & 15;  // read-back lane: row rr of 4, column quad qq
+    const int rr = elane >> 4, qq = elane & 15;  // read-back lane: row rr of 4, column quad qq
     const int n = n0 + wn * WN + 4 * qq;
 #pragma unroll
     for (int fm = 0; fm < FM; ++fm) {
 #pragma unroll
       for (int f = 0; f < FN; ++f)
-        *reinterpret_cast<v4i*>(buf + l16 * kRowB + (f * 16 + 4 * g) * 4) = outputs(fm, f);
+        *reinterpret_cast<v4i*>(buf + el16 * kRowB + (f * 16 + 4 * eg) * 4) = outputs(fm, f);
       // the wave's own writes, complete before it reads them back
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront", "local");
       __builtin_amdgcn_s_waitcnt(MMF_WAIT_LGKM0);
