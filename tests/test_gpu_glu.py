@@ -79,6 +79,31 @@ def gpu_pack(mmf, W_g, W_u, joint: bool):
     return Wgu, w_scales, t_g, t_u, ws_g, ws_u
 
 
+def test_glu_paired_tiles_ragged(mmf):
+    """A shape whose GLU contraction runs as two 128 x 256 workgroups per CU
+    (144 wide tiles at K <= 4096), ragged in every dimension: 1100 = 8 * 128
+    + 76 tokens, 2 L = 8000 = 31 * 256 + 64 interleaved columns, K = 528 = 4 *
+    128 + 16 (a whole ring period and a partial stage after it)."""
+    M, K, L = 1100, 528, 4000
+    rs = np.random.default_rng(2400)
+    bits, xf, g, W = workloads.random_case(rs, M, K, 2 * L)
+    log(f"[glu paired tiles] M={M} K={K} L={L}")
+    Wgu, w_scales, t_g, t_u, ws_g, ws_u = gpu_pack(mmf, W[:L], W[L:], False)
+    ref = oracle.glu_fwd(xf, g, t_g, ws_g, t_u, ws_u)
+    case = Case(bits, xf, g, W, "")
+    case.upload()
+    q = torch.empty((M, K), dtype=torch.int8, device=dev())
+    a = torch.empty((M,), dtype=torch.float32, device=dev())
+    mmf.mmf_act_quant(case.x_d, case.g_d, q, a)
+    p = torch.full((M, L), float("nan"), dtype=torch.float32, device=dev())
+    mmf.mmf_glu_fwd(case.x_d, case.g_d, Wgu, w_scales, p)
+    torch.cuda.synchronize()
+    flip_rows, _ = compare_q(q.cpu().numpy(), ref["q"])
+    flip = np.zeros(M, bool)
+    flip[flip_rows] = True
+    compare_p(p.cpu().numpy(), ref["p"], ref["acc_g"], ref["acc_u"], flip)
+
+
 @pytest.mark.parametrize("M", [1, 8, 17, 300])
 def test_glu_random_shapes(mmf, M):
     rs = np.random.default_rng(2000 + M)
