@@ -19,9 +19,10 @@
 // 64 x 256 tiles instead (waves of 64 x 64 or 32 x 64), whichever finishes
 // first by the rule of gemm_tile_choice: a lone tile's k loop is latency-
 // bound, so more, smaller tiles on more CUs beat a few wide ones.
-// Where the wide tile is chosen, K <= 4096 and the epilogue is not the
-// affine one, the same area is covered by two 128 x 256 workgroups of 4
-// waves per CU instead (75 KB of LDS each, the same 128 x 64 per wave): a
+// Where the wide tile is chosen, K <= 4096, the epilogue is not the affine
+// one and the wide tiles fill more than one round of the CUs (or most of one
+// at K <= 2048: gemm_paired), the same area is covered by two 128 x 256
+// workgroups of 4 waves per CU instead (75 KB of LDS each, the same 128 x 64 per wave): a
 // tile's output stores, which otherwise run after its k loop with the matrix
 // cores idle, then overlap the other workgroup's k loop.  The narrower tile moves 1.5x the operand bytes per MAC, a cost
 // that grows with K while the store time it hides does not, so at larger K
@@ -553,6 +554,19 @@ hipError_t launch_cfg(const ContractArgs& a, int64_t m_begin, int64_t m_rows, hi
 // projection (2048 x 2048 x 6144).
 constexpr int kPairedTileMaxK = 4096;
 
+// Whether the wide tiles of a problem run as paired 128 x 256 workgroups.
+// The pairs pay off once a CU has a next tile whose k loop can cover a
+// finished tile's stores, i.e. beyond one round of wide tiles (measured
+// 4-12 % faster at K = 1024-4096).  Within a single round they gain only at
+// small K on a nearly full round (K = 2048 with 192-256 wide tiles: 1-5 %)
+// and lose elsewhere (144 tiles at K = 1040: 5 % slower, 256 at K = 3072: 3 %).
+static bool gemm_paired(int64_t rows, int64_t N, int K, int cus, Epilogue ep) {
+  if (K > kPairedTileMaxK || ep == Epilogue::kAffineF32) return false;
+  const int64_t c = cus > 0 ? cus : 256;
+  const int64_t wide = ((rows + 127) / 128) * ((N + 511) / 512);
+  return wide > c || (K <= 2048 && 4 * wide >= 3 * c);
+}
+
 int gemm_tile_choice(int64_t rows, int64_t N, int cus) {
   // Estimated time = rounds of workgroups over the CUs x the time of one
   // tile's k loop when it runs alone, measured relative to each other at
@@ -591,7 +605,7 @@ hipError_t launch_gemm(const ContractArgs& a, hipStream_t stream) {
     const hipError_t e = choice < 0  ? launch_cfg<256, 256, 128, 64, 128, 3, false>(a, m0, rows, stream)
                          : choice == 1 ? launch_cfg<64, 512, 64, 64, 128, 3, true>(a, m0, rows, stream)
                          : choice == 2 ? launch_cfg<64, 256, 32, 64, 128, 3, true>(a, m0, rows, stream)
-                         : (a.K <= kPairedTileMaxK && a.epilogue != Epilogue::kAffineF32)
+                         : gemm_paired(rows, a.N, a.K, cus, a.epilogue)
                              ? launch_cfg<128, 256, 128, 64, 128, 3, true>(a, m0, rows, stream)
                              : launch_cfg<128, 512, 128, 64, 128, 3, true>(a, m0, rows, stream);
     if (e != hipSuccess) return e;

@@ -96,7 +96,9 @@ hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream);
 int device_cus();
 // Prefill kernel: int8 MFMA, any M.  The workgroup tile is 128 x 512, or
 // 64 x 512 / 64 x 256 when those finish a problem with few 128 x 512 tiles
-// sooner (gemm_tile_choice); 256 x 256 when N % 4 != 0.
+// sooner (gemm_tile_choice); 256 x 256 when N % 4 != 0.  Where 128 x 512 is
+// chosen at K <= 4096 it runs as two 128 x 256 workgroups per CU once its
+// tiles fill the CUs (except with the affine epilogue).
 hipError_t launch_gemm(const ContractArgs& a, hipStream_t stream);
 // Index of the tile shape launch_gemm uses for `rows` x N on `cus` compute
 // units (N % 4 == 0): 0 for 128 x 512, 1 for 64 x 512, 2 for 64 x 256.

@@ -81,10 +81,11 @@ def gpu_pack(mmf, W_g, W_u, joint: bool):
 
 def test_glu_paired_tiles_ragged(mmf):
     """A shape whose GLU contraction runs as two 128 x 256 workgroups per CU
-    (144 wide tiles at K <= 4096), ragged in every dimension: 1100 = 8 * 128
-    + 76 tokens, 2 L = 8000 = 31 * 256 + 64 interleaved columns, K = 528 = 4 *
-    128 + 16 (a whole ring period and a partial stage after it)."""
-    M, K, L = 1100, 528, 4000
+    (408 wide tiles, more than one round, at K <= 4096), ragged in every
+    dimension: 3000 = 23 * 128 + 56 tokens, 2 L = 8224 = 32 * 256 + 32
+    interleaved columns, K = 400 = 3 * 128 + 16 (a whole ring period, then a
+    partial stage with the offsets set afresh)."""
+    M, K, L = 3000, 400, 4112
     rs = np.random.default_rng(2400)
     bits, xf, g, W = workloads.random_case(rs, M, K, 2 * L)
     log(f"[glu paired tiles] M={M} K={K} L={L}")

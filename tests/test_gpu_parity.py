@@ -215,13 +215,14 @@ def test_random_shapes(mmf, M):
 # The MFMA kernel's tile shape follows the problem (on 256 compute units):
 # 64 x 256 tiles for a short M or a narrow N, 64 x 512 in between, 128 x 512
 # once the wide tiles fill the CUs, run as two 128 x 256 workgroups per CU at
-# K <= 4096 (the full-size workloads above take both forms).  Ragged in every
-# dimension (a partial last stage of K, partial row and column tiles).  The
-# automatic path sends 33-64 tokens to the MFMA kernel at K <= 2048 and to
-# decode launches of 16 tokens beyond.
+# K <= 4096 beyond one round of wide tiles (the full-size workloads above
+# take both forms).  Ragged in every dimension (a partial last stage of K,
+# partial row and column tiles).  The automatic path sends 33-64 tokens to
+# the MFMA kernel at K <= 2048 and to decode launches of 16 tokens beyond.
 @pytest.mark.parametrize("M,K,N", [(300, 1040, 2000),    # 64 x 256: 40 tiles
                                    (1000, 336, 6000),    # 64 x 512: 192 tiles
-                                   (1100, 528, 8000),    # 128 x 256 pairs: 288 tiles
+                                   (1100, 528, 8000),    # 128 x 512: 144 tiles, one round
+                                   (3000, 400, 8200),    # 128 x 256 pairs: 816 tiles
                                    (40, 2048, 1000),     # auto: MFMA kernel (64 x 256)
                                    (57, 2064, 1000)])    # auto: four decode launches
 def test_gemm_tile_shapes(mmf, M, K, N):
