@@ -22,11 +22,12 @@
 // Where the wide tile is chosen, K <= 4096, the epilogue is not the affine
 // one and the wide tiles fill more than one round of the CUs (or most of one
 // at K <= 2048: gemm_paired), the same area is covered by two 128 x 256
-// workgroups of 4 waves per CU instead (75 KB of LDS each, the same 128 x 64 per wave): a
-// tile's output stores, which otherwise run after its k loop with the matrix
-// cores idle, then overlap the other workgroup's k loop.  The narrower tile moves 1.5x the operand bytes per MAC, a cost
-// that grows with K while the store time it hides does not, so at larger K
-// the single wide tile stays ahead.
+// workgroups of 4 waves per CU instead (75 KB of LDS each, the same 128 x 64
+// per wave): a tile's output stores, which otherwise run after its k loop
+// with the matrix cores idle, then overlap the other workgroup's k loop.  The
+// narrower tile moves 1.5x the operand bytes per MAC, a cost that grows with
+// K while the store time it hides does not, so at larger K the single wide
+// tile stays ahead.
 //
 // Operands and pipeline:
 //  - The operands of one BK = 128 deep k stage stream through a 3-slot LDS
