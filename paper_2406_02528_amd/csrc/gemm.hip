@@ -303,6 +303,12 @@ __attribute__((amdgpu_waves_per_eu(2))) void gemm_kernel(
                  : "s"(dst), "v"(off), "s"(desc)
                  : "memory", "m0");
   }
+  // Paired tiles with the GLU epilogue: the k loop's waves issue ahead of the
+  // other workgroup's epilogue on the same SIMD (its SiLU arithmetic and
+  // direct stores), which keeps the matrix cores fed (glu_gate 4-5 % faster;
+  // the dequantising epilogue measured level and keeps the default).
+  constexpr bool kLoopPriority = T::kWaves == 4 && EP == Epilogue::kGluF32;
+  if constexpr (kLoopPriority) __builtin_amdgcn_s_setprio(1);
   // Prologue: stages 0 .. S-2, wait for stage 0 (and the row factors).
 #pragma unroll
   for (int p = 0; p < S - 1; ++p)
@@ -372,6 +378,7 @@ __attribute__((amdgpu_waves_per_eu(2))) void gemm_kernel(
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) step(kt, ks, slot, (slot + 1) % S, be[ks % 2], be[(ks + 1) % 2]);
   }
+  if constexpr (kLoopPriority) __builtin_amdgcn_s_setprio(0);
   // no LDS-DMA write may still be in flight when the workgroup's LDS is freed
   __builtin_amdgcn_s_waitcnt(MMF_WAIT_VM_LGKM0(0));
 
