@@ -414,6 +414,32 @@ int mmf_bitlinear_bwd(const uint16_t *dO, const void *x, int x_is_f32, const flo
 #define MMF_PATH_GEMM 2
 int mmf_set_path(int path);
 
+/*
+ * The workgroup tile of the prefill (MFMA) contraction for an M x K x N
+ * problem on `cus` compute units, as the library plans it for its launches
+ * (host only: no device call, nothing enqueued; for problems split into row
+ * slices by the 32-bit offset limit, the first slice's plan).  For callers
+ * sizing their own work and for tests that must know which kernel form a
+ * shape exercises.  `epilogue` is one of MMF_EPILOGUE_*; for the GLU, N is
+ * the interleaved width 2 L (a multiple of 32).  Returns one of MMF_TILE_*:
+ * 128 x 512 tiles with one 8-wave workgroup per CU; the same area as two
+ * 128 x 256 workgroups of 4 waves per CU (K <= 4096, not the affine
+ * epilogue, more than one round of wide tiles or most of one at K <= 2048);
+ * 64 x 512 or 64 x 256 tiles for problems with few wide tiles; 256 x 256
+ * when N % 4 != 0.  Errors as negative status: -MMF_ERR_SHAPE for a shape the
+ * contraction rejects or cus < 1, -MMF_ERR_ARG for an unknown epilogue.
+ */
+#define MMF_EPILOGUE_DEQUANT 0
+#define MMF_EPILOGUE_RAW_I32 1
+#define MMF_EPILOGUE_GLU 2
+#define MMF_EPILOGUE_AFFINE 3
+#define MMF_TILE_128x512 0
+#define MMF_TILE_128x256_PAIRED 1
+#define MMF_TILE_64x512 2
+#define MMF_TILE_64x256 3
+#define MMF_TILE_256x256 4
+int mmf_prefill_tile_plan(int64_t M, int64_t K, int64_t N, int epilogue, int cus);
+
 #ifdef __cplusplus
 }
 #endif

@@ -58,6 +58,8 @@ _SIGNATURES = {
     "mmf_ternary_gemm_dequant": ([_P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _P], ctypes.c_int),
     "mmf_ternary_gemm_i32": ([_P, _P, _P, _I64, _I64, _I64, _P], ctypes.c_int),
     "mmf_set_path": ([ctypes.c_int], ctypes.c_int),
+    "mmf_prefill_tile_plan": ([ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, ctypes.c_int, ctypes.c_int],
+                              ctypes.c_int),
     "mmf_glu_pack": ([_P, _P, _I64, _I64, _P, _P], ctypes.c_int),
     "mmf_glu_fwd": ([_P, _P, _P, _P, _P, _I64, _I64, _I64, _P], ctypes.c_int),
     "mmf_glu_fwd_f32": ([_P, _P, _P, _P, _P, _I64, _I64, _I64, _P], ctypes.c_int),
@@ -148,6 +150,18 @@ def mmf_set_path(path: int) -> int:
     if prev < 0:
         raise ValueError(f"unknown path {path}")
     return prev
+
+
+MMF_EPILOGUE_DEQUANT, MMF_EPILOGUE_RAW_I32, MMF_EPILOGUE_GLU, MMF_EPILOGUE_AFFINE = 0, 1, 2, 3
+TILE_PLANS = ("128x512", "128x256_paired", "64x512", "64x256", "256x256")
+
+
+def mmf_prefill_tile_plan(M: int, K: int, N: int, epilogue: int = MMF_EPILOGUE_DEQUANT, cus: int = 256) -> str:
+    """The prefill contraction's tile plan for M x K x N on `cus` compute
+    units (host only), as a name from TILE_PLANS."""
+    r = int(_lib.mmf_prefill_tile_plan(M, K, N, epilogue, cus))
+    _check(-r if r < 0 else 0)
+    return TILE_PLANS[r]
 
 
 def mmf_ternarize_weights(W: torch.Tensor, Wpacked: torch.Tensor, w_scale: torch.Tensor,

@@ -599,23 +599,31 @@ int gemm_tile_choice(int64_t rows, int64_t N, int cus) {
   return best;
 }
 
+int gemm_plan(int64_t rows, int K, int64_t N, Epilogue ep, int cus) {
+  if (N % 4 != 0) return kPlan256x256;
+  const int choice = gemm_tile_choice(rows, N, cus);
+  if (choice == 1) return kPlan64x512;
+  if (choice == 2) return kPlan64x256;
+  return gemm_paired(rows, N, K, cus, ep) ? kPlan128x256Paired : kPlan128x512;
+}
+
 hipError_t launch_gemm(const ContractArgs& a, hipStream_t stream) {
   // 32-bit buffer offsets: a launch covers at most 2^31 - 1 bytes of q, of
   // packed weights and of output; taller problems run in row slices.  The
   // C-ABI layer rejects shapes without a slice before enqueueing anything.
   const int64_t slice = gemm_row_slice(a.K, a.N);
   if (slice == 0) return hipErrorInvalidValue;
-  const bool bx4 = (a.N % 4) == 0;
   const int cus = device_cus();
   for (int64_t m0 = 0; m0 < a.M; m0 += slice) {
     const int64_t rows = a.M - m0 < slice ? a.M - m0 : slice;
-    const int choice = bx4 ? gemm_tile_choice(rows, a.N, cus) : -1;
-    const hipError_t e = choice < 0  ? launch_cfg<256, 256, 128, 64, 128, 3, false>(a, m0, rows, stream)
-                         : choice == 1 ? launch_cfg<64, 512, 64, 64, 128, 3, true>(a, m0, rows, stream)
-                         : choice == 2 ? launch_cfg<64, 256, 32, 64, 128, 3, true>(a, m0, rows, stream)
-                         : gemm_paired(rows, a.N, a.K, cus, a.epilogue)
-                             ? launch_cfg<128, 256, 128, 64, 128, 3, true>(a, m0, rows, stream)
-                             : launch_cfg<128, 512, 128, 64, 128, 3, true>(a, m0, rows, stream);
+    hipError_t e;
+    switch (gemm_plan(rows, a.K, a.N, a.epilogue, cus)) {
+      case kPlan256x256: e = launch_cfg<256, 256, 128, 64, 128, 3, false>(a, m0, rows, stream); break;
+      case kPlan64x512: e = launch_cfg<64, 512, 64, 64, 128, 3, true>(a, m0, rows, stream); break;
+      case kPlan64x256: e = launch_cfg<64, 256, 32, 64, 128, 3, true>(a, m0, rows, stream); break;
+      case kPlan128x256Paired: e = launch_cfg<128, 256, 128, 64, 128, 3, true>(a, m0, rows, stream); break;
+      default: e = launch_cfg<128, 512, 128, 64, 128, 3, true>(a, m0, rows, stream); break;
+    }
     if (e != hipSuccess) return e;
   }
   return hipSuccess;

@@ -885,4 +885,25 @@ int mmf_set_path(int path) {
   return g_path.exchange(path);
 }
 
+static_assert(mmf::kPlan128x512 == MMF_TILE_128x512 && mmf::kPlan128x256Paired == MMF_TILE_128x256_PAIRED &&
+                  mmf::kPlan64x512 == MMF_TILE_64x512 && mmf::kPlan64x256 == MMF_TILE_64x256 &&
+                  mmf::kPlan256x256 == MMF_TILE_256x256,
+              "tile plan values follow the header");
+
+int mmf_prefill_tile_plan(int64_t M, int64_t K, int64_t N, int epilogue, int cus) {
+  if (const int st = check_shape(M, K, N); st != MMF_OK) return -st;
+  if (M < 1 || N < 1 || cus < 1 || check_gemm(K, N) != MMF_OK) return -MMF_ERR_SHAPE;
+  mmf::Epilogue ep;
+  switch (epilogue) {
+    case MMF_EPILOGUE_DEQUANT: ep = mmf::Epilogue::kDequantF32; break;
+    case MMF_EPILOGUE_RAW_I32: ep = mmf::Epilogue::kRawI32; break;
+    case MMF_EPILOGUE_GLU: ep = mmf::Epilogue::kGluF32; break;
+    case MMF_EPILOGUE_AFFINE: ep = mmf::Epilogue::kAffineF32; break;
+    default: return -MMF_ERR_ARG;
+  }
+  if (ep == mmf::Epilogue::kGluF32 && N % 32 != 0) return -MMF_ERR_SHAPE;
+  const int64_t slice = mmf::gemm_row_slice(K, N);
+  return mmf::gemm_plan(M < slice ? M : slice, static_cast<int>(K), N, ep, cus);
+}
+
 }  // extern "C"

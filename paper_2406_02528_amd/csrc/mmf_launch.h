@@ -103,6 +103,10 @@ hipError_t launch_gemm(const ContractArgs& a, hipStream_t stream);
 // Index of the tile shape launch_gemm uses for `rows` x N on `cus` compute
 // units (N % 4 == 0): 0 for 128 x 512, 1 for 64 x 512, 2 for 64 x 256.
 int gemm_tile_choice(int64_t rows, int64_t N, int cus);
+// The tile plan launch_gemm follows for one launch of `rows` x K x N with
+// epilogue `ep` on `cus` compute units (the values of MMF_TILE_* in mmf.h).
+enum GemmPlan { kPlan128x512 = 0, kPlan128x256Paired = 1, kPlan64x512 = 2, kPlan64x256 = 3, kPlan256x256 = 4 };
+int gemm_plan(int64_t rows, int K, int64_t N, Epilogue ep, int cus);
 // Rows per launch of the MFMA kernel for K in-features and N out-features,
 // or 0 when the shape is beyond its 32-bit buffer offsets: the packed weights
 // must stay below 2^31 bytes, N at most 2^24, and a launch covers a slice of

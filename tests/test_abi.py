@@ -359,3 +359,36 @@ def test_noalloc_argument_checks(mmf):
     # 65536 tokens of 1040 features: 68 MB of q, past the 64 MiB array
     assert lib.mmf_bitlinear_fwd_noalloc(A, 0, B, C, D, E, 65536, 1040, 64, S) == 6
     assert lib.mmf_bitlinear_fwd_noalloc(A, 0, B, C, D, E, 65, 16, 1 << 21, S) == 2
+
+
+def test_prefill_tile_plan(mmf):
+    """The planner's choice on 256 compute units (host only): the parity shapes
+    take the kernel forms their tests name, and the workloads theirs."""
+    P = mmf.mmf_prefill_tile_plan
+    glu, affine, raw = mmf.MMF_EPILOGUE_GLU, mmf.MMF_EPILOGUE_AFFINE, mmf.MMF_EPILOGUE_RAW_I32
+    # tests/test_gpu_parity.py and tests/test_gpu_glu.py
+    assert P(300, 1040, 2000) == "64x256"
+    assert P(1000, 336, 6000) == "64x512"
+    assert P(1100, 528, 8000) == "128x512"              # one round of 144 wide tiles
+    assert P(3000, 400, 8200) == "128x256_paired"       # 408 wide tiles
+    assert P(3000, 400, 8200, raw) == "128x256_paired"
+    assert P(3000, 400, 2 * 4112, glu) == "128x256_paired"
+    assert P(37, 272, 300 + 2) == "256x256"             # N % 4 != 0
+    # workloads
+    assert P(16384, 5120, 27648) == "128x512"           # large: K > 4096
+    assert P(8192, 2048, 11264) == "128x256_paired"     # glu_up
+    assert P(8192, 2048, 11264, glu) == "128x256_paired"  # glu_gate
+    assert P(8192, 5632, 2048) == "128x512"             # glu_down: K > 4096
+    assert P(2048, 2048, 6144, affine) == "128x512"     # MLGRU gate projection: affine epilogue
+    assert P(2048, 2048, 2048) == "64x256"              # MLGRU output projection
+    assert P(16384, 1024, 1024) == "128x256_paired"     # training forward at d = 1024: a full round, K <= 2048
+    # a single round at K = 3072 keeps the wide tile; two rounds take the pairs
+    assert P(2048, 3072, 8192) == "128x512"
+    assert P(4096, 3072, 8192) == "128x256_paired"
+    # invalid arguments
+    for args in ((0, 16, 16, 0, 256), (16, 15, 16, 0, 256), (16, 16, 0, 0, 256), (16, 16, 16, 0, 0),
+                 (16, 16, 48, glu, 256)):
+        with pytest.raises(mmf.MMFError, match="MMF_ERR_SHAPE"):
+            P(*args)
+    with pytest.raises(mmf.MMFError):
+        P(16, 16, 16, 9, 256)
